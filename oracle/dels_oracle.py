@@ -1,0 +1,302 @@
+"""Plain CPU oracle for the DeLS-Spec block-drafting path.
+
+TEST INFRASTRUCTURE, NOT PRODUCT CODE.  Only the tests, the smoke check of the
+package entry point and the CPU-baseline leg of the benchmark may import this
+module.  It shares no code with the HIP library and imports nothing from it.
+
+Everything is computed in float64 with numpy, in the order the paper states:
+
+* fusion of long, short and prior logits        -- Sec. 4.3, fusion equation
+* DeLS-Spec inference over one draft block       -- Sec. 4.3, Algorithm 1
+* RNN local head (bias-free one-layer GRU on the frozen target embedding,
+  SiLU low-rank projection, vocabulary head)     -- App. A, RNN-head equation
+* Markov local head                               -- App. A, Markov-head equation
+* add-smoothing unigram log-prior                 -- App. A, prior estimation
+* acceptance length, tau and rate_i               -- Sec. 5.1; App. D
+
+Readings where the paper is silent (each is also listed in the design notes):
+
+* GRU gates follow the common (r, z, n) convention with the reset gate applied
+  to the recurrent part of the candidate, h' = (1 - z) * n + z * h, h_0 = 0.
+* Greedy decoding: the argmax takes the lowest index among equal values.  The
+  decision is taken on the fused logits rounded to float32 (the precision the
+  GPU path decides in); every reported value is float64.
+* The short-logit weight is the paper's alpha; a long-logit weight w_long
+  (1 in the paper) is kept so that w_long = 0 gives the local head alone.
+* Row j of the long logits is draft position j.  By default the head is seeded
+  with the last accepted token and every row is fused.  With
+  first_row_long_only=True row 0 is decoded from the long logits alone and the
+  head only sees drafted tokens (the literal form of Algorithm 1).
+* The acceptance length counts leading positions where draft == target
+  (0..B); the paper's tau adds the bonus token, tau = accepted + 1.
+
+Parity pins (tests/test_oracle_*.py): exact-rational brute force on tiny
+vocabularies, the alpha = 0 / w_long = 0 limits, shift invariance, a
+hand-worked three-position example, torch.nn.GRU equivalence and closed forms
+for the acceptance length.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Callable, Optional, Sequence
+
+import numpy as np
+
+F64 = np.float64
+
+
+# ----------------------------------------------------------------------------------------
+# elementary functions
+# ----------------------------------------------------------------------------------------
+def logsumexp(x: np.ndarray) -> float:
+    """log sum_v exp(x_v), by subtracting the maximum first."""
+    x = np.asarray(x, dtype=F64)
+    m = np.max(x)
+    if not np.isfinite(m):
+        return float(m)
+    return float(m + np.log(np.sum(np.exp(x - m))))
+
+
+def sigmoid(x):
+    return 1.0 / (1.0 + np.exp(-np.asarray(x, dtype=F64)))
+
+
+def silu(x):
+    x = np.asarray(x, dtype=F64)
+    return x * sigmoid(x)
+
+
+# ----------------------------------------------------------------------------------------
+# Sec. 4.3: logit fusion and greedy decoding of one row
+# ----------------------------------------------------------------------------------------
+@dataclasses.dataclass
+class RowResult:
+    token: int
+    score: float      # c_tok: w_long*log softmax(long) + alpha*log softmax(short) - beta*prior
+    logprob: float    # q_tok: log softmax(fused)
+    gap: float        # top-1 minus top-2 of the fused logits (inf if V == 1)
+    lse_long: float
+    lse_short: float  # nan when the row has no short logits
+    lse_fused: float
+    scores: Optional[np.ndarray] = None   # c_v for every v, when requested
+
+
+def fuse(long_row, short_row, prior, w_long: float, alpha: float, beta: float) -> np.ndarray:
+    """l = w_long * l_L + alpha * l_S - beta * l_P  (Sec. 4.3; w_long = 1 in the paper)."""
+    f = F64(w_long) * np.asarray(long_row, dtype=F64)
+    if short_row is not None:
+        f = f + F64(alpha) * np.asarray(short_row, dtype=F64)
+    if prior is not None:
+        f = f - F64(beta) * np.asarray(prior, dtype=F64)
+    return f
+
+
+def greedy_token(fused: np.ndarray) -> int:
+    """argmax over the vocabulary, decided in float32, lowest index on ties."""
+    return int(np.argmax(np.asarray(fused, dtype=np.float32)))
+
+
+def top2_gap(fused: np.ndarray) -> float:
+    if fused.shape[0] < 2:
+        return float("inf")
+    top = np.partition(fused, -2)[-2:]
+    return float(top[1] - top[0])
+
+
+def combine_row(long_row, short_row, prior, w_long: float, alpha: float, beta: float,
+                force_token: Optional[int] = None, want_scores: bool = False) -> RowResult:
+    """Fuse one row of long and short logits, decode greedily and report its statistics.
+
+    With short_row = None the row is decoded from the long logits alone (no prior
+    either), as for the first position of Algorithm 1.
+    """
+    long_row = np.asarray(long_row, dtype=F64)
+    if short_row is None:
+        fused = F64(w_long) * long_row
+        lse_s = float("nan")
+        a_eff = 0.0
+    else:
+        fused = fuse(long_row, short_row, prior, w_long, alpha, beta)
+        lse_s = logsumexp(short_row)
+        a_eff = alpha
+    lse_l = logsumexp(long_row)
+    lse_f = logsumexp(fused)
+    tok = greedy_token(fused) if force_token is None else int(force_token)
+    norm = F64(w_long) * lse_l + (F64(a_eff) * lse_s if short_row is not None else 0.0)
+    res = RowResult(token=tok, score=float(fused[tok] - norm), logprob=float(fused[tok] - lse_f),
+                    gap=top2_gap(fused), lse_long=lse_l, lse_short=lse_s, lse_fused=lse_f)
+    if want_scores:
+        res.scores = fused - norm
+    return res
+
+
+def combine_rows(long_rows, short_rows, prior, w_long, alpha, beta, want_scores=False):
+    """combine_row over every row of [rows, V] inputs."""
+    long_rows = np.asarray(long_rows, dtype=F64)
+    short_rows = np.asarray(short_rows, dtype=F64)
+    return [combine_row(long_rows[i], short_rows[i], prior, w_long, alpha, beta,
+                        want_scores=want_scores) for i in range(long_rows.shape[0])]
+
+
+# ----------------------------------------------------------------------------------------
+# App. A: local heads
+# ----------------------------------------------------------------------------------------
+def gru_cell(x, h, w_ih, w_hh):
+    """One step of a bias-free GRU; gate rows of w_ih [3H, d] and w_hh [3H, H] are (r, z, n)."""
+    x = np.asarray(x, dtype=F64)
+    h = np.asarray(h, dtype=F64)
+    H = h.shape[0]
+    gi = np.asarray(w_ih, dtype=F64) @ x
+    gh = np.asarray(w_hh, dtype=F64) @ h
+    r = sigmoid(gi[:H] + gh[:H])
+    z = sigmoid(gi[H:2 * H] + gh[H:2 * H])
+    n = np.tanh(gi[2 * H:] + r * gh[2 * H:])
+    return (1.0 - z) * n + z * h
+
+
+class RnnHead:
+    """r_i = SiLU(W_rank GRU(E_tgt(z_i))),  l_S = W_vocab r_i  (App. A)."""
+
+    def __init__(self, emb, w_ih, w_hh, w_rank, w_vocab):
+        self.emb = emb                                # indexed by token; rows become float64
+        self.w_ih = np.asarray(w_ih, dtype=F64)
+        self.w_hh = np.asarray(w_hh, dtype=F64)
+        self.w_rank = np.asarray(w_rank, dtype=F64)
+        self.w_vocab = np.asarray(w_vocab, dtype=F64)
+        self.H = self.w_hh.shape[1]
+
+    @classmethod
+    def from_weights(cls, hw) -> "RnnHead":
+        return cls(hw.emb, hw.w_ih, hw.w_hh, hw.w_rank, hw.w_vocab)
+
+    def init_state(self):
+        return np.zeros(self.H, dtype=F64)
+
+    def step(self, h, token: int):
+        x = np.asarray(self.emb[int(token)], dtype=F64)
+        h = gru_cell(x, h, self.w_ih, self.w_hh)
+        rho = silu(self.w_rank @ h)
+        return h, self.w_vocab @ rho
+
+    def rho(self, h):
+        return silu(self.w_rank @ h)
+
+
+class MarkovHead:
+    """r_i = E_M(x_{i-1}),  l_S = r_i W_M^T  with E_M, W_M in R^{V x d_r}  (App. A)."""
+
+    def __init__(self, e_m, w_m):
+        self.e_m = e_m
+        self.w_m = np.asarray(w_m, dtype=F64)
+
+    def init_state(self):
+        return None
+
+    def step(self, state, token: int):
+        r = np.asarray(self.e_m[int(token)], dtype=F64)
+        return state, self.w_m @ r
+
+
+# ----------------------------------------------------------------------------------------
+# Algorithm 1: one draft block
+# ----------------------------------------------------------------------------------------
+@dataclasses.dataclass
+class DraftResult:
+    tokens: np.ndarray          # [batch, B] int32
+    score: np.ndarray           # [batch, B]
+    logprob: np.ndarray
+    gap: np.ndarray
+    lse_long: np.ndarray
+    lse_short: np.ndarray
+    lse_fused: np.ndarray
+
+
+def draft_block(head, long_logits, last_token: Sequence[int], prior, w_long: float,
+                alpha: float, beta: float, first_row_long_only: bool = False,
+                force: Optional[np.ndarray] = None, sequences: Optional[Sequence[int]] = None
+                ) -> DraftResult:
+    """Greedy DeLS-Spec drafting of one block per sequence (Algorithm 1, decoding steps).
+
+    long_logits: [batch, B, V] (anything indexable to rows); last_token: [batch].
+    force: optional [batch, B] tokens that replace the decoded ones (statistics are then
+    reported for the forced token), used to keep a replay aligned after a near-tie.
+    sequences: optional subset of sequence indices to run (others are left at zero).
+    """
+    batch = len(last_token)
+    B = np.asarray(long_logits[0]).shape[0]
+    seqs = range(batch) if sequences is None else sequences
+    out = DraftResult(*[np.zeros((batch, B), dtype=np.int32)] +
+                      [np.zeros((batch, B), dtype=F64) for _ in range(6)])
+    for b in seqs:
+        rows = np.asarray(long_logits[b], dtype=F64)
+        state = head.init_state()
+        u = int(last_token[b])
+        for j in range(B):
+            f = None if force is None else int(force[b, j])
+            if first_row_long_only and j == 0:
+                res = combine_row(rows[0], None, None, w_long, alpha, beta, force_token=f)
+            else:
+                state, s = head.step(state, u)
+                res = combine_row(rows[j], s, prior, w_long, alpha, beta, force_token=f)
+            out.tokens[b, j] = res.token
+            out.score[b, j] = res.score
+            out.logprob[b, j] = res.logprob
+            out.gap[b, j] = res.gap
+            out.lse_long[b, j] = res.lse_long
+            out.lse_short[b, j] = res.lse_short
+            out.lse_fused[b, j] = res.lse_fused
+            u = res.token
+    return out
+
+
+def head_rollout(head, start_token: int, steps: int) -> np.ndarray:
+    """Greedy rollout of the local head alone (no long logits): each step feeds back its argmax."""
+    state = head.init_state()
+    u = int(start_token)
+    toks = []
+    for _ in range(steps):
+        state, s = head.step(state, u)
+        u = greedy_token(s)
+        toks.append(u)
+    return np.array(toks, dtype=np.int32)
+
+
+# ----------------------------------------------------------------------------------------
+# verification statistics (Sec. 5.1 tau; App. D rate_i)
+# ----------------------------------------------------------------------------------------
+def accept_len(draft: np.ndarray, target: np.ndarray) -> np.ndarray:
+    """Number of leading positions where the draft equals the target, per sequence."""
+    draft = np.asarray(draft)
+    target = np.asarray(target)
+    batch, B = draft.shape
+    out = np.zeros(batch, dtype=np.int32)
+    for b in range(batch):
+        a = 0
+        while a < B and draft[b, a] == target[b, a]:
+            a += 1
+        out[b] = a
+    return out
+
+
+def tau(accepted: np.ndarray) -> np.ndarray:
+    """Acceptance length including the bonus token."""
+    return np.asarray(accepted) + 1
+
+
+def rate_curve(accepted: np.ndarray, B: int) -> np.ndarray:
+    """rate_i = P(tau >= i) for i = 1..B+1."""
+    t = tau(accepted)
+    return np.array([np.mean(t >= i) for i in range(1, B + 2)], dtype=F64)
+
+
+def tau_gain_ratio(tau_dels: float, tau_base: float, tau_joint: float) -> float:
+    """Share of a jointly trained head's tau gain recovered: (t_dels - t_base)/(t_joint - t_base)."""
+    return (tau_dels - tau_base) / (tau_joint - tau_base)
+
+
+# ----------------------------------------------------------------------------------------
+# App. A: unigram log-prior with additive smoothing
+# ----------------------------------------------------------------------------------------
+def unigram_log_prior(counts: np.ndarray, smoothing: float = 1.0) -> np.ndarray:
+    c = np.asarray(counts, dtype=F64) + F64(smoothing)
+    return np.log(c / np.sum(c))
