@@ -1,0 +1,199 @@
+#!/usr/bin/env python3
+"""Benchmark of the DeLS-Spec block-drafting hot path on one MI355X.
+
+A step is one pass of the whole path over one batch: dls_draft_block (local head,
+fusion and greedy argmax at every draft position) followed by dls_accept_len.  The
+default workload is the Qwen3-4B-shaped batch-1 draft (B = 16, V = 151,936, d = 2560,
+GRU hidden 1024, rank 256).  Inputs are seeded synthetic tensors already resident in
+HBM.  Prints one JSON line with the drafted-token throughput, the roofline of the
+dominant kernel, the standalone fused combine at the serving shape, and the CPU oracle
+timed on the host as a baseline.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0     # MI355X HBM3E
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes_per_block(wl, esize=2):
+    """Bytes the method moves for one block when every step re-reads the head weights:
+    per step W_vocab + W_ih + W_hh + W_rank + one embedding row and one long-logit row per
+    sequence (prior not used)."""
+    V, d, H, r = wl.V, wl.d, wl.H, wl.r
+    per_step = (V * r + 3 * H * d + 3 * H * H + r * H) * esize + wl.batch * (d * esize + V * esize)
+    return per_step * wl.B, per_step
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="qwen3-4b-b1")
+    ap.add_argument("--init", default="stress", choices=["baseline", "stress"])
+    ap.add_argument("--alpha", type=float, default=0.5)
+    ap.add_argument("--combine-rows", type=int, default=1024)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build measures one GPU only (the drafting path has no multi-GPU form "
+              "here); run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2607_07409_amd import binding as B
+    from paper_2607_07409_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = W.WORKLOADS[args.workload]
+    log(f"generating {wl.name} inputs ({args.init} weights)")
+    hw = W.make_head(wl, args.init)
+    long_h = W.make_long_logits(wl)
+    last = W.make_last_token(wl)
+    head = B.LocalHead.from_weights(hw, dev)
+    L = B.as_tensor(long_h, dev)
+    last_t = torch.from_numpy(last).to(dev)
+
+    # ---- CPU oracle leg (also provides the target tokens) -------------------------------------
+    cpu = None
+    oracle_draft = None
+    if not args.no_cpu_baseline:
+        from oracle import dels_oracle as O
+        try:
+            from threadpoolctl import threadpool_info
+            cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        except Exception:
+            cores = 1
+        log("CPU oracle: preparing float64 head")
+        oh = O.RnnHead.from_weights(hw)
+        seq = [0]
+        t0 = time.perf_counter()
+        nblk = 0
+        while True:
+            res = O.draft_block(oh, long_h, last, None, 1.0, args.alpha, 0.0, sequences=seq)
+            nblk += 1
+            el = time.perf_counter() - t0
+            if el >= args.cpu_seconds or nblk >= 64:
+                break
+        oracle_draft = res.tokens
+        cpu = {"value": round(nblk * wl.B / el, 3), "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+               "sample": f"{nblk} draft block(s) of sequence 0 of {wl.name} (B={wl.B}), float64 numpy, "
+                         f"{el:.1f} s wall"}
+        log(f"CPU oracle: {cpu['value']} tokens/s over {nblk} blocks")
+    if oracle_draft is None:
+        oracle_draft = np.zeros((wl.batch, wl.B), np.int32)
+    targets, _ = W.make_targets(oracle_draft, wl)
+    tgt = torch.from_numpy(targets).to(dev)
+
+    # ---- the timed step ----------------------------------------------------------------------
+    tok = torch.empty((wl.batch, wl.B), dtype=torch.int32, device=dev)
+    st = torch.empty((wl.batch, wl.B, 6), dtype=torch.float32, device=dev)
+    acc = torch.empty(wl.batch, dtype=torch.int32, device=dev)
+    ws = torch.empty(max(256, B.draft_block_workspace_size(head, wl.batch, wl.B)), dtype=torch.uint8, device=dev)
+
+    def step():
+        B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws)
+        B.accept_len(tok, tgt, out=acc)
+
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log(f"timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = e0.elapsed_time(e1) / args.steps
+    tokens_per_s = wl.batch * wl.B / (ms_step * 1e-3)
+    log(f"step {ms_step * 1e3:.1f} us ({wall:.2f} s wall) -> {tokens_per_s:.0f} drafted tokens/s")
+
+    # ---- dominant kernel: the draft block on its own ---------------------------------------
+    n_k = max(20, args.steps // 2)
+    e2, e3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e2.record()
+    for _ in range(n_k):
+        B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws)
+    e3.record()
+    torch.cuda.synchronize()
+    blk_us = e2.elapsed_time(e3) / n_k * 1e3
+    alg_block, alg_step = algorithmic_bytes_per_block(wl)
+    achieved = alg_block / (blk_us * 1e-6) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "dls_draft_block (all launches of one block)", "us_per_launch": round(blk_us, 2),
+                "algorithmic_bytes_per_launch": alg_block}
+    log(f"draft block {blk_us:.1f} us, {achieved:.0f} GB/s algorithmic ({achieved / HBM_PEAK_GBS:.1%} of HBM peak)")
+
+    # ---- standalone fused combine at the serving shape (cold: inputs larger than the MALL) ----
+    R = args.combine_rows
+    Lc = B.as_tensor(W.make_logit_rows(R, wl.V, "bf16", 77, "onehot", 3.0, purpose=20), dev)
+    Sc = B.as_tensor(W.make_logit_rows(R, wl.V, "bf16", 77, "normal", 2.0, purpose=21), dev)
+    nbuf = max(1, int(np.ceil(1.0e9 / (Lc.numel() * 4))))    # rotate >= 1 GB of inputs
+    bufs = [(Lc, Sc)] + [(Lc.clone(), Sc.clone()) for _ in range(nbuf - 1)]
+    ctok = torch.empty(R, dtype=torch.int32, device=dev)
+    cst = torch.empty((R, 6), dtype=torch.float32, device=dev)
+    cws = torch.empty(max(256, B.combine_logits_workspace_size(R, wl.V)), dtype=torch.uint8, device=dev)
+    for i in range(5):
+        B.combine_logits(*bufs[i % nbuf], None, 1.0, args.alpha, 0.0, out=(ctok, cst, None), workspace=cws)
+    n_c = 60
+    e4, e5 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e4.record()
+    for i in range(n_c):
+        B.combine_logits(*bufs[i % nbuf], None, 1.0, args.alpha, 0.0, out=(ctok, cst, None), workspace=cws)
+    e5.record()
+    torch.cuda.synchronize()
+    c_us = e4.elapsed_time(e5) / n_c * 1e3
+    c_bytes = R * wl.V * 2 * 2
+    c_gbs = c_bytes / (c_us * 1e-6) / 1e9
+    combine = {"rows": R, "V": wl.V, "dtype": "bf16", "us_per_call": round(c_us, 2),
+               "algorithmic_bytes": c_bytes, "achieved_GBs": round(c_gbs, 1),
+               "frac_of_hbm_peak": round(c_gbs / HBM_PEAK_GBS, 4), "buffers_rotated": nbuf}
+    log(f"combine [{R}, {wl.V}] {c_us:.1f} us -> {c_gbs:.0f} GB/s ({c_gbs / HBM_PEAK_GBS:.1%})")
+
+    out = {
+        "metric": "drafted tokens/sec per block step; fused-combine HBM GB/s as % of peak",
+        "value": round(tokens_per_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": wl.batch, "B": wl.B, "V": wl.V, "d": wl.d, "H": wl.H,
+                   "r": wl.r, "weights": f"bf16 ({args.init} init)", "alpha": args.alpha, "beta": 0.0,
+                   "step": "draft_block + accept_len"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "combine": combine,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

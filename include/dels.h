@@ -1,0 +1,173 @@
+/*
+ * dels.h -- C ABI of the DeLS-Spec block-drafting library (libdels.so), MI355X / gfx950.
+ *
+ * The library drafts one block of B tokens per sequence the way DeLS-Spec does
+ * (Sec. 4.3, Algorithm 1): at each draft position a local head is stepped on the
+ * tokens drafted so far, its short-context logits are fused with fixed long-context
+ * (DFlash) logits and an optional log unigram prior,
+ *
+ *     l_v = w_long * l_L,v + alpha * l_S,v - beta * l_P,v          (Sec. 4.3 fusion)
+ *
+ * and the greedy (argmax) token is taken.  The local head is the paper's RNN head
+ * (App. A): a bias-free one-layer GRU over the frozen target embedding, a SiLU
+ * projection to rank r and a vocabulary head,
+ *
+ *     h' = GRU(E[u], h),   rho = SiLU(W_rank h'),   l_S = W_vocab rho.
+ *
+ * GRU gates use the (r, z, n) row order: r = sigmoid(W_ir x + W_hr h),
+ * z = sigmoid(W_iz x + W_hz h), n = tanh(W_in x + r * (W_hn h)),
+ * h' = (1 - z) * n + z * h, and h = 0 at the start of every block.
+ *
+ * Conventions shared by every entry point
+ *  - All tensor pointers are DEVICE pointers owned by the caller and must stay
+ *    valid until the work queued on `stream` has completed.  Tensors are dense and
+ *    row-major.  Bulk tensors (logits, weights, scores, workspace) must be 16-byte
+ *    aligned; int32/float vectors 4-byte aligned.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).  Every
+ *    call only enqueues work; nothing is synchronised.  Outputs are valid once the
+ *    caller has synchronised the stream.
+ *  - The library never allocates device memory in a call and holds no mutable
+ *    global state.  Scratch memory is the caller's `workspace`; one workspace must
+ *    not be used by two calls that may run concurrently.
+ *  - Arguments are checked on the host before any HIP call.  A failed check returns
+ *    DLS_ERR_ARG / DLS_ERR_SHAPE / DLS_ERR_DTYPE / DLS_ERR_WORKSPACE and enqueues
+ *    nothing.  No usable GPU gives DLS_ERR_DEVICE; a HIP failure gives DLS_ERR_HIP.
+ *    dls_last_error() returns a message for the last failure on the calling thread.
+ *  - Not checked (that would need a device sync): token ids lie in [0, V); logits
+ *    and weights are finite.  -inf is allowed in long logits (a masked token); NaN
+ *    gives unspecified results.
+ *  - Empty work (rows == 0, batch == 0 or B == 0) returns DLS_OK and enqueues nothing.
+ *  - Greedy decoding takes the lowest index among equal fused values.  All
+ *    arithmetic is float32; bf16 inputs are widened exactly.
+ */
+#ifndef DELS_H
+#define DELS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DLS_ABI_VERSION 1
+
+typedef enum dls_status {
+  DLS_OK = 0,
+  DLS_ERR_ARG = 1,        /* NULL or misaligned pointer, non-finite weight argument */
+  DLS_ERR_SHAPE = 2,      /* size outside the documented limits */
+  DLS_ERR_DTYPE = 3,      /* unknown or inconsistent element type */
+  DLS_ERR_WORKSPACE = 4,  /* workspace smaller than the size query returned */
+  DLS_ERR_DEVICE = 5,     /* no usable gfx950 device */
+  DLS_ERR_HIP = 6         /* a HIP runtime call or kernel launch failed */
+} dls_status;
+
+typedef enum dls_dtype { DLS_F32 = 0, DLS_BF16 = 1 } dls_dtype;
+
+/* dls_fusion.flags */
+#define DLS_FIRST_ROW_LONG_ONLY 0x1u  /* Algorithm 1 literally: draft position 0 is decoded
+                                         from the long logits alone (no short logits, no
+                                         prior) and the head only consumes drafted tokens;
+                                         the last accepted token is then unused. */
+
+/* Fusion weights (Sec. 4.3).  The paper uses w_long = 1 and alpha = beta = 0.3;
+   alpha = beta = 0 is the DFlash baseline (Sec. 5.6). */
+typedef struct dls_fusion {
+  float w_long;    /* weight on the long logits                       */
+  float alpha;     /* weight on the short (local-head) logits         */
+  float beta;      /* weight subtracted on the log unigram prior      */
+  uint32_t flags;  /* DLS_FIRST_ROW_LONG_ONLY or 0                    */
+} dls_fusion;
+
+/* Per-row statistics of the fused distribution, for the decoded token t.
+ *   score     = l_t - (w_long * lse_long + alpha * lse_short)
+ *             = w_long*log softmax(l_L)_t + alpha*log softmax(l_S)_t - beta*l_P,t
+ *   logprob   = l_t - lse_fused = log softmax(l)_t (the distribution Algorithm 1 decodes)
+ *   gap       = top-1 minus top-2 fused value (+inf when V == 1)
+ *   lse_*     = log-sum-exp over the vocabulary of l_L, l_S and l
+ * A row without short logits (DLS_FIRST_ROW_LONG_ONLY, position 0) has
+ * lse_short = NaN and score = l_t - w_long * lse_long. */
+typedef struct dls_row_stats {
+  float score;
+  float logprob;
+  float gap;
+  float lse_long;
+  float lse_short;
+  float lse_fused;
+} dls_row_stats;
+
+/* RNN local head (App. A).  All five tensors share `dtype` (DLS_BF16 or DLS_F32).
+ *   emb     [V, d]   frozen target embedding E_tgt
+ *   w_ih    [3H, d]  GRU input weights, rows (r, z, n)
+ *   w_hh    [3H, H]  GRU recurrent weights, rows (r, z, n)
+ *   w_rank  [r, H]   low-rank projection (followed by SiLU)
+ *   w_vocab [V, r]   vocabulary head
+ * Limits: 1 <= V <= 2^24; d, H, r multiples of 8 with 8 <= d <= 16384,
+ * 8 <= H <= 4096, 8 <= r <= 512. */
+typedef struct dls_local_head {
+  int32_t V, d, H, r;
+  dls_dtype dtype;
+  const void *emb;
+  const void *w_ih;
+  const void *w_hh;
+  const void *w_rank;
+  const void *w_vocab;
+} dls_local_head;
+
+/* ---------------------------------------------------------------------------------
+ * Fused combine + greedy argmax over independent rows (Sec. 4.3 fusion and the
+ * decode step of Algorithm 1), with the short logits given.
+ *   long_logits, short_logits  [rows, V] of `dtype`
+ *   prior        [V] float32 log unigram prior l_P, or NULL (then beta is ignored)
+ *   out_token    [rows] int32, the argmax of the fused logits
+ *   out_stats    [rows] dls_row_stats, or NULL
+ *   out_scores   [rows, V] float32, the full row of scores c_v (see dls_row_stats), or NULL
+ *   workspace    at least dls_combine_logits_workspace_size(rows, V) bytes (may be
+ *                NULL when that size is 0)
+ * Limits: 1 <= V <= 2^24, 0 <= rows <= 2^20.  The DLS_FIRST_ROW_LONG_ONLY flag is
+ * not used here. */
+size_t dls_combine_logits_workspace_size(int64_t rows, int32_t V);
+dls_status dls_combine_logits(const void *long_logits, const void *short_logits,
+                              dls_dtype dtype, const float *prior, int64_t rows, int32_t V,
+                              dls_fusion fusion, int32_t *out_token, dls_row_stats *out_stats,
+                              float *out_scores, void *workspace, size_t ws_bytes,
+                              void *stream);
+
+/* ---------------------------------------------------------------------------------
+ * One draft block per sequence (Algorithm 1, the decoding loop).
+ *   head         RNN local head (see dls_local_head); pointers are device pointers
+ *   long_logits  [batch, B, V] of `long_dtype`; row j is the long logits of draft
+ *                position j
+ *   last_token   [batch] int32, the last accepted token; it is the head's first input
+ *                (unused with DLS_FIRST_ROW_LONG_ONLY)
+ *   prior        [V] float32 or NULL
+ *   out_tokens   [batch, B] int32 drafted tokens; token j feeds the head at j + 1
+ *   out_stats    [batch, B] dls_row_stats, or NULL
+ *   workspace    at least dls_draft_block_workspace_size(head, batch, B) bytes
+ * Limits: 1 <= batch <= 256, 1 <= B <= 64 (0 is a no-op), the head limits above,
+ * long_dtype F32 or BF16. */
+size_t dls_draft_block_workspace_size(const dls_local_head *head, int32_t batch, int32_t B);
+dls_status dls_draft_block(const dls_local_head *head, const void *long_logits,
+                           dls_dtype long_dtype, const int32_t *last_token, const float *prior,
+                           int32_t batch, int32_t B, dls_fusion fusion, int32_t *out_tokens,
+                           dls_row_stats *out_stats, void *workspace, size_t ws_bytes,
+                           void *stream);
+
+/* ---------------------------------------------------------------------------------
+ * Prefix-acceptance length (verification step of Algorithm 1): out_len[b] is the
+ * number of leading positions j with draft[b, j] == target[b, j], in [0, B].  The
+ * paper's acceptance length tau counts the bonus token too: tau = out_len + 1.
+ *   draft, target [batch, B] int32;  out_len [batch] int32.
+ * Limits: 0 <= batch <= 2^24, 0 <= B <= 4096. */
+dls_status dls_accept_len(const int32_t *draft, const int32_t *target, int32_t batch,
+                          int32_t B, int32_t *out_len, void *stream);
+
+/* Names and messages. */
+const char *dls_status_string(dls_status status);
+const char *dls_last_error(void);
+int dls_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DELS_H */

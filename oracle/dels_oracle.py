@@ -78,6 +78,8 @@ class RowResult:
     lse_long: float
     lse_short: float  # nan when the row has no short logits
     lse_fused: float
+    argmax: int = -1  # the oracle's own decision (differs from token only when forced)
+    margin: float = 0.0   # fused[argmax] - fused[token] (0 unless forced)
     scores: Optional[np.ndarray] = None   # c_v for every v, when requested
 
 
@@ -121,10 +123,12 @@ def combine_row(long_row, short_row, prior, w_long: float, alpha: float, beta: f
         a_eff = alpha
     lse_l = logsumexp(long_row)
     lse_f = logsumexp(fused)
-    tok = greedy_token(fused) if force_token is None else int(force_token)
+    best = greedy_token(fused)
+    tok = best if force_token is None else int(force_token)
     norm = F64(w_long) * lse_l + (F64(a_eff) * lse_s if short_row is not None else 0.0)
     res = RowResult(token=tok, score=float(fused[tok] - norm), logprob=float(fused[tok] - lse_f),
-                    gap=top2_gap(fused), lse_long=lse_l, lse_short=lse_s, lse_fused=lse_f)
+                    gap=top2_gap(fused), lse_long=lse_l, lse_short=lse_s, lse_fused=lse_f,
+                    argmax=best, margin=float(fused[best] - fused[tok]))
     if want_scores:
         res.scores = fused - norm
     return res
@@ -209,6 +213,8 @@ class DraftResult:
     lse_long: np.ndarray
     lse_short: np.ndarray
     lse_fused: np.ndarray
+    argmax: np.ndarray          # the oracle's own decision at each position (given the history)
+    margin: np.ndarray          # fused[argmax] - fused[token]
 
 
 def draft_block(head, long_logits, last_token: Sequence[int], prior, w_long: float,
@@ -226,7 +232,8 @@ def draft_block(head, long_logits, last_token: Sequence[int], prior, w_long: flo
     B = np.asarray(long_logits[0]).shape[0]
     seqs = range(batch) if sequences is None else sequences
     out = DraftResult(*[np.zeros((batch, B), dtype=np.int32)] +
-                      [np.zeros((batch, B), dtype=F64) for _ in range(6)])
+                      [np.zeros((batch, B), dtype=F64) for _ in range(6)] +
+                      [np.zeros((batch, B), dtype=np.int32), np.zeros((batch, B), dtype=F64)])
     for b in seqs:
         rows = np.asarray(long_logits[b], dtype=F64)
         state = head.init_state()
@@ -245,6 +252,8 @@ def draft_block(head, long_logits, last_token: Sequence[int], prior, w_long: flo
             out.lse_long[b, j] = res.lse_long
             out.lse_short[b, j] = res.lse_short
             out.lse_fused[b, j] = res.lse_fused
+            out.argmax[b, j] = res.argmax
+            out.margin[b, j] = res.margin
             u = res.token
     return out
 

@@ -1,0 +1,205 @@
+"""Python binding of libdels (ctypes): argument marshalling only.
+
+Every computation runs in the HIP library; torch tensors only provide device memory
+and the stream.  Calling anything here without the built library raises at once.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdels.so")
+
+DLS_F32, DLS_BF16 = 0, 1
+DLS_FIRST_ROW_LONG_ONLY = 0x1
+STATUS = {0: "DLS_OK", 1: "DLS_ERR_ARG", 2: "DLS_ERR_SHAPE", 3: "DLS_ERR_DTYPE",
+          4: "DLS_ERR_WORKSPACE", 5: "DLS_ERR_DEVICE", 6: "DLS_ERR_HIP"}
+STATS_FIELDS = ("score", "logprob", "gap", "lse_long", "lse_short", "lse_fused")
+
+
+class DlsError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class Fusion(ctypes.Structure):
+    _fields_ = [("w_long", ctypes.c_float), ("alpha", ctypes.c_float), ("beta", ctypes.c_float),
+                ("flags", ctypes.c_uint32)]
+
+
+class RowStats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_float) for n in STATS_FIELDS]
+
+
+class LocalHeadC(ctypes.Structure):
+    _fields_ = [("V", ctypes.c_int32), ("d", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("r", ctypes.c_int32), ("dtype", ctypes.c_int),
+                ("emb", ctypes.c_void_p), ("w_ih", ctypes.c_void_p), ("w_hh", ctypes.c_void_p),
+                ("w_rank", ctypes.c_void_p), ("w_vocab", ctypes.c_void_p)]
+
+
+_lib = None
+_vp, _i32, _i64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        L.dls_combine_logits_workspace_size.restype = _sz
+        L.dls_combine_logits_workspace_size.argtypes = [_i64, _i32]
+        L.dls_combine_logits.restype = ctypes.c_int
+        L.dls_combine_logits.argtypes = [_vp, _vp, ctypes.c_int, _vp, _i64, _i32, Fusion, _vp, _vp, _vp,
+                                         _vp, _sz, _vp]
+        L.dls_draft_block_workspace_size.restype = _sz
+        L.dls_draft_block_workspace_size.argtypes = [ctypes.POINTER(LocalHeadC), _i32, _i32]
+        L.dls_draft_block.restype = ctypes.c_int
+        L.dls_draft_block.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
+                                      Fusion, _vp, _vp, _vp, _sz, _vp]
+        L.dls_accept_len.restype = ctypes.c_int
+        L.dls_accept_len.argtypes = [_vp, _vp, _i32, _i32, _vp, _vp]
+        L.dls_status_string.restype = ctypes.c_char_p
+        L.dls_status_string.argtypes = [ctypes.c_int]
+        L.dls_last_error.restype = ctypes.c_char_p
+        L.dls_last_error.argtypes = []
+        L.dls_abi_version.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != 0:
+        raise DlsError(status, lib().dls_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return DLS_BF16
+    if t.dtype == torch.float32:
+        return DLS_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def fusion(w_long=1.0, alpha=0.3, beta=0.3, first_row_long_only=False) -> Fusion:
+    return Fusion(w_long, alpha, beta, DLS_FIRST_ROW_LONG_ONLY if first_row_long_only else 0)
+
+
+# -----------------------------------------------------------------------------------
+# host data -> device tensors
+# -----------------------------------------------------------------------------------
+def as_tensor(x, device="cuda") -> torch.Tensor:
+    """Device tensor holding exactly the given values (bf16 bit patterns stay bf16)."""
+    bits = getattr(x, "bits", None)
+    if bits is not None:
+        return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(device)
+    a = np.ascontiguousarray(x)
+    return torch.from_numpy(a).to(device)
+
+
+class LocalHead:
+    """Device copy of an RNN local head (App. A) and its C descriptor."""
+
+    def __init__(self, emb, w_ih, w_hh, w_rank, w_vocab):
+        ts = [emb, w_ih, w_hh, w_rank, w_vocab]
+        dt = ts[0].dtype
+        if any(t.dtype != dt for t in ts):
+            raise TypeError("all head tensors must share one dtype")
+        self.emb, self.w_ih, self.w_hh, self.w_rank, self.w_vocab = [t.contiguous() for t in ts]
+        V, d = self.emb.shape
+        H = self.w_hh.shape[1]
+        r = self.w_rank.shape[0]
+        self.V, self.d, self.H, self.r = V, d, H, r
+        self.c = LocalHeadC(V, d, H, r, _dtype_code(self.emb), self.emb.data_ptr(), self.w_ih.data_ptr(),
+                            self.w_hh.data_ptr(), self.w_rank.data_ptr(), self.w_vocab.data_ptr())
+
+    @classmethod
+    def from_weights(cls, hw, device="cuda") -> "LocalHead":
+        return cls(*[as_tensor(a, device) for a in (hw.emb, hw.w_ih, hw.w_hh, hw.w_rank, hw.w_vocab)])
+
+    def nbytes(self) -> int:
+        return sum(t.numel() * t.element_size() for t in (self.emb, self.w_ih, self.w_hh, self.w_rank,
+                                                           self.w_vocab))
+
+
+# -----------------------------------------------------------------------------------
+# entry points
+# -----------------------------------------------------------------------------------
+def combine_logits_workspace_size(rows: int, V: int) -> int:
+    return int(lib().dls_combine_logits_workspace_size(rows, V))
+
+
+def combine_logits(long_logits: torch.Tensor, short_logits: torch.Tensor, prior=None, w_long=1.0, alpha=0.3,
+                   beta=0.3, want_stats=True, want_scores=False, out=None, workspace=None, stream=None):
+    """Fused combine + argmax of [rows, V] long and short logits.  Returns (tokens, stats, scores);
+    stats is a [rows, 6] float32 tensor (fields STATS_FIELDS) or None."""
+    L = lib()
+    rows, V = long_logits.shape
+    dev = long_logits.device
+    if out is None:
+        tok = torch.empty(rows, dtype=torch.int32, device=dev)
+        st = torch.empty((rows, 6), dtype=torch.float32, device=dev) if want_stats else None
+        sc = torch.empty((rows, V), dtype=torch.float32, device=dev) if want_scores else None
+    else:
+        tok, st, sc = out
+    need = L.dls_combine_logits_workspace_size(rows, V)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    _check(L.dls_combine_logits(_ptr(long_logits), _ptr(short_logits), _dtype_code(long_logits), _ptr(prior),
+                                rows, V, fusion(w_long, alpha, beta), _ptr(tok), _ptr(st), _ptr(sc),
+                                _ptr(workspace), workspace.numel(), _stream(stream)))
+    return tok, st, sc
+
+
+def draft_block_workspace_size(head: LocalHead, batch: int, B: int) -> int:
+    return int(lib().dls_draft_block_workspace_size(ctypes.byref(head.c), batch, B))
+
+
+def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional[torch.Tensor], prior=None,
+                w_long=1.0, alpha=0.3, beta=0.3, first_row_long_only=False, want_stats=True, out=None,
+                workspace=None, stream=None):
+    """Draft one block per sequence.  long_logits [batch, B, V]; returns (tokens [batch, B], stats
+    [batch, B, 6] or None)."""
+    L = lib()
+    batch, B, V = long_logits.shape
+    dev = long_logits.device
+    if out is None:
+        tok = torch.empty((batch, B), dtype=torch.int32, device=dev)
+        st = torch.empty((batch, B, 6), dtype=torch.float32, device=dev) if want_stats else None
+    else:
+        tok, st = out
+    if workspace is None:
+        need = L.dls_draft_block_workspace_size(ctypes.byref(head.c), batch, B)
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    _check(L.dls_draft_block(ctypes.byref(head.c), _ptr(long_logits), _dtype_code(long_logits), _ptr(last_token),
+                             _ptr(prior), batch, B, fusion(w_long, alpha, beta, first_row_long_only), _ptr(tok),
+                             _ptr(st), _ptr(workspace), workspace.numel(), _stream(stream)))
+    return tok, st
+
+
+def accept_len(draft: torch.Tensor, target: torch.Tensor, out=None, stream=None) -> torch.Tensor:
+    """Leading positions where draft == target, per sequence ([batch] int32)."""
+    L = lib()
+    batch, B = draft.shape
+    if out is None:
+        out = torch.empty(batch, dtype=torch.int32, device=draft.device)
+    _check(L.dls_accept_len(_ptr(draft), _ptr(target), batch, B, _ptr(out), _stream(stream)))
+    return out

@@ -1,0 +1,237 @@
+// C ABI of libdels: argument checks (host only, before any HIP call), workspace
+// sizing, device checks and dispatch to the kernel launchers.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+
+#include "dels_internal.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+dls_status fail(dls_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+dls_status fail(dls_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Device check: a visible gfx950 device must be current.  The result for each device
+// id is computed once; it never changes during the life of the process.
+struct DevInfo {
+  std::once_flag once;
+  bool ok = false;
+  std::string why;
+};
+DevInfo g_dev[64];
+
+dls_status check_device() {
+  int n = 0;
+  hipError_t e = hipGetDeviceCount(&n);
+  if (e != hipSuccess || n <= 0) return fail(DLS_ERR_DEVICE, "no HIP device available (%s)", hipGetErrorString(e));
+  int dev = 0;
+  if ((e = hipGetDevice(&dev)) != hipSuccess)
+    return fail(DLS_ERR_DEVICE, "hipGetDevice failed: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= 64) return fail(DLS_ERR_DEVICE, "device id %d out of range", dev);
+  DevInfo& di = g_dev[dev];
+  std::call_once(di.once, [&]() {
+    hipDeviceProp_t p;
+    hipError_t pe = hipGetDeviceProperties(&p, dev);
+    if (pe != hipSuccess) {
+      di.why = std::string("hipGetDeviceProperties failed: ") + hipGetErrorString(pe);
+      return;
+    }
+    if (std::strncmp(p.gcnArchName, "gfx950", 6) != 0) {
+      di.why = std::string("device is ") + p.gcnArchName + ", the library is built for gfx950 only";
+      return;
+    }
+    di.ok = true;
+  });
+  if (!di.ok) return fail(DLS_ERR_DEVICE, "%s", di.why.c_str());
+  return DLS_OK;
+}
+
+dls_status hip_fail(hipError_t e, const char* what) {
+  return fail(DLS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool valid_dtype(dls_dtype t) { return t == DLS_F32 || t == DLS_BF16; }
+size_t dsize(dls_dtype t) { return t == DLS_BF16 ? 2 : 4; }
+
+dls_status check_fusion(const dls_fusion& f) {
+  if (!std::isfinite(f.w_long) || !std::isfinite(f.alpha) || !std::isfinite(f.beta))
+    return fail(DLS_ERR_ARG, "fusion weights must be finite");
+  if (f.flags & ~DLS_FIRST_ROW_LONG_ONLY) return fail(DLS_ERR_ARG, "unknown fusion flags 0x%x", f.flags);
+  return DLS_OK;
+}
+
+dls_status check_head(const dls_local_head* h) {
+  if (!h) return fail(DLS_ERR_ARG, "head is NULL");
+  if (!valid_dtype(h->dtype)) return fail(DLS_ERR_DTYPE, "unknown head dtype %d", (int)h->dtype);
+  if (h->V < 1 || h->V > (1 << 24)) return fail(DLS_ERR_SHAPE, "V=%d outside [1, 2^24]", h->V);
+  if (h->d < 8 || h->d > 16384 || h->d % 8)
+    return fail(DLS_ERR_SHAPE, "d=%d must be a multiple of 8 in [8, 16384]", h->d);
+  if (h->H < 8 || h->H > 4096 || h->H % 8)
+    return fail(DLS_ERR_SHAPE, "H=%d must be a multiple of 8 in [8, 4096]", h->H);
+  if (h->r < 8 || h->r > 512 || h->r % 8)
+    return fail(DLS_ERR_SHAPE, "r=%d must be a multiple of 8 in [8, 512]", h->r);
+  const void* ps[5] = {h->emb, h->w_ih, h->w_hh, h->w_rank, h->w_vocab};
+  const char* nm[5] = {"emb", "w_ih", "w_hh", "w_rank", "w_vocab"};
+  for (int i = 0; i < 5; ++i) {
+    if (!ps[i]) return fail(DLS_ERR_ARG, "head.%s is NULL", nm[i]);
+    if (!aligned(ps[i], 16)) return fail(DLS_ERR_ARG, "head.%s is not 16-byte aligned", nm[i]);
+  }
+  return DLS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dls_status_string(dls_status s) {
+  switch (s) {
+    case DLS_OK: return "DLS_OK";
+    case DLS_ERR_ARG: return "DLS_ERR_ARG";
+    case DLS_ERR_SHAPE: return "DLS_ERR_SHAPE";
+    case DLS_ERR_DTYPE: return "DLS_ERR_DTYPE";
+    case DLS_ERR_WORKSPACE: return "DLS_ERR_WORKSPACE";
+    case DLS_ERR_DEVICE: return "DLS_ERR_DEVICE";
+    case DLS_ERR_HIP: return "DLS_ERR_HIP";
+  }
+  return "DLS_UNKNOWN_STATUS";
+}
+
+const char* dls_last_error(void) { return g_last_error.c_str(); }
+
+int dls_abi_version(void) { return DLS_ABI_VERSION; }
+
+size_t dls_combine_logits_workspace_size(int64_t rows, int32_t V) {
+  if (rows <= 0 || V <= 0) return 0;
+  const int parts = dls::combine_parts(rows, V);
+  size_t b = (size_t)rows * sizeof(float);                       // per-row normaliser
+  b = (b + 255) & ~(size_t)255;
+  if (parts > 1) b += (size_t)rows * parts * sizeof(dls::Partial);
+  return b;
+}
+
+dls_status dls_combine_logits(const void* long_logits, const void* short_logits, dls_dtype dtype,
+                              const float* prior, int64_t rows, int32_t V, dls_fusion fusion,
+                              int32_t* out_token, dls_row_stats* out_stats, float* out_scores,
+                              void* workspace, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  if (!valid_dtype(dtype)) return fail(DLS_ERR_DTYPE, "unknown dtype %d", (int)dtype);
+  if (rows < 0 || rows > (1 << 20)) return fail(DLS_ERR_SHAPE, "rows=%lld outside [0, 2^20]", (long long)rows);
+  if (V < 1 || V > (1 << 24)) return fail(DLS_ERR_SHAPE, "V=%d outside [1, 2^24]", V);
+  dls_status s = check_fusion(fusion);
+  if (s != DLS_OK) return s;
+  if (rows == 0) return DLS_OK;
+  if (!long_logits || !short_logits || !out_token) return fail(DLS_ERR_ARG, "required pointer is NULL");
+  if (!aligned(long_logits, 16) || !aligned(short_logits, 16))
+    return fail(DLS_ERR_ARG, "logits must be 16-byte aligned");
+  if (!aligned(out_token, 4) || (prior && !aligned(prior, 4)) || (out_stats && !aligned(out_stats, 4)) ||
+      (out_scores && !aligned(out_scores, 16)))
+    return fail(DLS_ERR_ARG, "misaligned output or prior pointer");
+  const size_t need = dls_combine_logits_workspace_size(rows, V);
+  if (ws_bytes < need) return fail(DLS_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, need);
+  if (need && (!workspace || !aligned(workspace, 16)))
+    return fail(DLS_ERR_ARG, "workspace is NULL or not 16-byte aligned");
+  if ((s = check_device()) != DLS_OK) return s;
+
+  dls::CombineArgs a;
+  a.long_logits = long_logits;
+  a.short_logits = short_logits;
+  a.dtype = dtype;
+  a.prior = prior;
+  a.rows = rows;
+  a.V = V;
+  a.wl = fusion.w_long;
+  a.al = fusion.alpha;
+  a.be = prior ? fusion.beta : 0.f;
+  a.parts = dls::combine_parts(rows, V);
+  a.norm = (float*)workspace;
+  a.partials = (dls::Partial*)((char*)workspace + (((size_t)rows * sizeof(float) + 255) & ~(size_t)255));
+  a.out_token = out_token;
+  a.out_stats = out_stats;
+  a.out_scores = out_scores;
+  hipError_t e = dls::launch_combine(a, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "combine_logits launch");
+  return DLS_OK;
+}
+
+size_t dls_draft_block_workspace_size(const dls_local_head* head, int32_t batch, int32_t B) {
+  if (!head || batch <= 0 || B <= 0 || head->V <= 0 || head->H <= 0 || head->r <= 0) return 0;
+  return dls::draft_layout(*head, batch, B).total;
+}
+
+dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,
+                           const int32_t* last_token, const float* prior, int32_t batch, int32_t B,
+                           dls_fusion fusion, int32_t* out_tokens, dls_row_stats* out_stats, void* workspace,
+                           size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  dls_status s = check_head(head);
+  if (s != DLS_OK) return s;
+  if (!valid_dtype(long_dtype)) return fail(DLS_ERR_DTYPE, "unknown long-logit dtype %d", (int)long_dtype);
+  if (batch < 0 || batch > 256) return fail(DLS_ERR_SHAPE, "batch=%d outside [0, 256]", batch);
+  if (B < 0 || B > 64) return fail(DLS_ERR_SHAPE, "B=%d outside [0, 64]", B);
+  if ((s = check_fusion(fusion)) != DLS_OK) return s;
+  if (batch == 0 || B == 0) return DLS_OK;
+  const bool literal = (fusion.flags & DLS_FIRST_ROW_LONG_ONLY) != 0;
+  if (!long_logits || !out_tokens || (!last_token && !literal))
+    return fail(DLS_ERR_ARG, "required pointer is NULL");
+  if (!aligned(long_logits, 16)) return fail(DLS_ERR_ARG, "long_logits must be 16-byte aligned");
+  if ((last_token && !aligned(last_token, 4)) || !aligned(out_tokens, 4) || (prior && !aligned(prior, 4)) ||
+      (out_stats && !aligned(out_stats, 4)))
+    return fail(DLS_ERR_ARG, "misaligned vector argument");
+  const size_t need = dls_draft_block_workspace_size(head, batch, B);
+  if (ws_bytes < need) return fail(DLS_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, need);
+  if (!workspace || !aligned(workspace, 256)) return fail(DLS_ERR_ARG, "workspace is NULL or not 256-byte aligned");
+  if ((s = check_device()) != DLS_OK) return s;
+
+  dls::DraftArgs a;
+  a.head = *head;
+  a.long_logits = long_logits;
+  a.long_dtype = long_dtype;
+  a.last_token = last_token;
+  a.prior = prior;
+  a.batch = batch;
+  a.B = B;
+  a.f = fusion;
+  if (!prior) a.f.beta = 0.f;
+  a.out_tokens = out_tokens;
+  a.out_stats = out_stats;
+  a.ws = (char*)workspace;
+  a.lay = dls::draft_layout(*head, batch, B);
+  hipError_t e = dls::launch_draft(a, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "draft_block launch");
+  return DLS_OK;
+}
+
+dls_status dls_accept_len(const int32_t* draft, const int32_t* target, int32_t batch, int32_t B, int32_t* out_len,
+                          void* stream) {
+  g_last_error.clear();
+  if (batch < 0 || batch > (1 << 24)) return fail(DLS_ERR_SHAPE, "batch=%d outside [0, 2^24]", batch);
+  if (B < 0 || B > 4096) return fail(DLS_ERR_SHAPE, "B=%d outside [0, 4096]", B);
+  if (batch == 0) return DLS_OK;
+  if (!out_len || (B > 0 && (!draft || !target))) return fail(DLS_ERR_ARG, "required pointer is NULL");
+  if (!aligned(out_len, 4) || (draft && !aligned(draft, 4)) || (target && !aligned(target, 4)))
+    return fail(DLS_ERR_ARG, "misaligned pointer");
+  dls_status s = check_device();
+  if (s != DLS_OK) return s;
+  hipError_t e = dls::launch_accept(draft, target, batch, B, out_len, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "accept_len launch");
+  return DLS_OK;
+}
+
+}  // extern "C"

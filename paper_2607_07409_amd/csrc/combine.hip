@@ -1,0 +1,180 @@
+// Fused combine + greedy argmax over independent rows (Sec. 4.3 fusion equation and
+// the decode step of Algorithm 1), short logits given in HBM.
+//
+// A row of V elements is split into `parts` contiguous ranges, one workgroup each.
+// Every thread streams 16-byte chunks of the long and short rows (coalesced across
+// the workgroup), forms l = w_long*l_L + alpha*l_S - beta*l_P in float32 and folds
+// the chunk into its running (max, sum exp) for l_L, l_S, l and into the top-2 of l.
+// The workgroup merge is a fixed-order butterfly, so results are deterministic.
+// With parts > 1 a second kernel merges the per-range partials of each row.
+#include "dels_internal.hpp"
+
+namespace dls {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kUnroll = 2;
+
+// l_v for one element (the GPU's float32 reading of the fusion equation)
+template <bool PRIOR>
+__device__ __forceinline__ float fuse1(float a, float b, float p, float wl, float al, float be) {
+  float f = __builtin_fmaf(al, b, wl * a);
+  if (PRIOR) f = __builtin_fmaf(-be, p, f);
+  return f;
+}
+
+template <typename T, bool PRIOR>
+__device__ __forceinline__ void fold_scalar(Partial& P, const T* Lr, const T* Sr, const float* prior,
+                                            int v, float wl, float al, float be) {
+  float a = to_f32(Lr[v]), b = to_f32(Sr[v]);
+  float f = fuse1<PRIOR>(a, b, PRIOR ? prior[v] : 0.f, wl, al, be);
+  lse_fold<1>(P.L, &a, a);
+  lse_fold<1>(P.S, &b, b);
+  lse_fold<1>(P.F, &f, f);
+  top2_push(P, f, v);
+}
+
+template <typename T>
+__device__ __forceinline__ int head_elems(const T* p, int V) {
+  const int h = (int)(((16u - ((uint32_t)(uintptr_t)p & 15u)) & 15u) / sizeof(T));
+  return h < V ? h : V;
+}
+
+template <typename T, bool PRIOR>
+__global__ __launch_bounds__(kThreads) void k_combine_part(
+    const T* __restrict__ L, const T* __restrict__ S, const float* __restrict__ prior, int V,
+    float wl, float al, float be, Partial* __restrict__ part_out, int32_t* __restrict__ out_token,
+    dls_row_stats* __restrict__ out_stats, float* __restrict__ norm_out) {
+  constexpr int N = Chunk<T>::N;
+  __shared__ Partial sh[kThreads / 64];
+  const int row = blockIdx.x, part = blockIdx.y, parts = gridDim.y;
+  const T* Lr = L + (size_t)row * V;
+  const T* Sr = S + (size_t)row * V;
+  const int h0 = head_elems(Lr, V);
+  const int nch = (V - h0) / N;
+  const int tail0 = h0 + nch * N;
+  const int c0 = (int)((int64_t)nch * part / parts), c1 = (int)((int64_t)nch * (part + 1) / parts);
+  const int t = threadIdx.x;
+
+  Partial P = partial_empty();
+  if (part == 0 && t < h0) fold_scalar<T, PRIOR>(P, Lr, Sr, prior, t, wl, al, be);
+
+  for (int c = c0 + t; c < c1; c += kThreads * kUnroll) {
+    uint4 ra[kUnroll], rb[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int cc = c + u * kThreads;
+      if (cc < c1) {
+        ra[u] = Chunk<T>::raw(Lr + h0 + (size_t)cc * N);
+        rb[u] = Chunk<T>::raw(Sr + h0 + (size_t)cc * N);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int cc = c + u * kThreads;
+      if (cc < c1) {
+        float a[N], b[N], f[N];
+        Chunk<T>::widen(ra[u], a);
+        Chunk<T>::widen(rb[u], b);
+        const int v0 = h0 + cc * N;
+        float ma = a[0], mb = b[0];
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+          f[i] = fuse1<PRIOR>(a[i], b[i], PRIOR ? prior[v0 + i] : 0.f, wl, al, be);
+          ma = fmaxf(ma, a[i]);
+          mb = fmaxf(mb, b[i]);
+        }
+        float mf = f[0];
+#pragma unroll
+        for (int i = 1; i < N; ++i) mf = fmaxf(mf, f[i]);
+        lse_fold<N>(P.L, a, ma);
+        lse_fold<N>(P.S, b, mb);
+        lse_fold<N>(P.F, f, mf);
+#pragma unroll
+        for (int i = 0; i < N; ++i) top2_push(P, f[i], v0 + i);
+      }
+    }
+  }
+  if (part == parts - 1 && t < V - tail0) fold_scalar<T, PRIOR>(P, Lr, Sr, prior, tail0 + t, wl, al, be);
+
+  P = block_merge(P, sh, kThreads / 64);
+  if (t == 0) {
+    if (parts == 1)
+      finalize_row(P, wl, al, false, out_token + row, out_stats ? out_stats + row : nullptr,
+                   norm_out ? norm_out + row : nullptr);
+    else
+      part_out[(size_t)row * parts + part] = P;
+  }
+}
+
+__global__ __launch_bounds__(64) void k_combine_finalize(const Partial* __restrict__ parts_in, int parts,
+                                                         float wl, float al, int32_t* __restrict__ out_token,
+                                                         dls_row_stats* __restrict__ out_stats,
+                                                         float* __restrict__ norm_out) {
+  const int row = blockIdx.x, lane = threadIdx.x;
+  Partial P = partial_empty();
+  for (int i = lane; i < parts; i += 64) P = partial_merge(P, parts_in[(size_t)row * parts + i]);
+  P = wave_merge(P);
+  if (lane == 0)
+    finalize_row(P, wl, al, false, out_token + row, out_stats ? out_stats + row : nullptr,
+                 norm_out ? norm_out + row : nullptr);
+}
+
+// c_v = l_v - (w_long * lse_long + alpha * lse_short), recomputing l_v exactly as above
+template <typename T, bool PRIOR>
+__global__ __launch_bounds__(kThreads) void k_combine_scores(const T* __restrict__ L, const T* __restrict__ S,
+                                                             const float* __restrict__ prior, int V, float wl,
+                                                             float al, float be, const float* __restrict__ norm,
+                                                             float* __restrict__ scores) {
+  const int row = blockIdx.x;
+  const T* Lr = L + (size_t)row * V;
+  const T* Sr = S + (size_t)row * V;
+  float* Cr = scores + (size_t)row * V;
+  const float nr = norm[row];
+  for (int v = blockIdx.y * kThreads + threadIdx.x; v < V; v += gridDim.y * kThreads)
+    Cr[v] = fuse1<PRIOR>(to_f32(Lr[v]), to_f32(Sr[v]), PRIOR ? prior[v] : 0.f, wl, al, be) - nr;
+}
+
+template <typename T, bool PRIOR>
+hipError_t launch_combine_t(const CombineArgs& a, hipStream_t st) {
+  const int parts = a.parts;
+  dim3 grid((unsigned)a.rows, parts);
+  k_combine_part<T, PRIOR><<<grid, kThreads, 0, st>>>(
+      (const T*)a.long_logits, (const T*)a.short_logits, a.prior, a.V, a.wl, a.al, a.be, a.partials,
+      a.out_token, a.out_stats, a.norm);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (parts > 1) {
+    k_combine_finalize<<<(unsigned)a.rows, 64, 0, st>>>(a.partials, parts, a.wl, a.al, a.out_token,
+                                                         a.out_stats, a.norm);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  if (a.out_scores) {
+    dim3 g2((unsigned)a.rows, (unsigned)std::min<int64_t>((a.V + kThreads - 1) / kThreads, 64));
+    k_combine_scores<T, PRIOR><<<g2, kThreads, 0, st>>>((const T*)a.long_logits, (const T*)a.short_logits,
+                                                        a.prior, a.V, a.wl, a.al, a.be, a.norm, a.out_scores);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace
+
+int combine_parts(int64_t rows, int32_t V) {
+  // enough workgroups to cover the chip when rows are few; each range >= 2048 elements
+  const int64_t target = 2048;
+  int64_t p = (target + rows - 1) / std::max<int64_t>(rows, 1);
+  const int64_t cap = std::max<int64_t>(1, V / 2048);
+  p = std::min(p, cap);
+  return (int)std::max<int64_t>(1, std::min<int64_t>(p, 256));
+}
+
+hipError_t launch_combine(const CombineArgs& a, hipStream_t st) {
+  const bool pr = a.prior != nullptr;
+  if (a.dtype == DLS_BF16)
+    return pr ? launch_combine_t<bf16_t, true>(a, st) : launch_combine_t<bf16_t, false>(a, st);
+  return pr ? launch_combine_t<float, true>(a, st) : launch_combine_t<float, false>(a, st);
+}
+
+}  // namespace dls

@@ -1,0 +1,175 @@
+// Device-side building blocks of the DeLS-Spec drafting kernels (gfx950, wave64).
+//
+//  * widening loads of 16-byte chunks (bf16 -> 8 floats, f32 -> 4 floats)
+//  * the running statistics of one vocabulary range of a fused row: online
+//    (max, sum of exp) pairs for the long, short and fused logits and the top-2 of
+//    the fused logits with the index of the top-1 (lowest index on ties)
+//  * an associative merge of two such partial statistics, used across lanes, waves
+//    and workgroups in a fixed order (deterministic results)
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dls {
+
+typedef uint16_t bf16_t;
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ float to_f32(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }
+__device__ __forceinline__ float to_f32(float f) { return f; }
+
+// 16-byte chunk of T, widened to float
+template <typename T> struct Chunk;
+template <> struct Chunk<bf16_t> {
+  static constexpr int N = 8;
+  __device__ __forceinline__ static void load(const bf16_t* p, float* o) {
+    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    o[0] = bf16_lo(v.x); o[1] = bf16_hi(v.x); o[2] = bf16_lo(v.y); o[3] = bf16_hi(v.y);
+    o[4] = bf16_lo(v.z); o[5] = bf16_hi(v.z); o[6] = bf16_lo(v.w); o[7] = bf16_hi(v.w);
+  }
+  __device__ __forceinline__ static uint4 raw(const bf16_t* p) { return *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ static void widen(const uint4 v, float* o) {
+    o[0] = bf16_lo(v.x); o[1] = bf16_hi(v.x); o[2] = bf16_lo(v.y); o[3] = bf16_hi(v.y);
+    o[4] = bf16_lo(v.z); o[5] = bf16_hi(v.z); o[6] = bf16_lo(v.w); o[7] = bf16_hi(v.w);
+  }
+};
+template <> struct Chunk<float> {
+  static constexpr int N = 4;
+  __device__ __forceinline__ static void load(const float* p, float* o) {
+    const float4 v = *reinterpret_cast<const float4*>(p);
+    o[0] = v.x; o[1] = v.y; o[2] = v.z; o[3] = v.w;
+  }
+  __device__ __forceinline__ static uint4 raw(const float* p) { return *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ static void widen(const uint4 v, float* o) {
+    o[0] = __uint_as_float(v.x); o[1] = __uint_as_float(v.y);
+    o[2] = __uint_as_float(v.z); o[3] = __uint_as_float(v.w);
+  }
+};
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+__device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + __expf(-x)); }
+__device__ __forceinline__ float tanhf_(float x) {
+  // tanh x = 1 - 2 / (exp(2x) + 1); exact limits +-1 at overflow/underflow of exp
+  return 1.0f - 2.0f / (__expf(2.0f * x) + 1.0f);
+}
+__device__ __forceinline__ float siluf_(float x) { return x * sigmoidf_(x); }
+
+// ------------------------------------------------------------------------------
+// Online log-sum-exp: value = m + ln(s), s = sum_i exp(x_i - m).  m = -inf, s = 0
+// is the empty set.
+// ------------------------------------------------------------------------------
+struct Lse {
+  float m, s;
+};
+__device__ __forceinline__ Lse lse_empty() { return {-INFINITY, 0.f}; }
+
+// fold a chunk of n values whose maximum is cm
+template <int n>
+__device__ __forceinline__ void lse_fold(Lse& a, const float* x, float cm) {
+  const float mn = fmaxf(a.m, cm);
+  if (mn == -INFINITY) return;                       // everything so far is -inf
+  const float ml = mn * kLog2e;
+  float acc = a.s * fast_exp2(a.m * kLog2e - ml);    // exp2(-inf) = 0 covers the empty case
+#pragma unroll
+  for (int i = 0; i < n; ++i) acc += fast_exp2(__builtin_fmaf(x[i], kLog2e, -ml));
+  a.m = mn;
+  a.s = acc;
+}
+
+__device__ __forceinline__ Lse lse_merge(Lse a, Lse b) {
+  const float mn = fmaxf(a.m, b.m);
+  if (mn == -INFINITY) return lse_empty();
+  const float ml = mn * kLog2e;
+  return {mn, a.s * fast_exp2(a.m * kLog2e - ml) + b.s * fast_exp2(b.m * kLog2e - ml)};
+}
+__device__ __forceinline__ float lse_value(Lse a) {
+  return a.m == -INFINITY ? -INFINITY : a.m + fast_log2(a.s) * kLn2;
+}
+
+// ------------------------------------------------------------------------------
+// Partial statistics of a vocabulary range of one fused row.
+// ------------------------------------------------------------------------------
+struct Partial {
+  Lse L, S, F;    // long, short, fused
+  float t1, t2;   // top-1 and top-2 fused values
+  int i1;         // index of t1 (lowest among equal values)
+  int pad;
+};
+static_assert(sizeof(Partial) == 40, "partial layout");
+
+__device__ __forceinline__ Partial partial_empty() {
+  Partial p;
+  p.L = p.S = p.F = lse_empty();
+  p.t1 = p.t2 = -INFINITY;
+  p.i1 = 0x7fffffff;
+  p.pad = 0;
+  return p;
+}
+
+// top-2 update with the values of one thread visited in increasing index order
+__device__ __forceinline__ void top2_push(Partial& p, float x, int idx) {
+  p.t2 = fmaxf(p.t2, fminf(x, p.t1));
+  const bool up = x > p.t1;
+  p.t1 = up ? x : p.t1;
+  p.i1 = up ? idx : p.i1;
+}
+
+__device__ __forceinline__ Partial partial_merge(const Partial& a, const Partial& b) {
+  Partial r;
+  r.L = lse_merge(a.L, b.L);
+  r.S = lse_merge(a.S, b.S);
+  r.F = lse_merge(a.F, b.F);
+  const bool a_wins = (a.t1 > b.t1) || (a.t1 == b.t1 && a.i1 < b.i1);
+  r.t1 = a_wins ? a.t1 : b.t1;
+  r.i1 = a_wins ? a.i1 : b.i1;
+  r.t2 = a_wins ? fmaxf(a.t2, b.t1) : fmaxf(b.t2, a.t1);
+  r.pad = 0;
+  return r;
+}
+
+__device__ __forceinline__ Partial shfl_xor_partial(const Partial& p, int m) {
+  Partial q;
+  q.L.m = __shfl_xor(p.L.m, m); q.L.s = __shfl_xor(p.L.s, m);
+  q.S.m = __shfl_xor(p.S.m, m); q.S.s = __shfl_xor(p.S.s, m);
+  q.F.m = __shfl_xor(p.F.m, m); q.F.s = __shfl_xor(p.F.s, m);
+  q.t1 = __shfl_xor(p.t1, m); q.t2 = __shfl_xor(p.t2, m);
+  q.i1 = __shfl_xor(p.i1, m);
+  q.pad = 0;
+  return q;
+}
+
+// Butterfly merge over the 64 lanes of a wave; every lane ends with the total.
+// The merge is commutative and the pairing is fixed, so the result is deterministic.
+__device__ __forceinline__ Partial wave_merge(Partial p) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) p = partial_merge(p, shfl_xor_partial(p, m));
+  return p;
+}
+
+// Merge over a workgroup of nwaves waves; the total is returned to every thread.
+// `sh` must hold nwaves Partials.
+__device__ __forceinline__ Partial block_merge(Partial p, Partial* sh, int nwaves) {
+  p = wave_merge(p);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) sh[wave] = p;
+  __syncthreads();
+  Partial t = sh[0];
+  for (int w = 1; w < nwaves; ++w) t = partial_merge(t, sh[w]);
+  return t;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+  return v;
+}
+
+}  // namespace dls

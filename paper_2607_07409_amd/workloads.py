@@ -310,3 +310,22 @@ class Problem:
 def make_problem(wl: Workload, init: str = "baseline", with_prior: bool = False) -> Problem:
     return Problem(wl, make_head(wl, init), make_long_logits(wl), make_last_token(wl),
                    make_zipf_log_prior(wl.V, wl.seed) if with_prior else None)
+
+
+def make_logit_rows(rows: int, V: int, dtype: str, seed: int, recipe: str = "onehot", scale: float = 3.0,
+                    purpose: int = 20):
+    """[rows, V] logits: 'normal' = N(0, scale^2); 'onehot' = scale*N(0,1) + 8 on one random token."""
+    out = np.empty((rows, V), dtype=np.uint16 if dtype == "bf16" else np.float32)
+
+    def work(i):
+        g = _rng(seed, purpose, i)
+        x = g.standard_normal(V, dtype=np.float32) * np.float32(scale)
+        if recipe == "onehot":
+            x[g.integers(0, V)] += np.float32(8.0)
+        elif recipe != "normal":
+            raise ValueError(recipe)
+        out[i] = f32_to_bf16_bits(x) if dtype == "bf16" else x
+
+    with ThreadPoolExecutor(_THREADS) as ex:
+        list(ex.map(work, range(rows)))
+    return Bf16Array(out) if dtype == "bf16" else out

@@ -1,0 +1,177 @@
+"""Host-side tests of the C ABI: the library loads, exports every function declared in
+include/dels.h, its structs have the layout a C compiler gives them, and bad arguments
+are rejected with status codes before any device call.  No kernel is launched.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+import torch
+
+from paper_2607_07409_amd import binding as b
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dels.h")
+HAS_GPU = torch.cuda.is_available()
+
+# fake, 256-byte-aligned device addresses: only ever passed to calls that fail validation
+# (or, without a GPU, stop at the device check)
+FAKE = [ctypes.c_void_p(0x7f0000000000 + 0x100000 * i) for i in range(16)]
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(dls_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_function():
+    L = b.lib()
+    names = _declared_functions()
+    assert {"dls_draft_block", "dls_combine_logits", "dls_accept_len"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", b.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (dls_\w+)", out))
+    assert set(names) <= exported
+
+
+def test_struct_layout_matches_c(tmp_path):
+    prog = tmp_path / "lay.c"
+    prog.write_text(f'''#include <stdio.h>
+#include <stddef.h>
+#include "{HEADER}"
+int main(void) {{
+  printf("%zu %zu %zu %zu %zu %zu %zu\\n", sizeof(dls_local_head), sizeof(dls_row_stats), sizeof(dls_fusion),
+         offsetof(dls_local_head, dtype), offsetof(dls_local_head, emb), offsetof(dls_local_head, w_vocab),
+         offsetof(dls_fusion, flags));
+  return 0;
+}}''')
+    exe = tmp_path / "lay"
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", str(prog), "-o", str(exe)], check=True)
+    got = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True).stdout.split()]
+    want = [ctypes.sizeof(b.LocalHeadC), ctypes.sizeof(b.RowStats), ctypes.sizeof(b.Fusion),
+            b.LocalHeadC.dtype.offset, b.LocalHeadC.emb.offset, b.LocalHeadC.w_vocab.offset,
+            b.Fusion.flags.offset]
+    assert got == want
+
+
+def test_header_compiles_as_cpp(tmp_path):
+    src = tmp_path / "h.cpp"
+    src.write_text(f'#include "{HEADER}"\nint main() {{ return dls_abi_version() == 1 ? 0 : 1; }}\n')
+    subprocess.run(["g++", "-std=c++17", "-Wall", "-Werror", "-c", str(src), "-o", str(tmp_path / "h.o")],
+                   check=True)
+
+
+def test_status_strings():
+    L = b.lib()
+    for code, name in b.STATUS.items():
+        assert L.dls_status_string(code).decode() == name
+    assert L.dls_status_string(99).decode() == "DLS_UNKNOWN_STATUS"
+    assert L.dls_abi_version() == 1
+
+
+def _head(**kw):
+    h = dict(V=1000, d=64, H=32, r=16, dtype=b.DLS_BF16, emb=FAKE[0].value, w_ih=FAKE[1].value,
+             w_hh=FAKE[2].value, w_rank=FAKE[3].value, w_vocab=FAKE[4].value)
+    h.update(kw)
+    return b.LocalHeadC(**h)
+
+
+def _draft(head, **kw):
+    a = dict(long=FAKE[5], ldt=b.DLS_BF16, last=FAKE[6], prior=None, batch=2, B=4, f=b.fusion(),
+             tok=FAKE[7], st=FAKE[8], ws=FAKE[9], wsb=1 << 30)
+    a.update(kw)
+    L = b.lib()
+    rc = L.dls_draft_block(ctypes.byref(head), a["long"], a["ldt"], a["last"], a["prior"], a["batch"], a["B"],
+                           a["f"], a["tok"], a["st"], a["ws"], a["wsb"], None)
+    return rc, L.dls_last_error().decode()
+
+
+def test_draft_block_rejects_bad_arguments():
+    E = {v: k for k, v in b.STATUS.items()}
+    cases = [
+        (dict(head=_head(V=0)), "DLS_ERR_SHAPE"),
+        (dict(head=_head(d=12)), "DLS_ERR_SHAPE"),
+        (dict(head=_head(H=4)), "DLS_ERR_SHAPE"),
+        (dict(head=_head(r=1024)), "DLS_ERR_SHAPE"),
+        (dict(head=_head(dtype=7)), "DLS_ERR_DTYPE"),
+        (dict(head=_head(w_rank=None)), "DLS_ERR_ARG"),
+        (dict(head=_head(w_vocab=FAKE[4].value + 2)), "DLS_ERR_ARG"),
+        (dict(head=_head(), ldt=5), "DLS_ERR_DTYPE"),
+        (dict(head=_head(), batch=257), "DLS_ERR_SHAPE"),
+        (dict(head=_head(), B=65), "DLS_ERR_SHAPE"),
+        (dict(head=_head(), long=None), "DLS_ERR_ARG"),
+        (dict(head=_head(), last=None), "DLS_ERR_ARG"),
+        (dict(head=_head(), tok=None), "DLS_ERR_ARG"),
+        (dict(head=_head(), long=ctypes.c_void_p(FAKE[5].value + 4)), "DLS_ERR_ARG"),
+        (dict(head=_head(), wsb=16), "DLS_ERR_WORKSPACE"),
+        (dict(head=_head(), ws=None), "DLS_ERR_ARG"),
+        (dict(head=_head(), f=b.Fusion(1.0, float("nan"), 0.0, 0)), "DLS_ERR_ARG"),
+        (dict(head=_head(), f=b.Fusion(1.0, 0.5, 0.0, 0x10)), "DLS_ERR_ARG"),
+    ]
+    for kw, want in cases:
+        head = kw.pop("head")
+        rc, msg = _draft(head, **kw)
+        assert b.STATUS[rc] == want, (kw, msg)
+        assert msg
+    # empty work is a no-op, even with NULL pointers
+    assert _draft(_head(), batch=0, long=None, tok=None)[0] == 0
+    assert _draft(_head(), B=0, long=None, tok=None)[0] == 0
+
+
+@pytest.mark.skipif(HAS_GPU, reason="would launch on fake pointers when a GPU is present")
+def test_valid_arguments_stop_at_device_check():
+    rc, msg = _draft(_head())
+    assert b.STATUS[rc] == "DLS_ERR_DEVICE", msg
+    # the literal first-row reading does not need the last token
+    rc, _ = _draft(_head(), last=None, f=b.fusion(first_row_long_only=True))
+    assert b.STATUS[rc] == "DLS_ERR_DEVICE"
+    L = b.lib()
+    rc = L.dls_combine_logits(FAKE[0], FAKE[1], b.DLS_BF16, None, 4, 1000, b.fusion(), FAKE[2], None, None,
+                              FAKE[3], 1 << 20, None)
+    assert b.STATUS[rc] == "DLS_ERR_DEVICE"
+    assert b.STATUS[L.dls_accept_len(FAKE[0], FAKE[1], 4, 16, FAKE[2], None)] == "DLS_ERR_DEVICE"
+
+
+def test_combine_rejects_bad_arguments():
+    L = b.lib()
+
+    def call(long=FAKE[0], short=FAKE[1], dt=b.DLS_BF16, prior=None, rows=4, V=1000, f=None, tok=FAKE[2],
+             ws=FAKE[3], wsb=1 << 20, scores=None):
+        return b.STATUS[L.dls_combine_logits(long, short, dt, prior, rows, V, f or b.fusion(), tok, None, scores,
+                                             ws, wsb, None)]
+
+    assert call(dt=3) == "DLS_ERR_DTYPE"
+    assert call(V=0) == "DLS_ERR_SHAPE"
+    assert call(rows=-1) == "DLS_ERR_SHAPE"
+    assert call(short=None) == "DLS_ERR_ARG"
+    assert call(tok=None) == "DLS_ERR_ARG"
+    assert call(long=ctypes.c_void_p(FAKE[0].value + 8)) == "DLS_ERR_ARG"
+    assert call(scores=ctypes.c_void_p(FAKE[4].value + 4)) == "DLS_ERR_ARG"
+    assert call(prior=ctypes.c_void_p(FAKE[5].value + 2)) == "DLS_ERR_ARG"
+    assert call(rows=4096, V=151936, wsb=16) == "DLS_ERR_WORKSPACE"
+    assert call(f=b.Fusion(float("inf"), 0.5, 0.0, 0)) == "DLS_ERR_ARG"
+    assert call(rows=0, long=None, short=None, tok=None) == "DLS_OK"
+
+
+def test_accept_len_rejects_bad_arguments():
+    L = b.lib()
+    assert b.STATUS[L.dls_accept_len(FAKE[0], FAKE[1], -1, 16, FAKE[2], None)] == "DLS_ERR_SHAPE"
+    assert b.STATUS[L.dls_accept_len(FAKE[0], FAKE[1], 4, 5000, FAKE[2], None)] == "DLS_ERR_SHAPE"
+    assert b.STATUS[L.dls_accept_len(None, FAKE[1], 4, 16, FAKE[2], None)] == "DLS_ERR_ARG"
+    assert b.STATUS[L.dls_accept_len(FAKE[0], FAKE[1], 4, 16, None, None)] == "DLS_ERR_ARG"
+    assert b.STATUS[L.dls_accept_len(None, None, 0, 16, None, None)] == "DLS_OK"
+
+
+def test_workspace_size_queries():
+    L = b.lib()
+    assert L.dls_combine_logits_workspace_size(0, 100) == 0
+    assert L.dls_combine_logits_workspace_size(16, 151936) > 0
+    h = _head(V=151936, d=2560, H=1024, r=256)
+    s1 = L.dls_draft_block_workspace_size(ctypes.byref(h), 1, 16)
+    s64 = L.dls_draft_block_workspace_size(ctypes.byref(h), 64, 16)
+    assert 0 < s1 < s64
+    assert L.dls_draft_block_workspace_size(None, 1, 16) == 0
