@@ -102,6 +102,8 @@ typedef struct dls_row_stats {
  *   w_hh    [3H, H]  GRU recurrent weights, rows (r, z, n)
  *   w_rank  [r, H]   low-rank projection (followed by SiLU)
  *   w_vocab [V, r]   vocabulary head
+ *   prepared         NULL, or a device buffer filled by dls_prepare_head from these same
+ *                    tensors; it enables the persistent drafting kernel (see below)
  * Limits: 1 <= V <= 2^24; d, H, r multiples of 8 with 8 <= d <= 16384,
  * 8 <= H <= 4096, 8 <= r <= 512. */
 typedef struct dls_local_head {
@@ -112,7 +114,22 @@ typedef struct dls_local_head {
   const void *w_hh;
   const void *w_rank;
   const void *w_vocab;
+  const void *prepared;
 } dls_local_head;
+
+/* ---------------------------------------------------------------------------------
+ * One-time preparation of a bf16 head for the persistent drafting kernel (App. A head,
+ * rearranged; nothing of the method changes):
+ *  - the GRU input projection is folded into a table T[u] = W_ih E[u] of [V, 3H] float32
+ *    values (E is frozen and the GRU has no bias, so the input term depends on the token
+ *    only); T is accumulated in float32 from exact bf16 products;
+ *  - W_vocab and W_hh are copied into the operand order of the bf16 matrix cores.
+ * The buffer needs dls_prepare_head_size(head) bytes (V*3H*4 + V*r*2 + 3H*H*2 + small,
+ * 1.98 GB for V = 151,936, H = 1024, r = 256) and stays valid while the head tensors
+ * are unchanged.  Requirements: dtype DLS_BF16, H a multiple of 32, r in {32, 64, 128,
+ * 256}; otherwise DLS_ERR_SHAPE / DLS_ERR_DTYPE.  Asynchronous on `stream`. */
+size_t dls_prepare_head_size(const dls_local_head *head);
+dls_status dls_prepare_head(const dls_local_head *head, void *prepared, size_t bytes, void *stream);
 
 /* ---------------------------------------------------------------------------------
  * Fused combine + greedy argmax over independent rows (Sec. 4.3 fusion and the
@@ -135,11 +152,21 @@ dls_status dls_combine_logits(const void *long_logits, const void *short_logits,
 
 /* ---------------------------------------------------------------------------------
  * One draft block per sequence (Algorithm 1, the decoding loop).
+ * Two implementations share this entry point.  With head->prepared set and a supported
+ * shape (bf16 head, batch <= 64, H/16 <= number of CUs, r divisible by H/16 with at most
+ * 16 rank rows per group, and the per-CU share of W_vocab fitting in AGPRs + LDS) one
+ * persistent kernel keeps the head weights on chip for the whole block; otherwise each
+ * position is a sequence of kernel launches.  dls_draft_block_path tells which is used.
+ * The workspace must be zero-filled before its first use; the library keeps it
+ * consistent afterwards.  If a persistent call ever sets the error word (the second
+ * uint32 of the workspace, nonzero after a stalled hand-off between workgroups), later
+ * persistent calls on that workspace do nothing until it is zero-filled again.
  *   head         RNN local head (see dls_local_head); pointers are device pointers
  *   long_logits  [batch, B, V] of `long_dtype`; row j is the long logits of draft
  *                position j
  *   last_token   [batch] int32, the last accepted token; it is the head's first input
- *                (unused with DLS_FIRST_ROW_LONG_ONLY)
+ *                (unused with DLS_FIRST_ROW_LONG_ONLY).  Values must lie in [0, V); one
+ *                outside is read as token 0 (no fault, but a meaningless draft)
  *   prior        [V] float32 or NULL
  *   out_tokens   [batch, B] int32 drafted tokens; token j feeds the head at j + 1
  *   out_stats    [batch, B] dls_row_stats, or NULL
@@ -147,6 +174,10 @@ dls_status dls_combine_logits(const void *long_logits, const void *short_logits,
  * Limits: 1 <= batch <= 256, 1 <= B <= 64 (0 is a no-op), the head limits above,
  * long_dtype F32 or BF16. */
 size_t dls_draft_block_workspace_size(const dls_local_head *head, int32_t batch, int32_t B);
+/* 1: the persistent kernel would be used for these arguments, 0: per-position launches,
+ * negative: the arguments are invalid.  Needs the device (it counts its CUs). */
+int dls_draft_block_path(const dls_local_head *head, int32_t batch, int32_t B, dls_dtype long_dtype,
+                         int has_prior);
 dls_status dls_draft_block(const dls_local_head *head, const void *long_logits,
                            dls_dtype long_dtype, const int32_t *last_token, const float *prior,
                            int32_t batch, int32_t B, dls_fusion fusion, int32_t *out_tokens,

@@ -41,7 +41,7 @@ class LocalHeadC(ctypes.Structure):
     _fields_ = [("V", ctypes.c_int32), ("d", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("r", ctypes.c_int32), ("dtype", ctypes.c_int),
                 ("emb", ctypes.c_void_p), ("w_ih", ctypes.c_void_p), ("w_hh", ctypes.c_void_p),
-                ("w_rank", ctypes.c_void_p), ("w_vocab", ctypes.c_void_p)]
+                ("w_rank", ctypes.c_void_p), ("w_vocab", ctypes.c_void_p), ("prepared", ctypes.c_void_p)]
 
 
 _lib = None
@@ -65,6 +65,12 @@ def lib() -> ctypes.CDLL:
         L.dls_draft_block.restype = ctypes.c_int
         L.dls_draft_block.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
                                       Fusion, _vp, _vp, _vp, _sz, _vp]
+        L.dls_prepare_head_size.restype = _sz
+        L.dls_prepare_head_size.argtypes = [ctypes.POINTER(LocalHeadC)]
+        L.dls_prepare_head.restype = ctypes.c_int
+        L.dls_prepare_head.argtypes = [ctypes.POINTER(LocalHeadC), _vp, _sz, _vp]
+        L.dls_draft_block_path.restype = ctypes.c_int
+        L.dls_draft_block_path.argtypes = [ctypes.POINTER(LocalHeadC), _i32, _i32, ctypes.c_int, ctypes.c_int]
         L.dls_accept_len.restype = ctypes.c_int
         L.dls_accept_len.argtypes = [_vp, _vp, _i32, _i32, _vp, _vp]
         L.dls_status_string.restype = ctypes.c_char_p
@@ -128,8 +134,29 @@ class LocalHead:
         H = self.w_hh.shape[1]
         r = self.w_rank.shape[0]
         self.V, self.d, self.H, self.r = V, d, H, r
+        self.prepared = None
         self.c = LocalHeadC(V, d, H, r, _dtype_code(self.emb), self.emb.data_ptr(), self.w_ih.data_ptr(),
-                            self.w_hh.data_ptr(), self.w_rank.data_ptr(), self.w_vocab.data_ptr())
+                            self.w_hh.data_ptr(), self.w_rank.data_ptr(), self.w_vocab.data_ptr(), None)
+
+    def prepare(self, stream=None) -> "LocalHead":
+        """Fill the prepared form (folded input table, operand-ordered weights) on the device."""
+        L = lib()
+        n = int(L.dls_prepare_head_size(ctypes.byref(self.c)))
+        buf = torch.empty(n, dtype=torch.uint8, device=self.emb.device)
+        _check(L.dls_prepare_head(ctypes.byref(self.c), _ptr(buf), n, _stream(stream)))
+        self.prepared = buf
+        self.c.prepared = buf.data_ptr()
+        return self
+
+    def unprepare(self) -> "LocalHead":
+        self.prepared = None
+        self.c.prepared = None
+        return self
+
+    def path(self, batch: int, B: int, long_dtype=torch.bfloat16, has_prior=False) -> int:
+        """1 if dls_draft_block would use the persistent kernel, 0 for per-position launches."""
+        code = DLS_BF16 if long_dtype == torch.bfloat16 else DLS_F32
+        return int(lib().dls_draft_block_path(ctypes.byref(self.c), batch, B, code, int(bool(has_prior))))
 
     @classmethod
     def from_weights(cls, hw, device="cuda") -> "LocalHead":
@@ -173,6 +200,17 @@ def draft_block_workspace_size(head: LocalHead, batch: int, B: int) -> int:
     return int(lib().dls_draft_block_workspace_size(ctypes.byref(head.c), batch, B))
 
 
+def draft_workspace(head: LocalHead, batch: int, B: int, device=None) -> torch.Tensor:
+    """A zero-filled draft workspace (the persistent kernel requires zeros before first use)."""
+    n = max(256, draft_block_workspace_size(head, batch, B))
+    return torch.zeros(n, dtype=torch.uint8, device=device or head.emb.device)
+
+
+def workspace_error(workspace: torch.Tensor) -> int:
+    """The persistent kernel's error word (nonzero after a stalled hand-off); synchronises."""
+    return int(workspace[4:8].view(torch.int32).item())
+
+
 def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional[torch.Tensor], prior=None,
                 w_long=1.0, alpha=0.3, beta=0.3, first_row_long_only=False, want_stats=True, out=None,
                 workspace=None, stream=None):
@@ -187,8 +225,7 @@ def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional
     else:
         tok, st = out
     if workspace is None:
-        need = L.dls_draft_block_workspace_size(ctypes.byref(head.c), batch, B)
-        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+        workspace = draft_workspace(head, batch, B, dev)
     _check(L.dls_draft_block(ctypes.byref(head.c), _ptr(long_logits), _dtype_code(long_logits), _ptr(last_token),
                              _ptr(prior), batch, B, fusion(w_long, alpha, beta, first_row_long_only), _ptr(tok),
                              _ptr(st), _ptr(workspace), workspace.numel(), _stream(stream)))

@@ -33,11 +33,12 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 struct DevInfo {
   std::once_flag once;
   bool ok = false;
+  int cus = 0;
   std::string why;
 };
 DevInfo g_dev[64];
 
-dls_status check_device() {
+dls_status check_device(int* cus = nullptr) {
   int n = 0;
   hipError_t e = hipGetDeviceCount(&n);
   if (e != hipSuccess || n <= 0) return fail(DLS_ERR_DEVICE, "no HIP device available (%s)", hipGetErrorString(e));
@@ -57,11 +58,18 @@ dls_status check_device() {
       di.why = std::string("device is ") + p.gcnArchName + ", the library is built for gfx950 only";
       return;
     }
+    int coop = 0;
+    if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess) coop = 0;
+    di.cus = coop ? p.multiProcessorCount : 0;
     di.ok = true;
   });
   if (!di.ok) return fail(DLS_ERR_DEVICE, "%s", di.why.c_str());
+  if (cus) *cus = di.cus;
   return DLS_OK;
 }
+
+// number of persistent workgroups for this device (0: no cooperative launch)
+int persist_groups(int cus) { return std::min(cus, dls::kMaxG); }
 
 dls_status hip_fail(hipError_t e, const char* what) {
   return fail(DLS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
@@ -170,9 +178,32 @@ dls_status dls_combine_logits(const void* long_logits, const void* short_logits,
   return DLS_OK;
 }
 
+size_t dls_prepare_head_size(const dls_local_head* head) {
+  if (!head || head->V <= 0 || head->H <= 0 || head->r <= 0) return 0;
+  return dls::prepared_layout(*head).total;
+}
+
+dls_status dls_prepare_head(const dls_local_head* head, void* prepared, size_t bytes, void* stream) {
+  g_last_error.clear();
+  dls_status s = check_head(head);
+  if (s != DLS_OK) return s;
+  if (head->dtype != DLS_BF16) return fail(DLS_ERR_DTYPE, "only bf16 heads can be prepared");
+  if (head->H % 32) return fail(DLS_ERR_SHAPE, "H=%d must be a multiple of 32 to prepare", head->H);
+  if (!(head->r == 32 || head->r == 64 || head->r == 128 || head->r == 256))
+    return fail(DLS_ERR_SHAPE, "r=%d must be 32, 64, 128 or 256 to prepare", head->r);
+  if (!prepared || !aligned(prepared, 256)) return fail(DLS_ERR_ARG, "prepared buffer is NULL or not 256-byte aligned");
+  const size_t need = dls::prepared_layout(*head).total;
+  if (bytes < need) return fail(DLS_ERR_WORKSPACE, "prepared buffer %zu bytes < %zu required", bytes, need);
+  if ((s = check_device()) != DLS_OK) return s;
+  hipError_t e = dls::launch_prepare(*head, prepared, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "prepare_head launch");
+  return DLS_OK;
+}
+
 size_t dls_draft_block_workspace_size(const dls_local_head* head, int32_t batch, int32_t B) {
   if (!head || batch <= 0 || B <= 0 || head->V <= 0 || head->H <= 0 || head->r <= 0) return 0;
-  return dls::draft_layout(*head, batch, B).total;
+  // persistent region first (its header must start zero-filled), per-launch region after it
+  return dls::persist_workspace(*head, batch, B).total + dls::draft_layout(*head, batch, B).total;
 }
 
 dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,
@@ -197,7 +228,52 @@ dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, 
   const size_t need = dls_draft_block_workspace_size(head, batch, B);
   if (ws_bytes < need) return fail(DLS_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, need);
   if (!workspace || !aligned(workspace, 256)) return fail(DLS_ERR_ARG, "workspace is NULL or not 256-byte aligned");
-  if ((s = check_device()) != DLS_OK) return s;
+  int cus = 0;
+  if ((s = check_device(&cus)) != DLS_OK) return s;
+
+  const dls::PersistWorkspace pw = dls::persist_workspace(*head, batch, B);
+  if (head->prepared) {
+    const dls::PersistPlan pl =
+        dls::persist_plan(*head, batch, B, long_dtype, prior != nullptr, persist_groups(cus));
+    if (pl.ok) {
+      const dls::PreparedLayout PL = dls::prepared_layout(*head);
+      const char* pp = (const char*)head->prepared;
+      char* ws = (char*)workspace;
+      dls::PersistArgs pa;
+      pa.T = (const float*)(pp + PL.off_T);
+      pa.wv = (const uint4*)(pp + PL.off_wv);
+      pa.whh = (const uint4*)(pp + PL.off_whh);
+      pa.w_rank = (const dls::bf16_t*)head->w_rank;
+      pa.V = head->V;
+      pa.H = head->H;
+      pa.r = head->r;
+      pa.NT = pl.NT;
+      pa.NG = pl.NG;
+      pa.rpg = pl.rpg;
+      pa.cap_a = pl.cap_a;
+      pa.rows_max = pl.rows_max;
+      pa.lds_region_a = pl.lds_region_a;
+      pa.L = long_logits;
+      pa.last = last_token;
+      pa.prior = prior;
+      pa.batch = batch;
+      pa.B = B;
+      pa.wl = fusion.w_long;
+      pa.al = fusion.alpha;
+      pa.be = prior ? fusion.beta : 0.f;
+      pa.literal = (fusion.flags & DLS_FIRST_ROW_LONG_ONLY) ? 1 : 0;
+      pa.out_tokens = out_tokens;
+      pa.out_stats = out_stats;
+      pa.hdr = (uint32_t*)ws;
+      pa.keys = (uint64_t*)(ws + pw.off_keys);
+      pa.hbuf = (uint64_t*)(ws + pw.off_h);
+      pa.rbuf = (uint64_t*)(ws + pw.off_rho);
+      pa.stats = (uint64_t*)(ws + pw.off_stats);
+      hipError_t e = dls::launch_persistent(pa, pl, long_dtype, (hipStream_t)stream);
+      if (e != hipSuccess) return hip_fail(e, "draft_block persistent launch");
+      return DLS_OK;
+    }
+  }
 
   dls::DraftArgs a;
   a.head = *head;
@@ -211,11 +287,24 @@ dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, 
   if (!prior) a.f.beta = 0.f;
   a.out_tokens = out_tokens;
   a.out_stats = out_stats;
-  a.ws = (char*)workspace;
+  a.ws = (char*)workspace + pw.total;
   a.lay = dls::draft_layout(*head, batch, B);
   hipError_t e = dls::launch_draft(a, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "draft_block launch");
   return DLS_OK;
+}
+
+int dls_draft_block_path(const dls_local_head* head, int32_t batch, int32_t B, dls_dtype long_dtype,
+                         int has_prior) {
+  g_last_error.clear();
+  if (check_head(head) != DLS_OK || !valid_dtype(long_dtype) || batch < 1 || batch > 256 || B < 1 || B > 64)
+    return -1;
+  if (!head->prepared) return 0;
+  int cus = 0;
+  if (check_device(&cus) != DLS_OK) return -1;
+  const dls::PersistPlan pl = dls::persist_plan(*head, batch, B, long_dtype, has_prior != 0, persist_groups(cus));
+  if (!pl.ok) fail(DLS_OK, "%s", pl.why);
+  return pl.ok ? 1 : 0;
 }
 
 dls_status dls_accept_len(const int32_t* draft, const int32_t* target, int32_t batch, int32_t B, int32_t* out_len,

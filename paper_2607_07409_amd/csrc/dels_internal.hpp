@@ -73,4 +73,59 @@ hipError_t launch_draft(const DraftArgs& a, hipStream_t st);
 hipError_t launch_accept(const int32_t* draft, const int32_t* target, int32_t batch, int32_t B,
                          int32_t* out, hipStream_t st);
 
+// ------------------------------------------------------------------------------------------
+// prepared heads and the persistent drafting kernel
+// ------------------------------------------------------------------------------------------
+constexpr int kMaxBatch = 64;              // sequences per call on the persistent path
+constexpr int kMaxG = 256;                 // workgroups (one per CU of a gfx950)
+constexpr size_t kMaxLds = 160 * 1024;     // LDS per CU on gfx950
+constexpr uint64_t kPreparedMagic = 0x50455250534c4544ull;
+
+struct PreparedHeader {
+  uint64_t magic;
+  int32_t V, d, H, r;
+  const void *emb, *w_ih, *w_hh, *w_vocab;
+};
+struct PreparedLayout {
+  int NT, KK;
+  size_t off_T, off_wv, off_whh, total;
+};
+PreparedLayout prepared_layout(const dls_local_head& h);
+hipError_t launch_prepare(const dls_local_head& h, void* buf, hipStream_t st);
+
+struct PersistArgs {
+  const float* T;            // folded input projection [V][3H]
+  const uint4* wv;           // W_vocab tiles in MFMA operand order
+  const uint4* whh;          // W_hh in MFMA operand order, per 16-unit group
+  const bf16_t* w_rank;      // [r][H]
+  int V, H, r, NT, NG, rpg, cap_a, rows_max;
+  size_t lds_region_a;
+  const void* L;             // long logits [batch][B][V]
+  const int32_t* last;
+  const float* prior;
+  int batch, B;
+  float wl, al, be;
+  int literal;
+  int32_t* out_tokens;
+  dls_row_stats* out_stats;
+  uint32_t* hdr;             // [0] call epoch, [1] error word
+  uint64_t* keys;            // [2 sets][2 parities][kMaxBatch][G]
+  uint64_t* hbuf;            // [2 parities][batch][H]
+  uint64_t* rbuf;            // [replicas][2 parities][batch][r]
+  uint64_t* stats;           // [B][batch][G][8] tagged LSE partials
+};
+struct PersistPlan {
+  bool ok;
+  const char* why;
+  int G, NG, rpg, NT, cap_a, rows_max;
+  size_t lds_region_a, lds;
+};
+struct PersistWorkspace {
+  size_t off_keys, off_h, off_rho, off_stats, total;
+};
+__host__ __device__ void persist_tile_range(int w, int G, int NG, int NT, int cap_a, int* t0, int* n);
+PersistPlan persist_plan(const dls_local_head& h, int32_t batch, int32_t B, dls_dtype long_dtype, bool prior, int G);
+PersistWorkspace persist_workspace(const dls_local_head& h, int32_t batch, int32_t B);
+hipError_t launch_persistent(const PersistArgs& pa, const PersistPlan& pl, dls_dtype long_dtype, hipStream_t st);
+
 }  // namespace dls

@@ -34,7 +34,7 @@ __device__ __forceinline__ float dotn(const float* a, const float* b) {
 // ----------------------------------------------------------------------------------
 template <typename WT>
 __global__ __launch_bounds__(kThreads) void k_gru(const WT* __restrict__ emb, const WT* __restrict__ w_ih,
-                                                  const WT* __restrict__ w_hh, int d, int H,
+                                                  const WT* __restrict__ w_hh, int d, int H, int V,
                                                   const int32_t* __restrict__ tok, const float* __restrict__ h_in,
                                                   int h_zero, float* __restrict__ h_out, int batch) {
   constexpr int N = Chunk<WT>::N;
@@ -56,7 +56,8 @@ __global__ __launch_bounds__(kThreads) void k_gru(const WT* __restrict__ emb, co
     for (int b = 0; b < kBC; ++b) {
       ar[b] = az[b] = anx[b] = anh[b] = 0.f;
       const int bb = b0 + b < batch ? b0 + b : b0;
-      xr[b] = emb + (size_t)tok[bb] * d;
+      const int t = tok[bb];
+      xr[b] = emb + (size_t)((unsigned)t < (unsigned)V ? t : 0) * d;   // out-of-range input reads as 0
     }
 #pragma unroll 2
     for (int c = lane; c < dc; c += 64) {
@@ -290,7 +291,7 @@ hipError_t launch_draft_t(const DraftArgs& a, hipStream_t st) {
   for (int j = 0; j < B; ++j) {
     const bool long_only = literal && j == 0;
     if (!long_only) {
-      k_gru<WT><<<(H + kWaves - 1) / kWaves, kThreads, 0, st>>>(emb, w_ih, w_hh, d, H, tok_in, hc,
+      k_gru<WT><<<(H + kWaves - 1) / kWaves, kThreads, 0, st>>>(emb, w_ih, w_hh, d, H, V, tok_in, hc,
                                                                  first_head_step ? 1 : 0, hn, batch);
       if ((e = hipGetLastError()) != hipSuccess) return e;
       k_rank<WT><<<(r + kWaves - 1) / kWaves, kThreads, 0, st>>>(w_rank, H, r, hn, rho, batch);

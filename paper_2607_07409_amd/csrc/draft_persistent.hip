@@ -1,0 +1,861 @@
+// Persistent, weight-stationary DeLS-Spec block drafting (Algorithm 1 decoding loop with
+// the App. A RNN head) for bf16 heads prepared by dls_prepare_head.
+//
+// One workgroup per CU stays resident for the whole block.  Each workgroup owns a
+// contiguous range of 16-row vocabulary tiles of W_vocab: the first tiles live in the
+// AGPRs of its four waves (fed straight into v_mfma_f32_16x16x32_bf16 as the B operand),
+// the rest in LDS.  The first NG = H/16 workgroups ("GRU workgroups") also own 16 hidden
+// units each (their W_hh rows in LDS) and r/NG rows of W_rank.  Per draft position j:
+//
+//   GRU wgs  merge the argmax keys of position j-1 -> tokens u_j (all sequences)
+//            gh = W_hh h_j (MFMA, h split into bf16 hi+lo), gi = T[u_j] (folded table),
+//            gates -> h_{j+1} for the owned units, published
+//            rho_i = SiLU(W_rank h_{j+1}) for the owned rank rows (MFMA), published
+//   all wgs  S = W_vocab rho on the owned tiles (MFMA, rho split hi+lo), fused with the
+//            long logits (prefetched into LDS while waiting), online LSEs and top-2,
+//            one packed argmax key + LSE partials per (sequence, workgroup), published
+//
+// Cross-workgroup data moves through device-coherent 64-bit words that carry a tag
+// (epoch of the call, position); a consumer spins on the word itself until the tag
+// matches, so each hand-off costs one propagation, with no counters and no cache
+// flushes.  Every wait is bounded; on expiry an error word is set and all waves leave.
+#include "dels_internal.hpp"
+
+namespace dls {
+
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+
+constexpr int kT = 256;          // threads per workgroup (one wave per SIMD)
+constexpr int kOps = 64;         // MFMA B operands of 16 bytes per lane held in AGPRs
+constexpr long kMaxSpins = 1L << 22;
+constexpr int kInflight = 8;     // hand-off loads a thread issues before checking any of them
+constexpr int kStageK = 256;     // K chunk of staged hand-off values (16 slots x 256 floats in LDS)
+constexpr int kStatWords = 9;    // tagged words of one published partial
+constexpr int kRhoCopies = 8;    // replicas of the published rank vector (spreads the readers)
+
+__device__ __forceinline__ uint64_t ld64(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st64(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ld32(const uint32_t* p) {
+  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st32(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void stf(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ldf(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// all earlier vector-memory operations of this wave have completed
+__device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+__device__ __forceinline__ uint64_t tagged(float v, uint32_t tag) {
+  return ((uint64_t)tag << 32) | __float_as_uint(v);
+}
+
+// wait until (word >> 32) == tag; false after the spin budget or when another wave failed
+__device__ __forceinline__ bool wait_tag(const uint64_t* p, uint32_t tag, uint32_t* err, uint64_t& v) {
+  v = ld64(p);
+  if ((uint32_t)(v >> 32) == tag) return true;
+  for (long s = 1;; ++s) {
+    __builtin_amdgcn_s_sleep(2);
+    v = ld64(p);
+    if ((uint32_t)(v >> 32) == tag) return true;
+    if ((s & 63) == 0 && ld32(err)) return false;
+    if (s > kMaxSpins) {
+      st32(err, 1u);
+      return false;
+    }
+  }
+}
+// keys carry an 8-bit position tag in their low byte
+__device__ __forceinline__ bool wait_key(const uint64_t* p, uint32_t tag8, uint32_t* err, uint64_t& v) {
+  v = ld64(p);
+  if ((uint32_t)(v & 0xffu) == tag8) return true;
+  for (long s = 1;; ++s) {
+    __builtin_amdgcn_s_sleep(2);
+    v = ld64(p);
+    if ((uint32_t)(v & 0xffu) == tag8) return true;
+    if ((s & 63) == 0 && ld32(err)) return false;
+    if (s > kMaxSpins) {
+      st32(err, 1u);
+      return false;
+    }
+  }
+}
+
+// argmax key: orderable fused value | (2^24 - 1 - index) | position tag
+__device__ __forceinline__ uint64_t make_key(float t1, int i1, uint32_t tag8) {
+  t1 += 0.0f;   // -0 -> +0, so that equal values compare equal
+  const uint32_t u = __float_as_uint(t1);
+  const uint32_t o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  const uint32_t ix = (i1 == 0x7fffffff) ? 0u : (0xffffffu - (uint32_t)i1);
+  return ((uint64_t)o << 32) | ((uint64_t)ix << 8) | tag8;
+}
+__device__ __forceinline__ float key_value(uint64_t k) {
+  const uint32_t o = (uint32_t)(k >> 32);
+  return __uint_as_float((o & 0x80000000u) ? (o & 0x7fffffffu) : ~o);
+}
+__device__ __forceinline__ int key_index(uint64_t k, int V) {
+  const int i = (int)(0xffffffu - (uint32_t)((k >> 8) & 0xffffffu));
+  return i < V ? i : 0;   // no finite value anywhere: the first index
+}
+__device__ __forceinline__ uint64_t key_max(uint64_t a, uint64_t b) { return (a >> 8) >= (b >> 8) ? a : b; }
+
+// fp32 -> bf16 hi + bf16 lo (v = hi + lo to ~2^-17 relative)
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+__device__ __forceinline__ void split_pair(float x0, float x1, uint32_t& hi, uint32_t& lo) {
+  const uint32_t h0 = bf16_rne(x0), h1 = bf16_rne(x1);
+  const uint32_t l0 = bf16_rne(x0 - __uint_as_float(h0 << 16));
+  const uint32_t l1 = bf16_rne(x1 - __uint_as_float(h1 << 16));
+  hi = h0 | (h1 << 16);
+  lo = l0 | (l1 << 16);
+}
+__device__ __forceinline__ void split8(const float* x, uint4& hi, uint4& lo) {
+  split_pair(x[0], x[1], hi.x, lo.x);
+  split_pair(x[2], x[3], hi.y, lo.y);
+  split_pair(x[4], x[5], hi.z, lo.z);
+  split_pair(x[6], x[7], hi.w, lo.w);
+}
+
+__device__ __forceinline__ bf16x8_t as_bf(uint4 v) {
+  union { uint4 u; bf16x8_t b; } c;
+  c.u = v;
+  return c.b;
+}
+__device__ __forceinline__ f32x4_t mfma_vv(uint4 a, uint4 b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(a), as_bf(b), c, 0, 0, 0);
+}
+// B operand resident in AGPRs (the matrix core reads it from there; the compiler keeps
+// track of the MFMA result hazards)
+__device__ __forceinline__ f32x4_t mfma_va(uint4 a, u32x4 b_agpr, f32x4_t c) {
+  union { u32x4 u; bf16x8_t b; } bb;
+  bb.u = b_agpr;
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(a), bb.b, c, 0, 0, 0);
+}
+__device__ __forceinline__ u32x4 to_agpr(uint4 v) {
+  u32x4 r = {v.x, v.y, v.z, v.w};
+  asm volatile("; weights -> agpr" : "=a"(r) : "0"(r));
+  return r;
+}
+
+__device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + __expf(-x)); }
+
+// Online log-sum-exp with one exponential per element: exp(-|x - m|) serves both the case of
+// a new maximum (rescale the sum) and of a smaller value (add it).  -inf adds nothing.
+__device__ __forceinline__ void lse_push(Lse& a, float x) {
+  const float d = x - a.m;
+  const float e = fast_exp2(-fabsf(d) * kLog2e);
+  const bool up = d > 0.f;
+  const float s_new = up ? __builtin_fmaf(a.s, e, 1.0f) : a.s + e;
+  a.s = (x == -INFINITY) ? a.s : s_new;
+  a.m = up ? x : a.m;
+}
+
+// value of the lane N places further along in the same row of 16 lanes (DPP row rotate)
+template <int N>
+__device__ __forceinline__ float row_ror(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x120 + N, 0xf, 0xf, false));
+}
+template <int N>
+__device__ __forceinline__ int row_ror_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, 0x120 + N, 0xf, 0xf, false);
+}
+template <int N>
+__device__ __forceinline__ uint64_t row_ror_u64(uint64_t v) {
+  const uint32_t lo = (uint32_t)row_ror_i<N>((int)(uint32_t)v), hi = (uint32_t)row_ror_i<N>((int)(uint32_t)(v >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+// largest key over the 16 lanes of a row (every lane of the row gets it)
+__device__ __forceinline__ uint64_t row_key_max(uint64_t k) {
+  k = key_max(k, row_ror_u64<8>(k));
+  k = key_max(k, row_ror_u64<4>(k));
+  k = key_max(k, row_ror_u64<2>(k));
+  k = key_max(k, row_ror_u64<1>(k));
+  return k;
+}
+// largest key over the wave (every lane gets it)
+__device__ __forceinline__ uint64_t wave_key_max(uint64_t k) {
+  k = row_key_max(k);
+  k = key_max(k, __shfl_xor(k, 16));
+  k = key_max(k, __shfl_xor(k, 32));
+  return k;
+}
+
+template <int N>
+__device__ __forceinline__ Partial row_ror_partial(const Partial& p) {
+  Partial q;
+  q.L.m = row_ror<N>(p.L.m); q.L.s = row_ror<N>(p.L.s);
+  q.S.m = row_ror<N>(p.S.m); q.S.s = row_ror<N>(p.S.s);
+  q.F.m = row_ror<N>(p.F.m); q.F.s = row_ror<N>(p.F.s);
+  q.t1 = row_ror<N>(p.t1); q.t2 = row_ror<N>(p.t2);
+  q.i1 = row_ror_i<N>(p.i1);
+  q.pad = 0;
+  return q;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------------------------------
+// tile ownership (shared with the host)
+// ------------------------------------------------------------------------------------------
+__host__ __device__ void persist_tile_range(int w, int G, int NG, int NT, int cap_a, int* t0, int* n) {
+  if (NT <= G * cap_a) {
+    const int q = NT / G, rm = NT % G;
+    *t0 = w * q + (w < rm ? w : rm);
+    *n = q + (w < rm ? 1 : 0);
+    return;
+  }
+  const int ga = NG * cap_a;
+  if (w < NG) {
+    *t0 = w * cap_a;
+    *n = cap_a;
+    return;
+  }
+  const int rest = NT - ga, m = G - NG, i = w - NG;
+  const int q = rest / m, rm = rest % m;
+  *t0 = ga + i * q + (i < rm ? i : rm);
+  *n = q + (i < rm ? 1 : 0);
+}
+
+namespace {
+
+// Copy n 16-byte words from global memory into LDS, 8 loads in flight per thread.
+__device__ __forceinline__ void copy_to_lds(uint4* dst, const uint4* src, int n) {
+  for (int base = 0; base < n; base += kT * 8) {
+    uint4 v[8];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      const int i = base + m * kT + (int)threadIdx.x;
+      if (i < n) v[m] = src[i];
+    }
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      const int i = base + m * kT + (int)threadIdx.x;
+      if (i < n) dst[i] = v[m];
+    }
+  }
+}
+
+// Wave 0 spins until the first word of each producer p < np (at src0 + p * pstride) carries
+// the tag, one lane per producer, while the other waves wait at the barrier: the data itself
+// is then read once.  Keeps the polling traffic on a hand-off to one load per producer.
+__device__ __forceinline__ void wait_producers(const uint64_t* src0, size_t pstride, int np, uint32_t tag,
+                                               uint32_t* err) {
+  if (threadIdx.x < 64) {
+    const int l = (int)threadIdx.x;
+    bool done = l >= np;
+    for (long s = 0;; ++s) {
+      if (!done) done = (uint32_t)(ld64(src0 + (size_t)l * pstride) >> 32) == tag;
+      if (__all(done)) break;
+      __builtin_amdgcn_s_sleep(4);
+      if ((s & 63) == 63 && ld32(err)) break;
+      if (s > kMaxSpins) {
+        st32(err, 1u);
+        break;
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// Stage rows x width tagged words (row stride `stride` words) into LDS floats
+// dst[row * width + c].  Every thread issues up to kInflight loads back to back before checking
+// any tag, so a whole stage costs about one round trip; stragglers are re-polled.
+__device__ __forceinline__ bool stage_tagged(const uint64_t* src, int rows, int width, size_t stride, uint32_t tag,
+                                             float* dst, uint32_t* err) {
+  const int n = rows * width;
+  bool ok = true;
+  for (int base = 0; base < n; base += kT * kInflight) {
+    uint64_t v[kInflight];
+#pragma unroll
+    for (int m = 0; m < kInflight; ++m) {
+      const int i = base + m * kT + (int)threadIdx.x;
+      v[m] = i < n ? ld64(src + (size_t)(i / width) * stride + (i % width)) : 0ull;
+    }
+#pragma unroll
+    for (int m = 0; m < kInflight; ++m) {
+      const int i = base + m * kT + (int)threadIdx.x;
+      if (i < n) {
+        if ((uint32_t)(v[m] >> 32) != tag) ok &= wait_tag(src + (size_t)(i / width) * stride + (i % width), tag, err, v[m]);
+        dst[i] = __uint_as_float((uint32_t)v[m]);
+      }
+    }
+  }
+  return ok;
+}
+
+// A operand (16 slots x 32 k) of chunk-local K block kk from staged values s[slot * width + k]:
+// lane (slot n16, group g4) takes k = 32 kk + 8 g4 .. +7, split into bf16 hi + lo.
+__device__ __forceinline__ void stage_operand(const float* s, int width, int nb, int n16, int g4, int kk, uint4& hi,
+                                              uint4& lo) {
+  float x[8];
+  if (n16 < nb) {
+    const float4* q = (const float4*)(s + n16 * width + 32 * kk + 8 * g4);
+    const float4 a = q[0], b = q[1];
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = 0.f;
+  }
+  split8(x, hi, lo);
+}
+
+template <int KK, typename LT, bool PRIOR>
+__global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  constexpr int TPW = kOps / KK;   // AGPR tiles per wave
+  const int w = blockIdx.x, G = gridDim.x, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, n16 = lane & 15, g4 = lane >> 4;
+  const int V = a.V, H = a.H, r = a.r, batch = a.batch, Bk = a.B;
+  const bool gru = w < a.NG;
+  const int KKH = H / 32;
+  uint32_t* err = a.hdr + 1;
+  if (ld32(err)) return;
+  const uint32_t epoch_full = ld32(a.hdr);
+  const uint32_t epoch = epoch_full & 0xffffffu;
+  const int set = (int)(epoch & 1u);
+  const size_t kstride = (size_t)kMaxBatch * G;       // one (set, parity) plane of keys
+
+  int t0, nt;
+  persist_tile_range(w, G, a.NG, a.NT, a.cap_a, &t0, &nt);
+  const int na = nt < a.cap_a ? nt : a.cap_a;
+  const int nl = nt - na;
+  const int v_base = 16 * t0;
+  const int nrows = 16 * nt;
+
+  // ---- LDS carve-up (offsets identical to the host's size computation)
+  char* p = smem;
+  uint4* s_wtiles = (uint4*)p;                      // nl tiles x KK x 64 (non-GRU wgs)
+  uint4* s_whh = (uint4*)p;                         // 3 x KKH x 64 (GRU wgs)
+  bf16_t* s_wrank = (bf16_t*)(p + (size_t)3 * KKH * 1024);   // rpg x H (GRU wgs)
+  p += a.lds_region_a;
+  LT* s_ll = (LT*)p;                                // 16 slots x rows_max long logits
+  p += (size_t)16 * a.rows_max * sizeof(LT);
+  float* s_prior = (float*)p;                       // rows_max
+  p += (size_t)a.rows_max * 4 * (PRIOR ? 1 : 0);
+  // s_stage holds, at different times: staged hand-off values (16 slots x kStageK), the
+  // cross-wave partial sums s_red (12 x 64 x f32x4), the gathered gi (16 x 48) and s_key
+  float* s_stage = (float*)p;
+  f32x4_t* s_red = (f32x4_t*)p;
+  uint64_t* s_key = (uint64_t*)p;                   // 4 waves x kMaxBatch
+  p += (size_t)16 * kStageK * 4;
+  float* s_gh = (float*)p;                          // per M tile: 16 slots x 48 (W_hh h of this step)
+  p += (size_t)((batch + 15) / 16) * 16 * 48 * 4;
+  Partial* s_part = (Partial*)p;                    // 4 waves x 16 slots
+  p += (size_t)4 * 16 * sizeof(Partial);
+  uint64_t* s_wkey = (uint64_t*)p;                  // 4 waves x 16 slots
+  p += (size_t)4 * 16 * 8;
+  int* s_tok = (int*)p;                             // kMaxBatch
+
+  // ---- clear this workgroup's key slots of the other set (read by the next call)
+  for (int i = tid; i < 2 * kMaxBatch; i += kT) {
+    const int par = i / kMaxBatch, b = i % kMaxBatch;
+    st64(a.keys + (size_t)(1 - set) * 2 * kstride + par * kstride + (size_t)b * G + w, 0ull);
+  }
+
+  // ---- resident weights
+  u32x4 wr[kOps];
+#pragma unroll
+  for (int q = 0; q < TPW; ++q) {
+    const int lt = wave * TPW + q;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (lt < na) v = a.wv[((size_t)(t0 + lt) * KK + kk) * 64 + lane];
+      wr[q * KK + kk] = to_agpr(v);
+    }
+  }
+  if (gru) {
+    copy_to_lds(s_whh, a.whh + (size_t)w * 3 * KKH * 64, 3 * KKH * 64);
+    const int rpg = a.rpg;
+    for (int i = tid; i < rpg * H / 8; i += kT) {
+      const int row = i / (H / 8), c = i % (H / 8);
+      *(uint4*)(s_wrank + (size_t)row * H + 8 * c) = *(const uint4*)(a.w_rank + (size_t)(w * rpg + row) * H + 8 * c);
+    }
+  } else {
+    copy_to_lds(s_wtiles, a.wv + ((size_t)(t0 + na) * KK) * 64, nl * KK * 64);
+  }
+  if (PRIOR)
+    for (int i = tid; i < nrows; i += kT) s_prior[i] = v_base + i < V ? a.prior[v_base + i] : 0.f;
+  __syncthreads();
+
+  const LT* L = (const LT*)a.L;
+  const float wl = a.wl, al = a.al, be = a.be;
+  const int mtiles = (batch + 15) / 16;
+
+  // merged tokens of position jm (GRU wgs); workgroup 0 also writes the drafted tokens
+  auto merge_position = [&](int jm) -> bool {
+    const int par = jm & 1;
+    const uint32_t tag8 = (uint32_t)(jm + 1);
+    const uint64_t* kp = a.keys + (size_t)set * 2 * kstride + par * kstride;
+    bool ok = true;
+    // thread i reads the key of workgroup i for kInflight sequences at a time, all in flight
+    for (int b0 = 0; b0 < batch; b0 += kInflight) {
+      uint64_t v[kInflight];
+#pragma unroll
+      for (int m = 0; m < kInflight; ++m)
+        v[m] = (b0 + m < batch && tid < G) ? ld64(kp + (size_t)(b0 + m) * G + tid) : 0ull;
+#pragma unroll
+      for (int m = 0; m < kInflight; ++m) {
+        if (b0 + m < batch) {
+          if (tid < G && (uint32_t)(v[m] & 0xffu) != tag8) ok &= wait_key(kp + (size_t)(b0 + m) * G + tid, tag8, err, v[m]);
+          const uint64_t best = wave_key_max(v[m]);
+          if (lane == 0) s_key[wave * kMaxBatch + b0 + m] = best;
+        }
+      }
+    }
+    __syncthreads();
+    if (tid < batch) {
+      uint64_t best = s_key[tid];
+      for (int k = 1; k < 4; ++k) best = key_max(best, s_key[k * kMaxBatch + tid]);
+      const int tok = key_index(best, V);
+      s_tok[tid] = tok;
+      if (w == 0) a.out_tokens[(size_t)tid * Bk + jm] = tok;
+    }
+    __syncthreads();
+    return ok;
+  };
+
+  // W_hh h for every M tile -> s_gh (the recurrent half of the gate pre-activations)
+  auto recurrent_gates = [&](const uint64_t* hsrc, uint32_t htag) -> bool {
+    for (int mt = 0; mt < mtiles; ++mt) {
+      const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
+      const int HC = (nb * H <= 16 * kStageK || H < kStageK) ? H : kStageK;
+      f32x4_t gacc[3];
+      for (int q = 0; q < 3; ++q) gacc[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int k0 = 0; k0 < H; k0 += HC) {
+        __syncthreads();
+        if (!stage_tagged(hsrc + (size_t)mt * 16 * H + k0, nb, HC, H, htag, s_stage, err)) return false;
+        __syncthreads();
+        for (int kk = wave; kk < HC / 32; kk += 4) {
+          uint4 hi, lo;
+          stage_operand(s_stage, HC, nb, n16, g4, kk, hi, lo);
+#pragma unroll
+          for (int q = 0; q < 3; ++q) {
+            const uint4 bh = s_whh[(q * KKH + k0 / 32 + kk) * 64 + lane];
+            gacc[q] = mfma_vv(hi, bh, gacc[q]);
+            gacc[q] = mfma_vv(lo, bh, gacc[q]);
+          }
+        }
+      }
+      __syncthreads();
+      for (int q = 0; q < 3; ++q) s_red[(wave * 3 + q) * 64 + lane] = gacc[q];
+      __syncthreads();
+      if (wave == 0) {
+        float* gh = s_gh + mt * 16 * 48;
+        for (int q = 0; q < 3; ++q) {
+          f32x4_t sm = s_red[q * 64 + lane];
+          for (int k = 1; k < 4; ++k) sm += s_red[(k * 3 + q) * 64 + lane];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) gh[(4 * g4 + i) * 48 + q * 16 + n16] = sm[i];
+        }
+      }
+    }
+    __syncthreads();
+    return true;
+  };
+
+  for (int j = 0; j < Bk; ++j) {
+    const uint32_t tag = (epoch << 8) | (uint32_t)(j + 1);
+    const uint32_t tag8 = (uint32_t)(j + 1);
+    const int par = j & 1;
+    const bool long_only = a.literal && j == 0;
+    const int hs = a.literal ? j - 1 : j;          // head step index (first one starts from h = 0)
+
+    // ======================= GRU and rank (GRU workgroups) =======================
+    if (gru && !long_only) {
+      const uint32_t tag_prev = (epoch << 8) | (uint32_t)j;   // h published at position j-1
+      const uint64_t* hprev = a.hbuf + (size_t)((j - 1) & 1) * batch * H;
+      uint64_t* hnew = a.hbuf + (size_t)par * batch * H;
+      // W_hh h_j needs no token: computed while the slowest keys of position j-1 arrive
+      if (hs > 0 && !recurrent_gates(hprev, tag_prev)) return;
+      if (j > 0) {
+        if (!merge_position(j - 1)) return;
+      } else {
+        for (int b = tid; b < batch; b += kT) {
+          const int u = a.last[b];
+          s_tok[b] = (unsigned)u < (unsigned)V ? u : 0;   // out-of-range input reads as 0
+        }
+        __syncthreads();
+      }
+      for (int mt = 0; mt < mtiles; ++mt) {
+        const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
+        // the owned units' previous state and the folded input projection gi = T[u_b]: both sets
+        // of loads in flight together
+        uint64_t hv[4];
+        if (wave == 0) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            hv[i] = (hs > 0 && 4 * g4 + i < nb) ? ld64(hprev + (size_t)(mt * 16 + 4 * g4 + i) * H + 16 * w + n16)
+                                                 : 0ull;
+        }
+        float* s_gi = s_stage;
+        for (int i = tid; i < 16 * 48; i += kT) {
+          const int slot = i / 48, q = (i % 48) / 16, u = i % 16;
+          s_gi[i] = slot < nb ? a.T[(size_t)s_tok[mt * 16 + slot] * 3 * H + q * H + 16 * w + u] : 0.f;
+        }
+        __syncthreads();
+        if (wave == 0) {
+          const float* gh = s_gh + mt * 16 * 48;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int slot = 4 * g4 + i, bb = mt * 16 + slot;
+            if (slot < nb) {
+              float hp = 0.f, ghr = 0.f, ghz = 0.f, ghn = 0.f;
+              if (hs > 0) {
+                if ((uint32_t)(hv[i] >> 32) != tag_prev &&
+                    !wait_tag(hprev + (size_t)bb * H + 16 * w + n16, tag_prev, err, hv[i]))
+                  return;
+                hp = __uint_as_float((uint32_t)hv[i]);
+                ghr = gh[slot * 48 + n16];
+                ghz = gh[slot * 48 + 16 + n16];
+                ghn = gh[slot * 48 + 32 + n16];
+              }
+              const float* gi = s_gi + slot * 48;
+              const float rg = sigm(gi[n16] + ghr);
+              const float zg = sigm(gi[16 + n16] + ghz);
+              const float ng = tanhf_(gi[32 + n16] + rg * ghn);
+              st64(hnew + (size_t)bb * H + 16 * w + n16, tagged((1.f - zg) * ng + zg * hp, tag));
+            }
+          }
+        }
+        __syncthreads();
+      }
+      // rho_i = SiLU(W_rank h_{j+1}) for the owned rank rows, on the vector ALUs: the rows of a
+      // wave split its lanes (64 / rpw lanes per row), each lane a strided share of K
+      const int rpg = a.rpg;
+      const int rpw = rpg <= 4 ? 1 : (rpg <= 8 ? 2 : 4);      // rows per wave
+      const int lpr = 64 / rpw;                                // lanes per row
+      const int myrow = wave * rpw + lane / lpr, kl = lane % lpr;
+      for (int mt = 0; mt < mtiles; ++mt) {
+        const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
+        const int HC = (nb * H <= 16 * kStageK || H < kStageK) ? H : kStageK;
+        float acc[16];
+#pragma unroll
+        for (int s = 0; s < 16; ++s) acc[s] = 0.f;
+        wait_producers(hnew + (size_t)mt * 16 * H, 16, a.NG, tag, err);
+        for (int k0 = 0; k0 < H; k0 += HC) {
+          __syncthreads();
+          if (!stage_tagged(hnew + (size_t)mt * 16 * H + k0, nb, HC, H, tag, s_stage, err)) return;
+          __syncthreads();
+          if (myrow < rpg) {
+            const bf16_t* wrow = s_wrank + (size_t)myrow * H + k0;
+            for (int k = 4 * kl; k < HC; k += 4 * lpr) {
+              const uint2 wq = *(const uint2*)(wrow + k);
+              const float w0 = bf16_lo(wq.x), w1 = bf16_hi(wq.x), w2 = bf16_lo(wq.y), w3 = bf16_hi(wq.y);
+#pragma unroll
+              for (int s = 0; s < 16; ++s) {
+                if (s < nb) {
+                  const float4 hq = *(const float4*)(s_stage + s * HC + k);
+                  acc[s] = __builtin_fmaf(w0, hq.x, acc[s]);
+                  acc[s] = __builtin_fmaf(w1, hq.y, acc[s]);
+                  acc[s] = __builtin_fmaf(w2, hq.z, acc[s]);
+                  acc[s] = __builtin_fmaf(w3, hq.w, acc[s]);
+                }
+              }
+            }
+          }
+        }
+        // reduce over the lanes of the row and publish (each rho replica)
+#pragma unroll
+        for (int s = 0; s < 16; ++s) {
+          if (s < nb) {
+            float v = acc[s];
+            v += row_ror<8>(v);
+            v += row_ror<4>(v);
+            v += row_ror<2>(v);
+            v += row_ror<1>(v);
+            if (lpr >= 32) v += __shfl_xor(v, 16);
+            if (lpr >= 64) v += __shfl_xor(v, 32);
+            if (kl == 0 && myrow < rpg) {
+              const uint64_t word = tagged(siluf_(v), tag);
+#pragma unroll
+              for (int c = 0; c < kRhoCopies; ++c)
+                st64(a.rbuf + ((size_t)c * 2 + par) * batch * r + (size_t)(mt * 16 + s) * r + w * rpg + myrow, word);
+            }
+          }
+        }
+      }
+      __syncthreads();
+    }
+
+    // ======================= vocabulary head + fused combine (all workgroups) =======================
+    for (int mt = 0; mt < mtiles; ++mt) {
+      const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
+      // long logits of the owned rows (independent of rho: in flight while rho is awaited)
+      for (int i = tid; i < nb * nrows; i += kT) {
+        const int slot = i / nrows, row = i % nrows;
+        const int v = v_base + row;
+        s_ll[slot * a.rows_max + row] = v < V ? L[((size_t)(mt * 16 + slot) * Bk + j) * V + v] : LT(0);
+      }
+      // rho of the slots, staged, then as bf16 hi + lo A operands
+      uint4 ahi[KK], alo[KK];
+      if (!long_only) {
+        const uint64_t* rsrc = a.rbuf + ((size_t)(w % kRhoCopies) * 2 + par) * batch * r + (size_t)mt * 16 * r;
+        wait_producers(rsrc, (size_t)a.rpg, a.NG, tag, err);
+        if (!stage_tagged(rsrc, nb, r, r, tag, s_stage, err)) return;
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) stage_operand(s_stage, r, nb, n16, g4, kk, ahi[kk], alo[kk]);
+      }
+      __syncthreads();   // s_ll complete, s_stage free again
+
+      Partial P[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) P[i] = partial_empty();
+
+      auto fold_tile = [&](const f32x4_t& acc, int lt) {
+        const int row = 16 * lt + n16;
+        const int v = v_base + row;
+        const bool vin = v < V;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int slot = 4 * g4 + i;
+          if (i < nb) {   // uniform: skips slot sets no lane holds
+            if (slot < nb && vin) {
+              const float x = to_f32(s_ll[slot * a.rows_max + row]);
+              float f;
+              if (long_only) {
+                f = wl * x;
+              } else {
+                const float s = acc[i];
+                f = __builtin_fmaf(al, s, wl * x);
+                if (PRIOR) f = __builtin_fmaf(-be, s_prior[row], f);
+                lse_push(P[i].S, s);
+              }
+              lse_push(P[i].L, x);
+              lse_push(P[i].F, f);
+              top2_push(P[i], f, v);
+            }
+          }
+        }
+      };
+
+      // AGPR-resident tiles of this wave, two at a time: four independent MFMA chains
+      // (hi and lo halves of rho for each tile) keep the matrix pipe busy
+#pragma unroll
+      for (int q = 0; q < TPW; q += 2) {
+        const int lt = wave * TPW + q;
+        if (lt < na) {
+          f32x4_t c0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, c1 = c0, c2 = c0, c3 = c0;
+          if (!long_only) {
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+              c0 = mfma_va(ahi[kk], wr[q * KK + kk], c0);
+              c1 = mfma_va(alo[kk], wr[q * KK + kk], c1);
+              c2 = mfma_va(ahi[kk], wr[(q + 1) * KK + kk], c2);
+              c3 = mfma_va(alo[kk], wr[(q + 1) * KK + kk], c3);
+            }
+          }
+          fold_tile(c0 + c1, lt);
+          if (lt + 1 < na) fold_tile(c2 + c3, lt + 1);
+        }
+      }
+      // LDS-resident tiles, round robin over the waves
+      for (int lq = wave; lq < nl; lq += 4) {
+        f32x4_t c0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, c1 = c0;
+        if (!long_only) {
+#pragma unroll
+          for (int kk = 0; kk < KK; ++kk) {
+            const uint4 bw = s_wtiles[((size_t)lq * KK + kk) * 64 + lane];
+            c0 = mfma_vv(ahi[kk], bw, c0);
+            c1 = mfma_vv(alo[kk], bw, c1);
+          }
+        }
+        fold_tile(c0 + c1, na + lq);
+      }
+      // argmax key of each slot: max over the 16 lanes of a row (DPP), then over the waves
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (i < nb) {
+          const uint64_t k = row_key_max(make_key(P[i].t1, P[i].i1, tag8));
+          if (n16 == 0) s_wkey[wave * 16 + 4 * g4 + i] = k;
+        }
+      }
+      __syncthreads();
+      if (tid < nb) {
+        uint64_t k = s_wkey[tid];
+        for (int q = 1; q < 4; ++q) k = key_max(k, s_wkey[q * 16 + tid]);
+        st64(a.keys + (size_t)set * 2 * kstride + par * kstride + (size_t)(mt * 16 + tid) * G + w, k);
+      }
+      // the full partials (LSEs, top-2) for the row statistics: off the critical path
+      if (a.out_stats) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (i < nb) {
+            P[i] = partial_merge(P[i], row_ror_partial<8>(P[i]));
+            P[i] = partial_merge(P[i], row_ror_partial<4>(P[i]));
+            P[i] = partial_merge(P[i], row_ror_partial<2>(P[i]));
+            P[i] = partial_merge(P[i], row_ror_partial<1>(P[i]));
+            if (n16 == 0) s_part[wave * 16 + 4 * g4 + i] = P[i];
+          }
+        }
+        __syncthreads();
+        if (tid < nb) {
+          Partial T = s_part[tid];
+          for (int q = 1; q < 4; ++q) T = partial_merge(T, s_part[q * 16 + tid]);
+          uint64_t* sp = a.stats + (((size_t)j * batch + mt * 16 + tid) * G + w) * kStatWords;
+          st64(sp + 0, tagged(T.L.m, tag)); st64(sp + 1, tagged(T.L.s, tag));
+          st64(sp + 2, tagged(T.S.m, tag)); st64(sp + 3, tagged(T.S.s, tag));
+          st64(sp + 4, tagged(T.F.m, tag)); st64(sp + 5, tagged(T.F.s, tag));
+          st64(sp + 6, tagged(T.t1, tag)); st64(sp + 7, tagged(T.t2, tag));
+          st64(sp + 8, tagged(__int_as_float(T.i1), tag));
+        }
+      }
+      __syncthreads();
+    }
+  }
+
+  // ---- the last position's tokens (workgroup 0)
+  if (w == 0) {
+    if (!merge_position(Bk - 1)) return;
+  }
+  // ---- row statistics: row (b, j) is merged by workgroup (b * B + j) % G from the tagged partials
+  if (a.out_stats) {
+    for (int q = w; q < batch * Bk; q += G) {
+      const int b = q / Bk, jm = q % Bk;
+      const uint32_t stag = (epoch << 8) | (uint32_t)(jm + 1);
+      Partial P = partial_empty();
+      if (tid < G) {
+        const uint64_t* sp = a.stats + (((size_t)jm * batch + b) * G + tid) * kStatWords;
+        uint64_t w9[kStatWords];
+#pragma unroll
+        for (int e = 0; e < kStatWords; ++e) w9[e] = ld64(sp + e);
+        float q9[kStatWords];
+#pragma unroll
+        for (int e = 0; e < kStatWords; ++e) {
+          if ((uint32_t)(w9[e] >> 32) != stag && !wait_tag(sp + e, stag, err, w9[e])) return;
+          q9[e] = __uint_as_float((uint32_t)w9[e]);
+        }
+        P.L.m = q9[0]; P.L.s = q9[1];
+        P.S.m = q9[2]; P.S.s = q9[3];
+        P.F.m = q9[4]; P.F.s = q9[5];
+        P.t1 = q9[6]; P.t2 = q9[7];
+        P.i1 = __float_as_int(q9[8]);
+      }
+      P = block_merge(P, s_part, 4);
+      if (tid == 0) {
+        int dummy;
+        finalize_row(P, wl, al, a.literal && jm == 0, &dummy, a.out_stats + (size_t)b * Bk + jm, nullptr);
+      }
+      __syncthreads();
+    }
+  }
+  if (w == 0 && tid == 0) {
+    vm_wait();
+    st32(a.hdr, epoch_full + 1u);
+  }
+}
+
+template <int KK, typename LT, bool PRIOR>
+hipError_t launch_k(const PersistArgs& pa, int G, size_t lds, hipStream_t st) {
+  auto kern = k_draft_persistent<KK, LT, PRIOR>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  PersistArgs copy = pa;
+  void* args[] = {&copy};
+  return hipLaunchCooperativeKernel((const void*)kern, dim3(G), dim3(kT), args, (unsigned)lds, st);
+}
+
+template <typename LT, bool PRIOR>
+hipError_t launch_kk(const PersistArgs& pa, int G, size_t lds, hipStream_t st) {
+  switch (pa.r / 32) {
+    case 4: return launch_k<4, LT, PRIOR>(pa, G, lds, st);
+    case 8: return launch_k<8, LT, PRIOR>(pa, G, lds, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+PersistPlan persist_plan(const dls_local_head& h, int32_t batch, int32_t B, dls_dtype long_dtype, bool prior,
+                         int G) {
+  PersistPlan pl;
+  pl.ok = false;
+  const int KK = h.r / 32;
+  // r = 128 or 256: the vocabulary tiles of a wave fill its 256 AGPRs without spills
+  if (h.dtype != DLS_BF16 || h.r % 32 || !(KK == 4 || KK == 8) || h.H % 32 ||
+      batch < 1 || batch > kMaxBatch || B < 1 || B > 64 || h.V >= (1 << 24) || G < 1 || G > kMaxG) {
+    pl.why = "shape outside the persistent kernel's range";
+    return pl;
+  }
+  const int NG = h.H / 16;
+  if (h.H > kStageK && h.H % kStageK) {
+    pl.why = "H above 256 must be a multiple of 256";
+    return pl;
+  }
+  if (NG > G || h.r % NG || h.r / NG > 16) {
+    pl.why = "hidden size / rank do not split over the workgroups";
+    return pl;
+  }
+  pl.G = G;
+  pl.NG = NG;
+  pl.rpg = h.r / NG;
+  pl.NT = (h.V + 15) / 16;
+  pl.cap_a = 4 * (kOps / KK);
+  int rows_max = 0, nl_max = 0;
+  for (int w = 0; w < G; ++w) {
+    int t0, n;
+    persist_tile_range(w, G, NG, pl.NT, pl.cap_a, &t0, &n);
+    rows_max = std::max(rows_max, 16 * n);
+    if (w >= NG) nl_max = std::max(nl_max, n - std::min(n, pl.cap_a));
+    else if (n > pl.cap_a) {
+      pl.why = "vocabulary tiles exceed the GRU workgroups' AGPRs";
+      return pl;
+    }
+  }
+  const size_t region_gru = (size_t)3 * (h.H / 32) * 1024 + (size_t)pl.rpg * h.H * 2;
+  const size_t region_tiles = (size_t)nl_max * KK * 1024;
+  pl.lds_region_a = (std::max(region_gru, region_tiles) + 15) & ~(size_t)15;
+  pl.rows_max = rows_max;
+  const size_t esz = long_dtype == DLS_BF16 ? 2 : 4;
+  size_t lds = pl.lds_region_a + (size_t)16 * rows_max * esz;
+  lds = (lds + 15) & ~(size_t)15;
+  if (prior) lds += (size_t)rows_max * 4;
+  lds += (size_t)16 * kStageK * 4 + (size_t)((batch + 15) / 16) * 16 * 48 * 4 + (size_t)4 * 16 * sizeof(Partial) +
+         (size_t)4 * 16 * 8 + (size_t)kMaxBatch * 4;
+  pl.lds = lds;
+  if (lds > kMaxLds) {
+    pl.why = "per-workgroup LDS need exceeds 160 KiB";
+    return pl;
+  }
+  pl.ok = true;
+  return pl;
+}
+
+PersistWorkspace persist_workspace(const dls_local_head& h, int32_t batch, int32_t B) {
+  PersistWorkspace L;
+  size_t o = 256;                                     // header: epoch, error word
+  L.off_keys = o;
+  o += (size_t)2 * 2 * kMaxBatch * kMaxG * 8;
+  L.off_h = o;
+  o += (size_t)2 * batch * h.H * 8;
+  L.off_rho = o;
+  o += (size_t)kRhoCopies * 2 * batch * h.r * 8;
+  L.off_stats = o;
+  o += (size_t)B * batch * kMaxG * kStatWords * 8;
+  L.total = (o + 255) & ~(size_t)255;
+  return L;
+}
+
+hipError_t launch_persistent(const PersistArgs& pa, const PersistPlan& pl, dls_dtype long_dtype, hipStream_t st) {
+  const bool pr = pa.prior != nullptr;
+  if (long_dtype == DLS_BF16)
+    return pr ? launch_kk<bf16_t, true>(pa, pl.G, pl.lds, st) : launch_kk<bf16_t, false>(pa, pl.G, pl.lds, st);
+  return pr ? launch_kk<float, true>(pa, pl.G, pl.lds, st) : launch_kk<float, false>(pa, pl.G, pl.lds, st);
+}
+
+}  // namespace dls

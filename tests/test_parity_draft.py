@@ -24,23 +24,41 @@ def _problem(name, init, V=None, d=None, H=None, r=None, Bk=None, batch=None, dt
     if kw:
         wl = wl.with_(**kw)
     hw = W.make_head(wl, init)
-    return dict(wl=wl, hw=hw, head=B.LocalHead.from_weights(hw), oracle=O.RnnHead.from_weights(hw),
+    head = B.LocalHead.from_weights(hw)
+    return dict(wl=wl, hw=hw, head=head, oracle=O.RnnHead.from_weights(hw),
                 long_h=W.make_long_logits(wl), last=W.make_last_token(wl),
-                prior=W.make_zipf_log_prior(wl.V, wl.seed))
+                prior=W.make_zipf_log_prior(wl.V, wl.seed), prepared=None)
 
 
-def _draft(p, alpha, beta=0.0, with_prior=False, literal=False, long_h=None):
+def _head(p, prepared):
+    """The unprepared head, or a prepared twin sharing its weight tensors."""
+    if not prepared:
+        return p["head"]
+    if p["prepared"] is None:
+        h = p["head"]
+        p["prepared"] = B.LocalHead(h.emb, h.w_ih, h.w_hh, h.w_rank, h.w_vocab).prepare()
+    return p["prepared"]
+
+
+def _draft(p, alpha, beta=0.0, with_prior=False, literal=False, long_h=None, prepared=False, expect_path=None):
     long_h = p["long_h"] if long_h is None else long_h
     lt = B.as_tensor(long_h)
     last = torch.from_numpy(p["last"]).cuda()
     prior = torch.from_numpy(p["prior"]).cuda() if with_prior else None
-    tok, st = B.draft_block(p["head"], lt, last, prior, 1.0, alpha, beta, first_row_long_only=literal)
+    head = _head(p, prepared)
+    path = head.path(lt.shape[0], lt.shape[1], lt.dtype, with_prior)
+    if expect_path is not None:
+        assert path == expect_path, f"draft path {path}, expected {expect_path}"
+    ws = B.draft_workspace(head, lt.shape[0], lt.shape[1])
+    tok, st = B.draft_block(head, lt, last, prior, 1.0, alpha, beta, first_row_long_only=literal, workspace=ws)
     torch.cuda.synchronize()
+    assert B.workspace_error(ws) == 0
     return tok.cpu().numpy(), st.cpu().numpy()
 
 
-def _check(p, alpha, beta=0.0, with_prior=False, literal=False, sequences=None):
-    tok, st = _draft(p, alpha, beta, with_prior, literal)
+def _check(p, alpha, beta=0.0, with_prior=False, literal=False, sequences=None, prepared=False):
+    tok, st = _draft(p, alpha, beta, with_prior, literal, prepared=prepared,
+                     expect_path=1 if prepared else 0)
     rep = check_draft(tok, st, p["oracle"], p["long_h"], p["last"], p["prior"] if with_prior else None,
                       1.0, alpha, beta if with_prior else 0.0, literal, sequences)
     print(f"{p['wl'].name}: near_ties={rep['near_ties']} fusion_active={rep['fusion_active']:.2f} "
@@ -72,43 +90,109 @@ def test_mixed_dtypes():
     check_draft(tok, st, p["oracle"], lb, p["last"], None, 1.0, 0.5, 0.0)
 
 
+@pytest.mark.parametrize("prepared", [False, True])
 @pytest.mark.parametrize("init", ["baseline", "stress"])
-def test_qwen3_4b_b1(init):
+def test_qwen3_4b_b1(init, prepared):
     p = _problem("qwen3-4b-b1", init)
-    tok, st, rep = _check(p, 0.5)
+    tok, st, rep = _check(p, 0.5, prepared=prepared)
     if init == "stress":
         assert rep["fusion_active"] > 0.3
     # literal first-row reading on the same inputs
-    _check(p, 0.5, literal=True)
+    _check(p, 0.5, literal=True, prepared=prepared)
 
 
+@pytest.mark.parametrize("prepared", [False, True])
 @pytest.mark.parametrize("alpha", [0.25, 0.5, 1.0])
-def test_qwen3_8b_b1_alpha_sweep(alpha):
+def test_qwen3_8b_b1_alpha_sweep(alpha, prepared):
     p = _problem("qwen3-8b-b1", "stress")
-    _check(p, alpha)
+    _check(p, alpha, prepared=prepared)
 
 
-def test_qwen3_8b_b1_alpha_zero_is_dflash():
+@pytest.mark.parametrize("prepared", [False, True])
+def test_qwen3_8b_b1_alpha_zero_is_dflash(prepared):
     p = _problem("qwen3-8b-b1", "stress")
-    tok, _ = _draft(p, 0.0)
+    tok, _ = _draft(p, 0.0, prepared=prepared)
     assert np.array_equal(tok, np.argmax(np.asarray(p["long_h"], np.float32), axis=2))
 
 
+@pytest.mark.parametrize("prepared", [False, True])
 @pytest.mark.parametrize("init", ["baseline", "stress"])
-def test_serving_b16(init):
+def test_serving_b16(init, prepared):
     p = _problem("qwen3-8b-b16", init)
-    _check(p, 0.5, sequences=[0, 5, 10, 15])
+    _check(p, 0.5, sequences=[0, 5, 10, 15], prepared=prepared)
 
 
-def test_serving_b64():
+@pytest.mark.parametrize("prepared", [False, True])
+def test_serving_b64(prepared):
     p = _problem("b64-d5120", "stress")
-    _check(p, 0.5, sequences=[0, 21, 42, 63])
+    _check(p, 0.5, sequences=[0, 21, 42, 63], prepared=prepared)
 
 
-def test_serving_b64_prior():
+@pytest.mark.parametrize("prepared", [False, True])
+def test_serving_b64_prior(prepared):
     """beta = alpha with the Zipf log-prior (the paper's alpha = beta diagonal)."""
     p = _problem("b64-d5120", "stress")
-    _check(p, 0.5, 0.5, with_prior=True, sequences=[1, 62])
+    _check(p, 0.5, 0.5, with_prior=True, sequences=[1, 62], prepared=prepared)
+
+
+# ---------------------------------------------------------------------------------------------
+# persistent kernel on small shapes (oracle in seconds): ragged vocabularies, few tiles per CU,
+# both first-row readings, the prior, float32 long logits, batches spanning several 16-slot tiles
+# ---------------------------------------------------------------------------------------------
+SMALL = [
+    dict(V=5003, d=96, H=128, r=128, Bk=7, batch=3),
+    dict(V=7001, d=64, H=256, r=256, Bk=9, batch=2),
+    dict(V=1024, d=64, H=128, r=128, Bk=4, batch=1),
+    dict(V=4099, d=128, H=128, r=128, Bk=5, batch=37),
+]
+
+
+@pytest.mark.parametrize("shape", range(len(SMALL)))
+@pytest.mark.parametrize("literal", [False, True])
+def test_persistent_small(shape, literal):
+    sh = SMALL[shape]
+    p = _problem("qwen3-8b-b16", "stress", dtype="bf16", **sh)
+    seqs = list(range(min(sh["batch"], 6))) + ([sh["batch"] - 1] if sh["batch"] > 6 else [])
+    _, _, rep = _check(p, 0.7, literal=literal, prepared=True, sequences=seqs)
+    assert rep["fusion_active"] > 0.2
+
+
+@pytest.mark.parametrize("shape", [0, 3])
+def test_persistent_small_prior(shape):
+    p = _problem("qwen3-8b-b16", "stress", dtype="bf16", **SMALL[shape])
+    _check(p, 0.5, 0.5, with_prior=True, prepared=True, sequences=[0, 1, 2])
+
+
+def test_persistent_f32_long_logits():
+    p = _problem("qwen3-8b-b16", "stress", dtype="bf16", **SMALL[0])
+    lf = np.asarray(p["long_h"], np.float32) + np.float32(1e-3)     # not bf16-representable
+    tok, st = _draft(p, 0.5, long_h=lf, prepared=True, expect_path=1)
+    check_draft(tok, st, p["oracle"], lf, p["last"], None, 1.0, 0.5, 0.0)
+
+
+def test_persistent_repeat_and_paths_agree():
+    """Back-to-back calls on one workspace (the epoch tags of the hand-offs advance every call)
+    are bit-identical, and agree with the per-position launches on the tokens."""
+    p = _problem("qwen3-8b-b16", "stress", dtype="bf16", **SMALL[1])
+    head = _head(p, True)
+    lt = B.as_tensor(p["long_h"])
+    last = torch.from_numpy(p["last"]).cuda()
+    ws = B.draft_workspace(head, lt.shape[0], lt.shape[1])
+    outs = []
+    for i in range(6):
+        tok, st = B.draft_block(head, lt, last, None, 1.0, 0.5, 0.0, first_row_long_only=bool(i % 2), workspace=ws)
+        outs.append((tok.clone(), st.clone()))
+    torch.cuda.synchronize()
+    assert B.workspace_error(ws) == 0
+    for i in range(2, 6):   # bit patterns: the literal reading's first row has NaN lse_short
+        assert torch.equal(outs[i][0], outs[i % 2][0])
+        assert torch.equal(outs[i][1].view(torch.int32), outs[i % 2][1].view(torch.int32))
+    tok1, _ = _draft(p, 0.5, prepared=False)
+    tok_p, _ = _draft(p, 0.5, prepared=True)
+    ref = O.draft_block(p["oracle"], p["long_h"], p["last"], None, 1.0, 0.5, 0.0)
+    for t in (tok1, tok_p):
+        near = (t != ref.tokens)
+        assert np.all(ref.gap[near] < TOL)
 
 
 @pytest.mark.parametrize("name", ["tiny", "qwen3-4b-b1", "qwen3-8b-b16"])
@@ -144,9 +228,10 @@ def test_accept_len_cases():
         assert np.array_equal(got.cpu().numpy(), O.accept_len(d, t)), (batch, Bk)
 
 
-def test_draft_deterministic():
+@pytest.mark.parametrize("prepared", [False, True])
+def test_draft_deterministic(prepared):
     p = _problem("qwen3-4b-b1", "stress")
-    t0, s0 = _draft(p, 0.5)
+    t0, s0 = _draft(p, 0.5, prepared=prepared)
     for _ in range(3):
-        t1, s1 = _draft(p, 0.5)
-        assert np.array_equal(t0, t1) and np.array_equal(s0, s1)
+        t1, s1 = _draft(p, 0.5, prepared=prepared)
+        assert np.array_equal(t0, t1) and np.array_equal(s0.view(np.int32), s1.view(np.int32))
