@@ -8,12 +8,16 @@
 // units each (their W_hh rows in LDS) and r/NG rows of W_rank.  Per draft position j:
 //
 //   GRU wgs  merge the argmax keys of position j-1 -> tokens u_j (all sequences)
-//            gh = W_hh h_j (MFMA, h split into bf16 hi+lo), gi = T[u_j] (folded table),
-//            gates -> h_{j+1} for the owned units, published
-//            rho_i = SiLU(W_rank h_{j+1}) for the owned rank rows (MFMA), published
-//   all wgs  S = W_vocab rho on the owned tiles (MFMA, rho split hi+lo), fused with the
-//            long logits (prefetched into LDS while waiting), online LSEs and top-2,
-//            one packed argmax key + LSE partials per (sequence, workgroup), published
+//            gi = T[u_j] (folded table) + gh (from the previous step) -> gates -> h_{j+1}
+//            of the owned units, published
+//            rho_i = SiLU(W_rank h_{j+1}) for the owned rank rows (MFMA), published; then
+//            gh = W_hh h_{j+1} for the next position from the same staged h (MFMA)
+//   all wgs  S = W_vocab rho on the owned tiles (MFMA), fused with the long logits
+//            (prefetched into LDS while waiting), online LSEs and top-2; one packed argmax
+//            key per (sequence, workgroup) published first, the LSE partials after it
+//
+// fp32 activations enter the bf16 matrix cores as two bf16 halves (hi + lo), split once
+// when they are staged into LDS.
 //
 // Cross-workgroup data moves through device-coherent 64-bit words that carry a tag
 // (epoch of the call, position); a consumer spins on the word itself until the tag
@@ -30,7 +34,8 @@ typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 
 constexpr int kT = 256;          // threads per workgroup (one wave per SIMD)
-constexpr int kOps = 64;         // MFMA B operands of 16 bytes per lane held in AGPRs
+constexpr int kOps = 56;         // MFMA B operands of 16 bytes per lane held in AGPRs (224 of
+                                 // the 256; the rest take the accumulators)
 constexpr long kMaxSpins = 1L << 22;
 constexpr int kInflight = 8;     // hand-off loads a thread issues before checking any of them
 constexpr int kStageK = 256;     // K chunk of staged hand-off values (16 slots x 256 floats in LDS)
@@ -232,14 +237,15 @@ __host__ __device__ void persist_tile_range(int w, int G, int NG, int NT, int ca
 
 namespace {
 
-// Copy n 16-byte words from global memory into LDS, 8 loads in flight per thread.
+// Copy n 16-byte words from global memory into LDS, 8 loads in flight per thread (indices past
+// the end re-read the last word, so that every load is unconditional).
 __device__ __forceinline__ void copy_to_lds(uint4* dst, const uint4* src, int n) {
   for (int base = 0; base < n; base += kT * 8) {
     uint4 v[8];
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
       const int i = base + m * kT + (int)threadIdx.x;
-      if (i < n) v[m] = src[i];
+      v[m] = src[i < n ? i : n - 1];
     }
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
@@ -271,46 +277,79 @@ __device__ __forceinline__ void wait_producers(const uint64_t* src0, size_t pstr
   __syncthreads();
 }
 
-// Stage rows x width tagged words (row stride `stride` words) into LDS floats
-// dst[row * width + c].  Every thread issues up to kInflight loads back to back before checking
-// any tag, so a whole stage costs about one round trip; stragglers are re-polled.
-__device__ __forceinline__ bool stage_tagged(const uint64_t* src, int rows, int width, size_t stride, uint32_t tag,
-                                             float* dst, uint32_t* err) {
-  const int n = rows * width;
+// Operand planes: staged hand-off values as bf16 hi and lo halves, 16 slots x (K + 8) each
+// (the 8-element pad spreads the slots' rows over the LDS banks).
+constexpr int kPlane = 16 * (kStageK + 8);
+
+// one staged value: its bf16 hi and lo halves (hi + lo = x to about 2^-17 relative)
+__device__ __forceinline__ void put_split(uint16_t* hi, uint16_t* lo, int idx, uint32_t bits) {
+  const float x = __uint_as_float(bits);
+  const uint32_t h = bf16_rne(x);
+  hi[idx] = (uint16_t)h;
+  lo[idx] = (uint16_t)bf16_rne(x - __uint_as_float(h << 16));
+}
+
+// Stage rows x width tagged words (row stride `stride` words) into the operand planes at
+// [row * pitch + c].  Every thread issues kInflight loads back to back before checking any tag
+// (one round trip per stage); words that were not ready yet are re-polled one by one.
+__device__ __forceinline__ bool stage_split(const uint64_t* src, int rows, int width, size_t stride, uint32_t tag,
+                                            uint16_t* hi, uint16_t* lo, int pitch, uint32_t* err) {
+  const int q = kT / width, rm = kT % width;
+  int row = (int)threadIdx.x / width, col = (int)threadIdx.x % width;
   bool ok = true;
-  for (int base = 0; base < n; base += kT * kInflight) {
+  for (int base = 0; base < rows * width; base += kT * kInflight) {
     uint64_t v[kInflight];
+    int rr[kInflight], cc[kInflight];
 #pragma unroll
     for (int m = 0; m < kInflight; ++m) {
-      const int i = base + m * kT + (int)threadIdx.x;
-      v[m] = i < n ? ld64(src + (size_t)(i / width) * stride + (i % width)) : 0ull;
+      rr[m] = row;
+      cc[m] = col;
+      v[m] = row < rows ? ld64(src + (size_t)row * stride + col) : 0ull;
+      col += rm;
+      row += q;
+      if (col >= width) {
+        col -= width;
+        ++row;
+      }
     }
+    uint32_t bad = 0;
 #pragma unroll
     for (int m = 0; m < kInflight; ++m) {
-      const int i = base + m * kT + (int)threadIdx.x;
-      if (i < n) {
-        if ((uint32_t)(v[m] >> 32) != tag) ok &= wait_tag(src + (size_t)(i / width) * stride + (i % width), tag, err, v[m]);
-        dst[i] = __uint_as_float((uint32_t)v[m]);
+      if (rr[m] < rows) {
+        if ((uint32_t)(v[m] >> 32) == tag) put_split(hi, lo, rr[m] * pitch + cc[m], (uint32_t)v[m]);
+        else bad |= 1u << m;
+      }
+    }
+#pragma unroll 1
+    for (int m = 0; bad; ++m, bad >>= 1) {
+      if (bad & 1u) {
+        const int e = base + m * kT + (int)threadIdx.x;
+        const int r0 = e / width, c0 = e % width;
+        uint64_t x;
+        ok &= wait_tag(src + (size_t)r0 * stride + c0, tag, err, x);
+        put_split(hi, lo, r0 * pitch + c0, (uint32_t)x);
       }
     }
   }
   return ok;
 }
 
-// A operand (16 slots x 32 k) of chunk-local K block kk from staged values s[slot * width + k]:
-// lane (slot n16, group g4) takes k = 32 kk + 8 g4 .. +7, split into bf16 hi + lo.
-__device__ __forceinline__ void stage_operand(const float* s, int width, int nb, int n16, int g4, int kk, uint4& hi,
-                                              uint4& lo) {
-  float x[8];
-  if (n16 < nb) {
-    const float4* q = (const float4*)(s + n16 * width + 32 * kk + 8 * g4);
-    const float4 a = q[0], b = q[1];
-    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
-  } else {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) x[e] = 0.f;
-  }
-  split8(x, hi, lo);
+// Workgroup barrier that also tells whether any thread failed.  A failure is final (all waves
+// leave), so the LDS flag is set once and never cleared.
+__device__ __forceinline__ bool fail_barrier(bool failed, volatile int* s_fail) {
+  if (failed) *s_fail = 1;
+  __syncthreads();
+  return *s_fail != 0;
+}
+
+// A operand (16 slots x 32 k) at column k of the planes: lane (slot n16, group g4) takes
+// k + 8 g4 .. +7 of its slot.  Lanes of slots >= nb read slot 0 instead: an MFMA output row
+// depends on its own A row only, and the rows of empty slots are never used.
+__device__ __forceinline__ void plane_operand(const uint16_t* hi, const uint16_t* lo, int pitch, int nb, int n16,
+                                              int g4, int k, uint4& ahi, uint4& alo) {
+  const int o = (n16 < nb ? n16 : 0) * pitch + k + 8 * g4;
+  ahi = *(const uint4*)(hi + o);
+  alo = *(const uint4*)(lo + o);
 }
 
 template <int KK, typename LT, bool PRIOR>
@@ -319,7 +358,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   constexpr int TPW = kOps / KK;   // AGPR tiles per wave
   const int w = blockIdx.x, G = gridDim.x, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, n16 = lane & 15, g4 = lane >> 4;
-  const int V = a.V, H = a.H, r = a.r, batch = a.batch, Bk = a.B;
+  const int V = a.V, H = a.H, r = a.r, batch = a.batch, Bk = a.B, rpg = a.rpg;
   const bool gru = w < a.NG;
   const int KKH = H / 32;
   uint32_t* err = a.hdr + 1;
@@ -335,6 +374,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   const int nl = nt - na;
   const int v_base = 16 * t0;
   const int nrows = 16 * nt;
+  const int mtiles = (batch + 15) / 16;
+  const int ll_slots = batch < 16 ? batch : 16;
 
   // ---- LDS carve-up (offsets identical to the host's size computation)
   char* p = smem;
@@ -342,23 +383,29 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   uint4* s_whh = (uint4*)p;                         // 3 x KKH x 64 (GRU wgs)
   bf16_t* s_wrank = (bf16_t*)(p + (size_t)3 * KKH * 1024);   // rpg x H (GRU wgs)
   p += a.lds_region_a;
-  LT* s_ll = (LT*)p;                                // 16 slots x rows_max long logits
-  p += (size_t)16 * a.rows_max * sizeof(LT);
+  LT* s_ll = (LT*)p;                                // ll_slots x rows_max long logits
+  p += ((size_t)ll_slots * a.rows_max * sizeof(LT) + 15) & ~(size_t)15;
   float* s_prior = (float*)p;                       // rows_max
   p += (size_t)a.rows_max * 4 * (PRIOR ? 1 : 0);
-  // s_stage holds, at different times: staged hand-off values (16 slots x kStageK), the
-  // cross-wave partial sums s_red (12 x 64 x f32x4), the gathered gi (16 x 48) and s_key
-  float* s_stage = (float*)p;
+  // operand planes; at other times the gh partials (12 x 64 x f32x4) and the gathered gi (16 x 48)
+  uint16_t* s_hi = (uint16_t*)p;
+  uint16_t* s_lo = s_hi + kPlane;
   f32x4_t* s_red = (f32x4_t*)p;
-  uint64_t* s_key = (uint64_t*)p;                   // 4 waves x kMaxBatch
-  p += (size_t)16 * kStageK * 4;
-  float* s_gh = (float*)p;                          // per M tile: 16 slots x 48 (W_hh h of this step)
-  p += (size_t)((batch + 15) / 16) * 16 * 48 * 4;
+  float* s_gi = (float*)p;
+  p += (size_t)2 * kPlane * 2;
+  f32x4_t* s_rred = (f32x4_t*)p;                    // rank partials [wave][g4][rpg]
+  p += (size_t)16 * rpg * 16;
+  float* s_gh = (float*)p;                          // per M tile: 16 slots x 48 (W_hh h for the next step)
+  p += (size_t)mtiles * 16 * 48 * 4;
   Partial* s_part = (Partial*)p;                    // 4 waves x 16 slots
   p += (size_t)4 * 16 * sizeof(Partial);
-  uint64_t* s_wkey = (uint64_t*)p;                  // 4 waves x 16 slots
-  p += (size_t)4 * 16 * 8;
+  uint64_t* s_wkey = (uint64_t*)p;                  // 4 waves x 16 slots; the merge's per-sequence maxima
+  uint64_t* s_best = s_wkey;
+  p += (size_t)kMaxBatch * 8;
   int* s_tok = (int*)p;                             // kMaxBatch
+  p += (size_t)kMaxBatch * 4;
+  volatile int* s_fail = (volatile int*)p;          // sticky failure flag
+  if (tid == 0) *s_fail = 0;
 
   // ---- clear this workgroup's key slots of the other set (read by the next call)
   for (int i = tid; i < 2 * kMaxBatch; i += kT) {
@@ -367,7 +414,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   }
 
   // ---- resident weights
-  u32x4 wr[kOps];
+  u32x4 wr[TPW * KK];
 #pragma unroll
   for (int q = 0; q < TPW; ++q) {
     const int lt = wave * TPW + q;
@@ -380,7 +427,6 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   }
   if (gru) {
     copy_to_lds(s_whh, a.whh + (size_t)w * 3 * KKH * 64, 3 * KKH * 64);
-    const int rpg = a.rpg;
     for (int i = tid; i < rpg * H / 8; i += kT) {
       const int row = i / (H / 8), c = i % (H / 8);
       *(uint4*)(s_wrank + (size_t)row * H + 8 * c) = *(const uint4*)(a.w_rank + (size_t)(w * rpg + row) * H + 8 * c);
@@ -394,75 +440,44 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
 
   const LT* L = (const LT*)a.L;
   const float wl = a.wl, al = a.al, be = a.be;
-  const int mtiles = (batch + 15) / 16;
 
-  // merged tokens of position jm (GRU wgs); workgroup 0 also writes the drafted tokens
+  // Tokens of position jm (the argmax keys of all workgroups, max-reduced through LDS atomics)
+  // into s_tok; workgroup 0 also writes the drafted tokens.  Workgroup-uniform result.
   auto merge_position = [&](int jm) -> bool {
-    const int par = jm & 1;
     const uint32_t tag8 = (uint32_t)(jm + 1);
-    const uint64_t* kp = a.keys + (size_t)set * 2 * kstride + par * kstride;
+    const uint64_t* kp = a.keys + (size_t)set * 2 * kstride + (size_t)(jm & 1) * kstride;
+    for (int b = tid; b < batch; b += kT) s_best[b] = 0ull;
+    __syncthreads();
     bool ok = true;
-    // thread i reads the key of workgroup i for kInflight sequences at a time, all in flight
-    for (int b0 = 0; b0 < batch; b0 += kInflight) {
-      uint64_t v[kInflight];
+    if (tid < G) {
+      for (int b0 = 0; b0 < batch; b0 += kInflight) {
+        uint64_t v[kInflight];
 #pragma unroll
-      for (int m = 0; m < kInflight; ++m)
-        v[m] = (b0 + m < batch && tid < G) ? ld64(kp + (size_t)(b0 + m) * G + tid) : 0ull;
+        for (int m = 0; m < kInflight; ++m)
+          v[m] = b0 + m < batch ? ld64(kp + (size_t)(b0 + m) * G + tid) : 0ull;
+        uint32_t bad = 0;
 #pragma unroll
-      for (int m = 0; m < kInflight; ++m) {
-        if (b0 + m < batch) {
-          if (tid < G && (uint32_t)(v[m] & 0xffu) != tag8) ok &= wait_key(kp + (size_t)(b0 + m) * G + tid, tag8, err, v[m]);
-          const uint64_t best = wave_key_max(v[m]);
-          if (lane == 0) s_key[wave * kMaxBatch + b0 + m] = best;
+        for (int m = 0; m < kInflight; ++m) {
+          if (b0 + m < batch) {
+            if ((uint32_t)(v[m] & 0xffu) == tag8) atomicMax((unsigned long long*)&s_best[b0 + m], v[m]);
+            else bad |= 1u << m;
+          }
         }
-      }
-    }
-    __syncthreads();
-    if (tid < batch) {
-      uint64_t best = s_key[tid];
-      for (int k = 1; k < 4; ++k) best = key_max(best, s_key[k * kMaxBatch + tid]);
-      const int tok = key_index(best, V);
-      s_tok[tid] = tok;
-      if (w == 0) a.out_tokens[(size_t)tid * Bk + jm] = tok;
-    }
-    __syncthreads();
-    return ok;
-  };
-
-  // W_hh h for every M tile -> s_gh (the recurrent half of the gate pre-activations)
-  auto recurrent_gates = [&](const uint64_t* hsrc, uint32_t htag) -> bool {
-    for (int mt = 0; mt < mtiles; ++mt) {
-      const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
-      const int HC = (nb * H <= 16 * kStageK || H < kStageK) ? H : kStageK;
-      f32x4_t gacc[3];
-      for (int q = 0; q < 3; ++q) gacc[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      for (int k0 = 0; k0 < H; k0 += HC) {
-        __syncthreads();
-        if (!stage_tagged(hsrc + (size_t)mt * 16 * H + k0, nb, HC, H, htag, s_stage, err)) return false;
-        __syncthreads();
-        for (int kk = wave; kk < HC / 32; kk += 4) {
-          uint4 hi, lo;
-          stage_operand(s_stage, HC, nb, n16, g4, kk, hi, lo);
-#pragma unroll
-          for (int q = 0; q < 3; ++q) {
-            const uint4 bh = s_whh[(q * KKH + k0 / 32 + kk) * 64 + lane];
-            gacc[q] = mfma_vv(hi, bh, gacc[q]);
-            gacc[q] = mfma_vv(lo, bh, gacc[q]);
+#pragma unroll 1
+        for (int m = 0; bad; ++m, bad >>= 1) {
+          if (bad & 1u) {
+            uint64_t k;
+            ok &= wait_key(kp + (size_t)(b0 + m) * G + tid, tag8, err, k);
+            atomicMax((unsigned long long*)&s_best[b0 + m], k);
           }
         }
       }
-      __syncthreads();
-      for (int q = 0; q < 3; ++q) s_red[(wave * 3 + q) * 64 + lane] = gacc[q];
-      __syncthreads();
-      if (wave == 0) {
-        float* gh = s_gh + mt * 16 * 48;
-        for (int q = 0; q < 3; ++q) {
-          f32x4_t sm = s_red[q * 64 + lane];
-          for (int k = 1; k < 4; ++k) sm += s_red[(k * 3 + q) * 64 + lane];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) gh[(4 * g4 + i) * 48 + q * 16 + n16] = sm[i];
-        }
-      }
+    }
+    if (fail_barrier(!ok, s_fail)) return false;
+    if (tid < batch) {
+      const int tok = key_index(s_best[tid], V);
+      s_tok[tid] = tok;
+      if (w == 0) a.out_tokens[(size_t)tid * Bk + jm] = tok;
     }
     __syncthreads();
     return true;
@@ -473,15 +488,13 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     const uint32_t tag8 = (uint32_t)(j + 1);
     const int par = j & 1;
     const bool long_only = a.literal && j == 0;
-    const int hs = a.literal ? j - 1 : j;          // head step index (first one starts from h = 0)
+    const int hs = a.literal ? j - 1 : j;          // head step index (the first one starts from h = 0)
 
     // ======================= GRU and rank (GRU workgroups) =======================
     if (gru && !long_only) {
       const uint32_t tag_prev = (epoch << 8) | (uint32_t)j;   // h published at position j-1
       const uint64_t* hprev = a.hbuf + (size_t)((j - 1) & 1) * batch * H;
       uint64_t* hnew = a.hbuf + (size_t)par * batch * H;
-      // W_hh h_j needs no token: computed while the slowest keys of position j-1 arrive
-      if (hs > 0 && !recurrent_gates(hprev, tag_prev)) return;
       if (j > 0) {
         if (!merge_position(j - 1)) return;
       } else {
@@ -491,23 +504,22 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         }
         __syncthreads();
       }
+      // gates of the owned units: gi = T[u] (folded input projection), gh from the previous step
       for (int mt = 0; mt < mtiles; ++mt) {
         const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
-        // the owned units' previous state and the folded input projection gi = T[u_b]: both sets
-        // of loads in flight together
-        uint64_t hv[4];
+        uint64_t hv[4];   // the owned units' previous state, in flight together with the gather
         if (wave == 0) {
 #pragma unroll
           for (int i = 0; i < 4; ++i)
             hv[i] = (hs > 0 && 4 * g4 + i < nb) ? ld64(hprev + (size_t)(mt * 16 + 4 * g4 + i) * H + 16 * w + n16)
                                                  : 0ull;
         }
-        float* s_gi = s_stage;
         for (int i = tid; i < 16 * 48; i += kT) {
           const int slot = i / 48, q = (i % 48) / 16, u = i % 16;
           s_gi[i] = slot < nb ? a.T[(size_t)s_tok[mt * 16 + slot] * 3 * H + q * H + 16 * w + u] : 0.f;
         }
         __syncthreads();
+        bool ok = true;
         if (wave == 0) {
           const float* gh = s_gh + mt * 16 * 48;
 #pragma unroll
@@ -516,9 +528,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
             if (slot < nb) {
               float hp = 0.f, ghr = 0.f, ghz = 0.f, ghn = 0.f;
               if (hs > 0) {
-                if ((uint32_t)(hv[i] >> 32) != tag_prev &&
-                    !wait_tag(hprev + (size_t)bb * H + 16 * w + n16, tag_prev, err, hv[i]))
-                  return;
+                if ((uint32_t)(hv[i] >> 32) != tag_prev)
+                  ok &= wait_tag(hprev + (size_t)bb * H + 16 * w + n16, tag_prev, err, hv[i]);
                 hp = __uint_as_float((uint32_t)hv[i]);
                 ghr = gh[slot * 48 + n16];
                 ghz = gh[slot * 48 + 16 + n16];
@@ -532,86 +543,114 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
             }
           }
         }
-        __syncthreads();
+        if (fail_barrier(!ok, s_fail)) return;
       }
-      // rho_i = SiLU(W_rank h_{j+1}) for the owned rank rows, on the vector ALUs: the rows of a
-      // wave split its lanes (64 / rpw lanes per row), each lane a strided share of K
-      const int rpg = a.rpg;
-      const int rpw = rpg <= 4 ? 1 : (rpg <= 8 ? 2 : 4);      // rows per wave
-      const int lpr = 64 / rpw;                                // lanes per row
-      const int myrow = wave * rpw + lane / lpr, kl = lane % lpr;
+      // rho_i = SiLU(W_rank h_{j+1}) for the owned rank rows (MFMA over the staged h, K split
+      // over the waves), then W_hh h_{j+1} for the next position from the same staged h
       for (int mt = 0; mt < mtiles; ++mt) {
         const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
-        const int HC = (nb * H <= 16 * kStageK || H < kStageK) ? H : kStageK;
-        float acc[16];
-#pragma unroll
-        for (int s = 0; s < 16; ++s) acc[s] = 0.f;
-        wait_producers(hnew + (size_t)mt * 16 * H, 16, a.NG, tag, err);
+        const int HC = nb * (H + 8) <= kPlane ? H : kStageK;
+        const int pitch = HC + 8;
+        const uint64_t* hsrc = hnew + (size_t)mt * 16 * H;
+        wait_producers(hsrc, 16, a.NG, tag, err);
+        bool ok = true;
+        f32x4_t racc = f32x4_t{0.f, 0.f, 0.f, 0.f};
         for (int k0 = 0; k0 < H; k0 += HC) {
+          if (k0) __syncthreads();
+          ok &= stage_split(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
           __syncthreads();
-          if (!stage_tagged(hnew + (size_t)mt * 16 * H + k0, nb, HC, H, tag, s_stage, err)) return;
-          __syncthreads();
-          if (myrow < rpg) {
-            const bf16_t* wrow = s_wrank + (size_t)myrow * H + k0;
-            for (int k = 4 * kl; k < HC; k += 4 * lpr) {
-              const uint2 wq = *(const uint2*)(wrow + k);
-              const float w0 = bf16_lo(wq.x), w1 = bf16_hi(wq.x), w2 = bf16_lo(wq.y), w3 = bf16_hi(wq.y);
+          for (int kk = wave; kk < HC / 32; kk += 4) {
+            uint4 ahi, alo;
+            plane_operand(s_hi, s_lo, pitch, nb, n16, g4, 32 * kk, ahi, alo);
+            const uint4 bw = n16 < rpg ? *(const uint4*)(s_wrank + (size_t)n16 * H + k0 + 32 * kk + 8 * g4)
+                                       : make_uint4(0, 0, 0, 0);
+            racc = mfma_vv(ahi, bw, racc);
+            racc = mfma_vv(alo, bw, racc);
+          }
+        }
+        if (n16 < rpg) s_rred[(wave * 4 + g4) * rpg + n16] = racc;
+        if (fail_barrier(!ok, s_fail)) return;
+        if (wave == 0 && n16 < rpg) {
+          f32x4_t sm = s_rred[g4 * rpg + n16];
+          for (int q = 1; q < 4; ++q) sm += s_rred[(q * 4 + g4) * rpg + n16];
 #pragma unroll
-              for (int s = 0; s < 16; ++s) {
-                if (s < nb) {
-                  const float4 hq = *(const float4*)(s_stage + s * HC + k);
-                  acc[s] = __builtin_fmaf(w0, hq.x, acc[s]);
-                  acc[s] = __builtin_fmaf(w1, hq.y, acc[s]);
-                  acc[s] = __builtin_fmaf(w2, hq.z, acc[s]);
-                  acc[s] = __builtin_fmaf(w3, hq.w, acc[s]);
-                }
+          for (int i = 0; i < 4; ++i) {
+            const int slot = 4 * g4 + i;
+            if (slot < nb) {
+              const uint64_t word = tagged(siluf_(sm[i]), tag);
+              for (int c = 0; c < kRhoCopies; ++c)
+                st64(a.rbuf + ((size_t)c * 2 + par) * batch * r + (size_t)(mt * 16 + slot) * r + w * rpg + n16, word);
+            }
+          }
+        }
+        if (j + 1 < Bk) {
+          f32x4_t gacc[3];
+          for (int q = 0; q < 3; ++q) gacc[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+          for (int k0 = 0; k0 < H; k0 += HC) {
+            if (HC < H) {   // several chunks: stage each again (all of h is there by now)
+              __syncthreads();
+              ok &= stage_split(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
+              __syncthreads();
+            }
+            for (int kk = wave; kk < HC / 32; kk += 4) {
+              uint4 ahi, alo;
+              plane_operand(s_hi, s_lo, pitch, nb, n16, g4, 32 * kk, ahi, alo);
+#pragma unroll
+              for (int q = 0; q < 3; ++q) {
+                const uint4 bh = s_whh[(q * KKH + k0 / 32 + kk) * 64 + lane];
+                gacc[q] = mfma_vv(ahi, bh, gacc[q]);
+                gacc[q] = mfma_vv(alo, bh, gacc[q]);
               }
             }
           }
-        }
-        // reduce over the lanes of the row and publish (each rho replica)
+          __syncthreads();   // planes read: their space takes the partial sums
+          for (int q = 0; q < 3; ++q) s_red[(wave * 3 + q) * 64 + lane] = gacc[q];
+          __syncthreads();
+          if (wave == 0) {
+            float* gh = s_gh + mt * 16 * 48;
+            for (int q = 0; q < 3; ++q) {
+              f32x4_t sm = s_red[q * 64 + lane];
+              for (int k = 1; k < 4; ++k) sm += s_red[(k * 3 + q) * 64 + lane];
 #pragma unroll
-        for (int s = 0; s < 16; ++s) {
-          if (s < nb) {
-            float v = acc[s];
-            v += row_ror<8>(v);
-            v += row_ror<4>(v);
-            v += row_ror<2>(v);
-            v += row_ror<1>(v);
-            if (lpr >= 32) v += __shfl_xor(v, 16);
-            if (lpr >= 64) v += __shfl_xor(v, 32);
-            if (kl == 0 && myrow < rpg) {
-              const uint64_t word = tagged(siluf_(v), tag);
-#pragma unroll
-              for (int c = 0; c < kRhoCopies; ++c)
-                st64(a.rbuf + ((size_t)c * 2 + par) * batch * r + (size_t)(mt * 16 + s) * r + w * rpg + myrow, word);
+              for (int i = 0; i < 4; ++i) gh[(4 * g4 + i) * 48 + q * 16 + n16] = sm[i];
             }
           }
         }
+        if (fail_barrier(!ok, s_fail)) return;
       }
-      __syncthreads();
     }
 
     // ======================= vocabulary head + fused combine (all workgroups) =======================
     for (int mt = 0; mt < mtiles; ++mt) {
       const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
       // long logits of the owned rows (independent of rho: in flight while rho is awaited)
-      for (int i = tid; i < nb * nrows; i += kT) {
-        const int slot = i / nrows, row = i % nrows;
-        const int v = v_base + row;
-        s_ll[slot * a.rows_max + row] = v < V ? L[((size_t)(mt * 16 + slot) * Bk + j) * V + v] : LT(0);
+      for (int slot = 0; slot < nb; ++slot) {
+        const LT* src = L + ((size_t)(mt * 16 + slot) * Bk + j) * V + v_base;
+        LT* dst = s_ll + (size_t)slot * a.rows_max;
+        for (int r0 = 0; r0 < nrows; r0 += 4 * kT) {
+          LT x[4];
+#pragma unroll
+          for (int m = 0; m < 4; ++m) {
+            const int row = r0 + m * kT + tid;
+            x[m] = (row < nrows && v_base + row < V) ? src[row] : LT(0);
+          }
+#pragma unroll
+          for (int m = 0; m < 4; ++m) {
+            const int row = r0 + m * kT + tid;
+            if (row < nrows) dst[row] = x[m];
+          }
+        }
       }
-      // rho of the slots, staged, then as bf16 hi + lo A operands
-      uint4 ahi[KK], alo[KK];
+      // rho of the slots, staged as bf16 hi + lo planes (the A operands are read from there
+      // at each K block: holding all of them would crowd out the accumulators)
       if (!long_only) {
         const uint64_t* rsrc = a.rbuf + ((size_t)(w % kRhoCopies) * 2 + par) * batch * r + (size_t)mt * 16 * r;
-        wait_producers(rsrc, (size_t)a.rpg, a.NG, tag, err);
-        if (!stage_tagged(rsrc, nb, r, r, tag, s_stage, err)) return;
-        __syncthreads();
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) stage_operand(s_stage, r, nb, n16, g4, kk, ahi[kk], alo[kk]);
+        wait_producers(rsrc, (size_t)rpg, a.NG, tag, err);
+        const bool ok = stage_split(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err);
+        if (fail_barrier(!ok, s_fail)) return;
+      } else {
+        __syncthreads();   // s_ll complete
       }
-      __syncthreads();   // s_ll complete, s_stage free again
 
       Partial P[4];
 #pragma unroll
@@ -649,19 +688,25 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
 #pragma unroll
       for (int q = 0; q < TPW; q += 2) {
         const int lt = wave * TPW + q;
+        const bool two = q + 1 < TPW;   // constant once unrolled (TPW may be odd)
+        const int q2 = two ? q + 1 : q;
         if (lt < na) {
           f32x4_t c0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, c1 = c0, c2 = c0, c3 = c0;
           if (!long_only) {
 #pragma unroll
             for (int kk = 0; kk < KK; ++kk) {
-              c0 = mfma_va(ahi[kk], wr[q * KK + kk], c0);
-              c1 = mfma_va(alo[kk], wr[q * KK + kk], c1);
-              c2 = mfma_va(ahi[kk], wr[(q + 1) * KK + kk], c2);
-              c3 = mfma_va(alo[kk], wr[(q + 1) * KK + kk], c3);
+              uint4 ahi, alo;
+              plane_operand(s_hi, s_lo, r + 8, nb, n16, g4, 32 * kk, ahi, alo);
+              c0 = mfma_va(ahi, wr[q * KK + kk], c0);
+              c1 = mfma_va(alo, wr[q * KK + kk], c1);
+              if (two) {
+                c2 = mfma_va(ahi, wr[q2 * KK + kk], c2);
+                c3 = mfma_va(alo, wr[q2 * KK + kk], c3);
+              }
             }
           }
           fold_tile(c0 + c1, lt);
-          if (lt + 1 < na) fold_tile(c2 + c3, lt + 1);
+          if (two && lt + 1 < na) fold_tile(c2 + c3, lt + 1);
         }
       }
       // LDS-resident tiles, round robin over the waves
@@ -670,9 +715,11 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         if (!long_only) {
 #pragma unroll
           for (int kk = 0; kk < KK; ++kk) {
+            uint4 ahi, alo;
+            plane_operand(s_hi, s_lo, r + 8, nb, n16, g4, 32 * kk, ahi, alo);
             const uint4 bw = s_wtiles[((size_t)lq * KK + kk) * 64 + lane];
-            c0 = mfma_vv(ahi[kk], bw, c0);
-            c1 = mfma_vv(alo[kk], bw, c1);
+            c0 = mfma_vv(ahi, bw, c0);
+            c1 = mfma_vv(alo, bw, c1);
           }
         }
         fold_tile(c0 + c1, na + lq);
@@ -729,6 +776,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       const int b = q / Bk, jm = q % Bk;
       const uint32_t stag = (epoch << 8) | (uint32_t)(jm + 1);
       Partial P = partial_empty();
+      bool ok = true;
       if (tid < G) {
         const uint64_t* sp = a.stats + (((size_t)jm * batch + b) * G + tid) * kStatWords;
         uint64_t w9[kStatWords];
@@ -737,7 +785,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         float q9[kStatWords];
 #pragma unroll
         for (int e = 0; e < kStatWords; ++e) {
-          if ((uint32_t)(w9[e] >> 32) != stag && !wait_tag(sp + e, stag, err, w9[e])) return;
+          if ((uint32_t)(w9[e] >> 32) != stag) ok &= wait_tag(sp + e, stag, err, w9[e]);
           q9[e] = __uint_as_float((uint32_t)w9[e]);
         }
         P.L.m = q9[0]; P.L.s = q9[1];
@@ -746,6 +794,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         P.t1 = q9[6]; P.t2 = q9[7];
         P.i1 = __float_as_int(q9[8]);
       }
+      if (fail_barrier(!ok, s_fail)) return;
       P = block_merge(P, s_part, 4);
       if (tid == 0) {
         int dummy;
@@ -822,11 +871,11 @@ PersistPlan persist_plan(const dls_local_head& h, int32_t batch, int32_t B, dls_
   pl.lds_region_a = (std::max(region_gru, region_tiles) + 15) & ~(size_t)15;
   pl.rows_max = rows_max;
   const size_t esz = long_dtype == DLS_BF16 ? 2 : 4;
-  size_t lds = pl.lds_region_a + (size_t)16 * rows_max * esz;
-  lds = (lds + 15) & ~(size_t)15;
+  const int ll_slots = batch < 16 ? batch : 16;
+  size_t lds = pl.lds_region_a + (((size_t)ll_slots * rows_max * esz + 15) & ~(size_t)15);
   if (prior) lds += (size_t)rows_max * 4;
-  lds += (size_t)16 * kStageK * 4 + (size_t)((batch + 15) / 16) * 16 * 48 * 4 + (size_t)4 * 16 * sizeof(Partial) +
-         (size_t)4 * 16 * 8 + (size_t)kMaxBatch * 4;
+  lds += (size_t)2 * kPlane * 2 + (size_t)16 * pl.rpg * 16 + (size_t)((batch + 15) / 16) * 16 * 48 * 4 +
+         (size_t)4 * 16 * sizeof(Partial) + (size_t)kMaxBatch * 8 + (size_t)kMaxBatch * 4 + 16;
   pl.lds = lds;
   if (lds > kMaxLds) {
     pl.why = "per-workgroup LDS need exceeds 160 KiB";
