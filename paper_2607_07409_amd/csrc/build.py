@@ -17,6 +17,9 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-Wall", "-Wno-unused-function",
          # no packed fp32 arithmetic in any generated code
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         # LDS atomics stay single instructions: the default rewrite into a scalar loop over the
+         # active lanes costs about a microsecond per wave in the persistent kernel's key merge
+         "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
          "-I", os.path.join(ROOT, "include")]
 
 

@@ -641,13 +641,15 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
           }
         }
       }
-      // rho of the slots, staged as bf16 hi + lo planes (the A operands are read from there
-      // at each K block: holding all of them would crowd out the accumulators)
+      // rho of the slots, staged as bf16 hi + lo planes, then held as the A operands
+      uint4 ahi[KK], alo[KK];
       if (!long_only) {
         const uint64_t* rsrc = a.rbuf + ((size_t)(w % kRhoCopies) * 2 + par) * batch * r + (size_t)mt * 16 * r;
         wait_producers(rsrc, (size_t)rpg, a.NG, tag, err);
         const bool ok = stage_split(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err);
         if (fail_barrier(!ok, s_fail)) return;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) plane_operand(s_hi, s_lo, r + 8, nb, n16, g4, 32 * kk, ahi[kk], alo[kk]);
       } else {
         __syncthreads();   // s_ll complete
       }
@@ -695,13 +697,11 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
           if (!long_only) {
 #pragma unroll
             for (int kk = 0; kk < KK; ++kk) {
-              uint4 ahi, alo;
-              plane_operand(s_hi, s_lo, r + 8, nb, n16, g4, 32 * kk, ahi, alo);
-              c0 = mfma_va(ahi, wr[q * KK + kk], c0);
-              c1 = mfma_va(alo, wr[q * KK + kk], c1);
+              c0 = mfma_va(ahi[kk], wr[q * KK + kk], c0);
+              c1 = mfma_va(alo[kk], wr[q * KK + kk], c1);
               if (two) {
-                c2 = mfma_va(ahi, wr[q2 * KK + kk], c2);
-                c3 = mfma_va(alo, wr[q2 * KK + kk], c3);
+                c2 = mfma_va(ahi[kk], wr[q2 * KK + kk], c2);
+                c3 = mfma_va(alo[kk], wr[q2 * KK + kk], c3);
               }
             }
           }
@@ -715,11 +715,9 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         if (!long_only) {
 #pragma unroll
           for (int kk = 0; kk < KK; ++kk) {
-            uint4 ahi, alo;
-            plane_operand(s_hi, s_lo, r + 8, nb, n16, g4, 32 * kk, ahi, alo);
             const uint4 bw = s_wtiles[((size_t)lq * KK + kk) * 64 + lane];
-            c0 = mfma_vv(ahi, bw, c0);
-            c1 = mfma_vv(alo, bw, c1);
+            c0 = mfma_vv(ahi[kk], bw, c0);
+            c1 = mfma_vv(alo[kk], bw, c1);
           }
         }
         fold_tile(c0 + c1, na + lq);
