@@ -44,6 +44,33 @@ def compulsory_bytes_per_block(wl, esize=2):
     return once + wl.B * wl.batch * (3 * H * 4 + V * esize)
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_draft_persistent_qwen3-4b-b1_traffic.txt")
+KERNEL_SOURCES = ["paper_2607_07409_amd/csrc/draft_persistent.hip", "paper_2607_07409_amd/csrc/dels_internal.hpp",
+                  "paper_2607_07409_amd/csrc/dels_device.hpp", "paper_2607_07409_amd/csrc/build.py"]
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch of the persistent kernel from the committed PMC counter record, or None
+    when there is none for this workload or the kernel sources changed after it was taken."""
+    if workload != "qwen3-4b-b1" or not os.path.exists(TRAFFIC_FILE):
+        return None
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    rec = {}
+    with open(TRAFFIC_FILE) as fh:
+        for line in fh:
+            if line.startswith("#") or ":" not in line:
+                continue
+            k, v = line.split(":", 1)
+            rec[k.strip()] = v.split()[0] if v.split() else ""
+    if rec.get("kernel_source_sha256") != h.hexdigest():
+        return None
+    return int(rec["traffic_bytes_per_launch"])
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -55,6 +82,9 @@ def main():
     ap.add_argument("--combine-rows", type=int, default=1024)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-only", action="store_true",
+                    help="for hardware-counter runs: only --steps draft blocks and a 1 GiB device copy "
+                         "(the copy calibrates the HBM byte counters); no JSON line")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -84,6 +114,22 @@ def main():
     path = head.path(wl.batch, wl.B, L.dtype, False)
     log(f"draft path: {'persistent' if path == 1 else 'per-position launches'}")
     last_t = torch.from_numpy(last).to(dev)
+
+    if args.profile_only:
+        tok = torch.empty((wl.batch, wl.B), dtype=torch.int32, device=dev)
+        st = torch.empty((wl.batch, wl.B, 6), dtype=torch.float32, device=dev)
+        ws = B.draft_workspace(head, wl.batch, wl.B, dev)
+        for _ in range(args.steps):
+            B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws)
+        src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)      # 1 GiB read + 1 GiB written per copy
+        torch.cuda.synchronize()
+        assert B.workspace_error(ws) == 0, "persistent kernel reported a stalled hand-off"
+        log(f"profile run done: {args.steps} draft blocks, 3 copies of 1 GiB")
+        return
 
     # ---- CPU oracle leg (also provides the target tokens) -------------------------------------
     cpu = None
@@ -158,7 +204,8 @@ def main():
     achieved = alg_block / (blk_us * 1e-6) / 1e9
     comp = compulsory_bytes_per_block(wl)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": measured_traffic(wl.name) if path == 1 else None,
                 "kernel": "k_draft_persistent (one launch per block)" if path == 1 else
                           "dls_draft_block (all launches of one block)",
                 "us_per_launch": round(blk_us, 2),

@@ -23,6 +23,8 @@
 // (epoch of the call, position); a consumer spins on the word itself until the tag
 // matches, so each hand-off costs one propagation, with no counters and no cache
 // flushes.  Every wait is bounded; on expiry an error word is set and all waves leave.
+#include <atomic>
+
 #include "dels_internal.hpp"
 
 namespace dls {
@@ -810,8 +812,19 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
 template <int KK, typename LT, bool PRIOR>
 hipError_t launch_k(const PersistArgs& pa, int G, size_t lds, hipStream_t st) {
   auto kern = k_draft_persistent<KK, LT, PRIOR>;
-  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  // the dynamic LDS limit is raised to the maximum once per device (a per-call attribute
+  // change costs microseconds of host time)
+  static std::atomic<uint64_t> raised{0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
+  const uint64_t bit = dev < 64 ? (uint64_t)1 << dev : 0;
+  if (!bit || !(raised.load(std::memory_order_acquire) & bit)) {
+    e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
+    if (e != hipSuccess) return e;
+    raised.fetch_or(bit, std::memory_order_acq_rel);
+  }
+  (void)lds;
   PersistArgs copy = pa;
   void* args[] = {&copy};
   return hipLaunchCooperativeKernel((const void*)kern, dim3(G), dim3(kT), args, (unsigned)lds, st);

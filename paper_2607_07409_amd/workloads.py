@@ -6,7 +6,7 @@ the method's arithmetic (no fusion, no GRU, no softmax, no argmax), so both the
 CPU oracle side and the HIP side of a test can consume the same inputs.
 
 Shapes follow the paper's setting: Qwen3 vocabulary (V = 151,936), block size
-16 (Sec. 5.1), GRU hidden 1024 and rank 256 (App. A, Table 5), embedding
+16 (Sec. 5.1), GRU hidden 1024 and rank 256 (App. A, Table 6), embedding
 widths 2560 / 4096 / 5120.  bf16 inputs are produced by rounding fp32 draws to
 bf16 (round to nearest, ties to even); both sides see the identical bf16
 values.

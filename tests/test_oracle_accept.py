@@ -3,7 +3,7 @@ and the add-smoothing unigram prior.
 
 * closed forms of the acceptance length on constructed targets;
 * E[tau] = sum_i rate_i (tail-sum formula) on any sample;
-* the paper's printed Table 3 gain ratios (Sec. 5.5) and Table 7 rate curves (App. D);
+* the paper's printed Table 3 gain ratios (Sec. 5.5) and Table 8 rate curves (App. D);
 * the prior of App. A on small hand-checked counts.
 """
 import json
@@ -49,10 +49,10 @@ def test_tau_tail_sum():
     assert abs(rate.sum() - O.tau(acc).mean()) < 1e-12
 
 
-def test_table7_rate_curve():
-    """A population whose acceptance-length frequencies are read off the paper's Table 7
+def test_table8_rate_curve():
+    """A population whose acceptance-length frequencies are read off the paper's Table 8
     reproduces the printed rate_i through rate_curve, and the printed differences agree."""
-    gold = json.load(open(os.path.join(GOLD, "table7_rate_curve.json")))
+    gold = json.load(open(os.path.join(GOLD, "table8_rate_curve.json")))
     for col in ("dflash_percent", "dels_percent"):
         surv = np.array(gold[col]) / 100.0
         n = 100000

@@ -6,7 +6,7 @@
   and its argmax, ties, gap and log-probabilities are known exactly;
 * half-integer alpha with perfect-square short weights (still rational);
 * shift invariance of log-softmax (Sec. 4.1: token-independent factors drop out);
-* the limits alpha = beta = 0 (DFlash alone, Sec. 5.4 / Table 4) and the
+* the limits alpha = beta = 0 (DFlash alone, Sec. 5.6, Table 4) and the
   all-zero head;
 * a hand-worked three-position example through the Markov head of App. A.
 """
