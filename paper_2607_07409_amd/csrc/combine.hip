@@ -6,6 +6,8 @@
 // the workgroup), forms l = w_long*l_L + alpha*l_S - beta*l_P in float32 and folds
 // the chunk into its running (max, sum exp) for l_L, l_S, l and into the top-2 of l.
 // The workgroup merge is a fixed-order butterfly, so results are deterministic.
+// Without row statistics or scores only the running maximum of l and its index are
+// kept: the argmax needs no normaliser, and the kernel is then bound by HBM bandwidth.
 // With parts > 1 a second kernel merges the per-range partials of each row.
 #include "dels_internal.hpp"
 
@@ -24,15 +26,26 @@ __device__ __forceinline__ float fuse1(float a, float b, float p, float wl, floa
   return f;
 }
 
-template <typename T, bool PRIOR>
+// running maximum and its index only (lowest index among equal values)
+__device__ __forceinline__ void top1_push(Partial& p, float x, int idx) {
+  const bool up = x > p.t1;
+  p.t1 = up ? x : p.t1;
+  p.i1 = up ? idx : p.i1;
+}
+
+template <typename T, bool PRIOR, bool STATS>
 __device__ __forceinline__ void fold_scalar(Partial& P, const T* Lr, const T* Sr, const float* prior,
                                             int v, float wl, float al, float be) {
   float a = to_f32(Lr[v]), b = to_f32(Sr[v]);
   float f = fuse1<PRIOR>(a, b, PRIOR ? prior[v] : 0.f, wl, al, be);
-  lse_fold<1>(P.L, &a, a);
-  lse_fold<1>(P.S, &b, b);
-  lse_fold<1>(P.F, &f, f);
-  top2_push(P, f, v);
+  if (STATS) {
+    lse_fold<1>(P.L, &a, a);
+    lse_fold<1>(P.S, &b, b);
+    lse_fold<1>(P.F, &f, f);
+    top2_push(P, f, v);
+  } else {
+    top1_push(P, f, v);
+  }
 }
 
 template <typename T>
@@ -41,7 +54,7 @@ __device__ __forceinline__ int head_elems(const T* p, int V) {
   return h < V ? h : V;
 }
 
-template <typename T, bool PRIOR>
+template <typename T, bool PRIOR, bool STATS>
 __global__ __launch_bounds__(kThreads) void k_combine_part(
     const T* __restrict__ L, const T* __restrict__ S, const float* __restrict__ prior, int V,
     float wl, float al, float be, Partial* __restrict__ part_out, int32_t* __restrict__ out_token,
@@ -58,7 +71,7 @@ __global__ __launch_bounds__(kThreads) void k_combine_part(
   const int t = threadIdx.x;
 
   Partial P = partial_empty();
-  if (part == 0 && t < h0) fold_scalar<T, PRIOR>(P, Lr, Sr, prior, t, wl, al, be);
+  if (part == 0 && t < h0) fold_scalar<T, PRIOR, STATS>(P, Lr, Sr, prior, t, wl, al, be);
 
   for (int c = c0 + t; c < c1; c += kThreads * kUnroll) {
     uint4 ra[kUnroll], rb[kUnroll];
@@ -78,25 +91,29 @@ __global__ __launch_bounds__(kThreads) void k_combine_part(
         Chunk<T>::widen(ra[u], a);
         Chunk<T>::widen(rb[u], b);
         const int v0 = h0 + cc * N;
-        float ma = a[0], mb = b[0];
 #pragma unroll
-        for (int i = 0; i < N; ++i) {
-          f[i] = fuse1<PRIOR>(a[i], b[i], PRIOR ? prior[v0 + i] : 0.f, wl, al, be);
-          ma = fmaxf(ma, a[i]);
-          mb = fmaxf(mb, b[i]);
+        for (int i = 0; i < N; ++i) f[i] = fuse1<PRIOR>(a[i], b[i], PRIOR ? prior[v0 + i] : 0.f, wl, al, be);
+        if (STATS) {
+          float ma = a[0], mb = b[0], mf = f[0];
+#pragma unroll
+          for (int i = 1; i < N; ++i) {
+            ma = fmaxf(ma, a[i]);
+            mb = fmaxf(mb, b[i]);
+            mf = fmaxf(mf, f[i]);
+          }
+          lse_fold<N>(P.L, a, ma);
+          lse_fold<N>(P.S, b, mb);
+          lse_fold<N>(P.F, f, mf);
+#pragma unroll
+          for (int i = 0; i < N; ++i) top2_push(P, f[i], v0 + i);
+        } else {
+#pragma unroll
+          for (int i = 0; i < N; ++i) top1_push(P, f[i], v0 + i);
         }
-        float mf = f[0];
-#pragma unroll
-        for (int i = 1; i < N; ++i) mf = fmaxf(mf, f[i]);
-        lse_fold<N>(P.L, a, ma);
-        lse_fold<N>(P.S, b, mb);
-        lse_fold<N>(P.F, f, mf);
-#pragma unroll
-        for (int i = 0; i < N; ++i) top2_push(P, f[i], v0 + i);
       }
     }
   }
-  if (part == parts - 1 && t < V - tail0) fold_scalar<T, PRIOR>(P, Lr, Sr, prior, tail0 + t, wl, al, be);
+  if (part == parts - 1 && t < V - tail0) fold_scalar<T, PRIOR, STATS>(P, Lr, Sr, prior, tail0 + t, wl, al, be);
 
   P = block_merge(P, sh, kThreads / 64);
   if (t == 0) {
@@ -115,7 +132,7 @@ __global__ __launch_bounds__(64) void k_combine_finalize(const Partial* __restri
   const int row = blockIdx.x, lane = threadIdx.x;
   Partial P = partial_empty();
   for (int i = lane; i < parts; i += 64) P = partial_merge(P, parts_in[(size_t)row * parts + i]);
-  P = wave_merge(P);
+  P = allred_partial(P, WaveXor{});
   if (lane == 0)
     finalize_row(P, wl, al, false, out_token + row, out_stats ? out_stats + row : nullptr,
                  norm_out ? norm_out + row : nullptr);
@@ -140,14 +157,17 @@ template <typename T, bool PRIOR>
 hipError_t launch_combine_t(const CombineArgs& a, hipStream_t st) {
   const int parts = a.parts;
   dim3 grid((unsigned)a.rows, parts);
-  k_combine_part<T, PRIOR><<<grid, kThreads, 0, st>>>(
-      (const T*)a.long_logits, (const T*)a.short_logits, a.prior, a.V, a.wl, a.al, a.be, a.partials,
-      a.out_token, a.out_stats, a.norm);
+  // the normaliser feeds only the statistics and the score rows
+  const bool stats = a.out_stats != nullptr || a.out_scores != nullptr;
+  float* norm = stats ? a.norm : nullptr;
+  auto kern = stats ? k_combine_part<T, PRIOR, true> : k_combine_part<T, PRIOR, false>;
+  kern<<<grid, kThreads, 0, st>>>((const T*)a.long_logits, (const T*)a.short_logits, a.prior, a.V, a.wl, a.al,
+                                  a.be, a.partials, a.out_token, a.out_stats, norm);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (parts > 1) {
     k_combine_finalize<<<(unsigned)a.rows, 64, 0, st>>>(a.partials, parts, a.wl, a.al, a.out_token,
-                                                         a.out_stats, a.norm);
+                                                         a.out_stats, norm);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (a.out_scores) {
@@ -162,8 +182,9 @@ hipError_t launch_combine_t(const CombineArgs& a, hipStream_t st) {
 }  // namespace
 
 int combine_parts(int64_t rows, int32_t V) {
-  // enough workgroups to cover the chip when rows are few; each range >= 2048 elements
-  const int64_t target = 2048;
+  // enough workgroups to cover the chip when rows are few (four per CU); each range >= 2048
+  // elements.  From 1024 rows on every row is one workgroup and no merge launch follows.
+  const int64_t target = 1024;
   int64_t p = (target + rows - 1) / std::max<int64_t>(rows, 1);
   const int64_t cap = std::max<int64_t>(1, V / 2048);
   p = std::min(p, cap);

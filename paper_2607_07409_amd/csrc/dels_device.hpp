@@ -115,7 +115,7 @@ __device__ __forceinline__ Partial partial_empty() {
 
 // top-2 update with the values of one thread visited in increasing index order
 __device__ __forceinline__ void top2_push(Partial& p, float x, int idx) {
-  p.t2 = fmaxf(p.t2, fminf(x, p.t1));
+  p.t2 = __builtin_amdgcn_fmed3f(x, p.t1, p.t2);   // t1 >= t2: the median is the new second value
   const bool up = x > p.t1;
   p.t1 = up ? x : p.t1;
   p.i1 = up ? idx : p.i1;
@@ -134,29 +134,63 @@ __device__ __forceinline__ Partial partial_merge(const Partial& a, const Partial
   return r;
 }
 
-__device__ __forceinline__ Partial shfl_xor_partial(const Partial& p, int m) {
-  Partial q;
-  q.L.m = __shfl_xor(p.L.m, m); q.L.s = __shfl_xor(p.L.s, m);
-  q.S.m = __shfl_xor(p.S.m, m); q.S.s = __shfl_xor(p.S.s, m);
-  q.F.m = __shfl_xor(p.F.m, m); q.F.s = __shfl_xor(p.F.s, m);
-  q.t1 = __shfl_xor(p.t1, m); q.t2 = __shfl_xor(p.t2, m);
-  q.i1 = __shfl_xor(p.i1, m);
-  q.pad = 0;
-  return q;
+// All-reduce of a partial over lane groups, given a lane permutation `x(v, m)` (a shuffle or
+// DPP rotate) applied for each m in a list: the three maxima first, then every lane rescales
+// its sums once to the common maxima and the sums are added up, then the top-1 as a
+// (value, lowest index) maximum and the top-2 as the largest value that is not the winner.
+// One exponential per log-sum-exp per lane instead of two per merge step.
+template <typename Perm>
+__device__ __forceinline__ float allred_max(float v, Perm x) {
+  x.each([&](int m) { v = fmaxf(v, x(v, m)); });
+  return v;
 }
-
-// Butterfly merge over the 64 lanes of a wave; every lane ends with the total.
-// The merge is commutative and the pairing is fixed, so the result is deterministic.
-__device__ __forceinline__ Partial wave_merge(Partial p) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) p = partial_merge(p, shfl_xor_partial(p, m));
+template <typename Perm>
+__device__ __forceinline__ float allred_sum(float v, Perm x) {
+  x.each([&](int m) { v += x(v, m); });
+  return v;
+}
+template <typename Perm>
+__device__ __forceinline__ Lse allred_lse(Lse a, Perm x) {
+  const float m = allred_max(a.m, x);
+  float s = (a.m == -INFINITY) ? 0.f : a.s * fast_exp2((a.m - m) * kLog2e);
+  return {m, allred_sum(s, x)};
+}
+template <typename Perm>
+__device__ __forceinline__ Partial allred_partial(Partial p, Perm x) {
+  p.L = allred_lse(p.L, x);
+  p.S = allred_lse(p.S, x);
+  p.F = allred_lse(p.F, x);
+  float T = p.t1;
+  int I = p.i1;
+  x.each([&](int m) {
+    const float ot = x(T, m);
+    const int oi = x.i(I, m);
+    const bool take = ot > T || (ot == T && oi < I);
+    T = take ? ot : T;
+    I = take ? oi : I;
+  });
+  const float c = (p.t1 == T && p.i1 == I) ? p.t2 : p.t1;
+  p.t2 = allred_max(c, x);
+  p.t1 = T;
+  p.i1 = I;
+  p.pad = 0;
   return p;
 }
+// xor shuffles over the 64 lanes of a wave
+struct WaveXor {
+  template <typename F>
+  __device__ __forceinline__ void each(F f) const {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) f(m);
+  }
+  __device__ __forceinline__ float operator()(float v, int m) const { return __shfl_xor(v, m); }
+  __device__ __forceinline__ int i(int v, int m) const { return __shfl_xor(v, m); }
+};
 
 // Merge over a workgroup of nwaves waves; the total is returned to every thread.
-// `sh` must hold nwaves Partials.
+// `sh` must hold nwaves Partials.  The pairing is fixed, so the result is deterministic.
 __device__ __forceinline__ Partial block_merge(Partial p, Partial* sh, int nwaves) {
-  p = wave_merge(p);
+  p = allred_partial(p, WaveXor{});
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __syncthreads();
   if (lane == 0) sh[wave] = p;

@@ -201,17 +201,26 @@ __device__ __forceinline__ uint64_t wave_key_max(uint64_t k) {
   return k;
 }
 
-template <int N>
-__device__ __forceinline__ Partial row_ror_partial(const Partial& p) {
-  Partial q;
-  q.L.m = row_ror<N>(p.L.m); q.L.s = row_ror<N>(p.L.s);
-  q.S.m = row_ror<N>(p.S.m); q.S.s = row_ror<N>(p.S.s);
-  q.F.m = row_ror<N>(p.F.m); q.F.s = row_ror<N>(p.F.s);
-  q.t1 = row_ror<N>(p.t1); q.t2 = row_ror<N>(p.t2);
-  q.i1 = row_ror_i<N>(p.i1);
-  q.pad = 0;
-  return q;
-}
+// lane permutations for allred_partial: DPP rotations within each row of 16 lanes, then
+// (FULL) xor shuffles across the four rows
+template <bool FULL>
+struct RowRor {
+  template <typename F>
+  __device__ __forceinline__ void each(F f) const {
+    f(8); f(4); f(2); f(1);
+    if (FULL) { f(16); f(32); }
+  }
+  __device__ __forceinline__ int i(int v, int m) const {
+    switch (m) {
+      case 8: return row_ror_i<8>(v);
+      case 4: return row_ror_i<4>(v);
+      case 2: return row_ror_i<2>(v);
+      case 1: return row_ror_i<1>(v);
+      default: return __shfl_xor(v, m);
+    }
+  }
+  __device__ __forceinline__ float operator()(float v, int m) const { return __int_as_float(i(__float_as_int(v), m)); }
+};
 
 }  // namespace
 
@@ -354,7 +363,8 @@ __device__ __forceinline__ void plane_operand(const uint16_t* hi, const uint16_t
   alo = *(const uint4*)(lo + o);
 }
 
-template <int KK, typename LT, bool PRIOR>
+// NARROW: at most 4 sequences (one M tile whose useful rows all sit in lanes 0..15)
+template <int KK, typename LT, bool PRIOR, bool NARROW>
 __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr int TPW = kOps / KK;   // AGPR tiles per wave
@@ -485,6 +495,29 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     return true;
   };
 
+  // Publish the row-statistics partial of this workgroup for position jp (slots of M tile mtp,
+  // per-wave partials in s_part): merged over the waves, then nine tagged words per slot,
+  // written by the lanes of wave `by` (a wave's loads wait for its earlier stores, so the
+  // stores go to a wave that loads nothing critical soon after).
+  auto publish_stats = [&](int jp, int mtp, int nbp, int by) {
+    const int sl = tid - 64 * by;
+    if (sl >= 0 && sl < nbp) {
+      Partial T = s_part[sl];
+      for (int q = 1; q < 4; ++q) T = partial_merge(T, s_part[q * 16 + sl]);
+      const uint32_t stag = (epoch << 8) | (uint32_t)(jp + 1);
+      uint64_t* sp = a.stats + (((size_t)jp * batch + mtp * 16 + sl) * G + w) * kStatWords;
+      st64(sp + 0, tagged(T.L.m, stag)); st64(sp + 1, tagged(T.L.s, stag));
+      st64(sp + 2, tagged(T.S.m, stag)); st64(sp + 3, tagged(T.S.s, stag));
+      st64(sp + 4, tagged(T.F.m, stag)); st64(sp + 5, tagged(T.F.s, stag));
+      st64(sp + 6, tagged(T.t1, stag)); st64(sp + 7, tagged(T.t2, stag));
+      st64(sp + 8, tagged(__int_as_float(T.i1), stag));
+    }
+  };
+  // GRU workgroups with a single M tile hand their statistics of position j over during
+  // position j + 1: right after the argmax key they are on the critical path to the next
+  // merge.  -1: nothing pending.
+  int pending_stats = -1;
+
   for (int j = 0; j < Bk; ++j) {
     const uint32_t tag = (epoch << 8) | (uint32_t)(j + 1);
     const uint32_t tag8 = (uint32_t)(j + 1);
@@ -561,6 +594,10 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
           if (k0) __syncthreads();
           ok &= stage_split(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
           __syncthreads();
+          if (pending_stats >= 0) {   // s_part still holds it: nothing has used the space since
+            publish_stats(pending_stats, 0, batch, 3);
+            pending_stats = -1;
+          }
           for (int kk = wave; kk < HC / 32; kk += 4) {
             uint4 ahi, alo;
             plane_operand(s_hi, s_lo, pitch, nb, n16, g4, 32 * kk, ahi, alo);
@@ -655,10 +692,52 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       } else {
         __syncthreads();   // s_ll complete
       }
+      // With at most 4 sequences every useful MFMA output sits in lanes 0..15 (rows = slots).
+      // Such "narrow" tiles are stashed in LDS (the planes, free once the A operands are in
+      // registers) and folded four tiles at a time, one tile per 16-lane group.
+      constexpr bool narrow = NARROW;
+      float* s_stash = (float*)s_hi + wave * 256;   // [4 tiles][4 slots][16 rows]
+      if (narrow) __syncthreads();
 
       Partial P[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) P[i] = partial_empty();
+
+      // narrow: keep the useful rows (slots < nb) of a tile's result at stash position tq
+      auto stash = [&](const f32x4_t& acc, int tq) {
+        if (g4 == 0) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (i < nb) s_stash[(tq * 4 + i) * 16 + n16] = acc[i];
+        }
+      };
+      // narrow: fold stashed tiles base + stride * tq (tq < ntile), lane group tq taking tile tq
+      auto fold_narrow = [&](int base, int stride, int ntile) {
+        if (g4 < ntile) {
+          const int row = 16 * (base + stride * g4) + n16;
+          const int v = v_base + row;
+          if (v < V) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              if (i < nb) {
+                const float x = to_f32(s_ll[i * a.rows_max + row]);
+                float f;
+                if (long_only) {
+                  f = wl * x;
+                } else {
+                  const float sv = s_stash[(g4 * 4 + i) * 16 + n16];
+                  f = __builtin_fmaf(al, sv, wl * x);
+                  if (PRIOR) f = __builtin_fmaf(-be, s_prior[row], f);
+                  lse_push(P[i].S, sv);
+                }
+                lse_push(P[i].L, x);
+                lse_push(P[i].F, f);
+                top2_push(P[i], f, v);
+              }
+            }
+          }
+        }
+      };
 
       auto fold_tile = [&](const f32x4_t& acc, int lt) {
         const int row = 16 * lt + n16;
@@ -707,12 +786,23 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
               }
             }
           }
-          fold_tile(c0 + c1, lt);
-          if (two && lt + 1 < na) fold_tile(c2 + c3, lt + 1);
+          if (narrow) {
+            stash(c0 + c1, q % 4);
+            if (two) stash(c2 + c3, q % 4 + 1);
+          } else {
+            fold_tile(c0 + c1, lt);
+            if (two && lt + 1 < na) fold_tile(c2 + c3, lt + 1);
+          }
+        }
+        if (narrow && (q % 4 == 2 || q + 2 >= TPW)) {   // a group of four tiles (or the last) is stashed
+          const int g0 = q - q % 4;
+          const int cnt = (TPW - g0 < 4 ? TPW - g0 : 4);
+          const int avail = na - (wave * TPW + g0);
+          fold_narrow(wave * TPW + g0, 1, avail < cnt ? (avail > 0 ? avail : 0) : cnt);
         }
       }
-      // LDS-resident tiles, round robin over the waves
-      for (int lq = wave; lq < nl; lq += 4) {
+      // LDS-resident tiles, round robin over the waves (narrow: four at a time)
+      auto lds_tile = [&](int lq) -> f32x4_t {
         f32x4_t c0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, c1 = c0;
         if (!long_only) {
 #pragma unroll
@@ -722,14 +812,34 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
             c1 = mfma_vv(alo[kk], bw, c1);
           }
         }
-        fold_tile(c0 + c1, na + lq);
+        return c0 + c1;
+      };
+      if (narrow) {
+        for (int m0 = 0; wave + 4 * m0 < nl; m0 += 4) {
+          int cnt = 0;
+          for (int tq = 0; tq < 4; ++tq) {
+            const int lq = wave + 4 * (m0 + tq);
+            if (lq < nl) {
+              stash(lds_tile(lq), tq);
+              ++cnt;
+            }
+          }
+          fold_narrow(na + wave + 4 * m0, 4, cnt);
+        }
+      } else {
+        for (int lq = wave; lq < nl; lq += 4) fold_tile(lds_tile(lq), na + lq);
       }
       // argmax key of each slot: max over the 16 lanes of a row (DPP), then over the waves
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         if (i < nb) {
-          const uint64_t k = row_key_max(make_key(P[i].t1, P[i].i1, tag8));
-          if (n16 == 0) s_wkey[wave * 16 + 4 * g4 + i] = k;
+          if (narrow) {   // slot i spread over the whole wave
+            const uint64_t k = wave_key_max(make_key(P[i].t1, P[i].i1, tag8));
+            if (lane == 0) s_wkey[wave * 16 + i] = k;
+          } else {
+            const uint64_t k = row_key_max(make_key(P[i].t1, P[i].i1, tag8));
+            if (n16 == 0) s_wkey[wave * 16 + 4 * g4 + i] = k;
+          }
         }
       }
       __syncthreads();
@@ -743,23 +853,19 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           if (i < nb) {
-            P[i] = partial_merge(P[i], row_ror_partial<8>(P[i]));
-            P[i] = partial_merge(P[i], row_ror_partial<4>(P[i]));
-            P[i] = partial_merge(P[i], row_ror_partial<2>(P[i]));
-            P[i] = partial_merge(P[i], row_ror_partial<1>(P[i]));
-            if (n16 == 0) s_part[wave * 16 + 4 * g4 + i] = P[i];
+            P[i] = allred_partial(P[i], RowRor<NARROW>{});   // over the row (narrow: the wave)
+            if (narrow) {
+              if (lane == 0) s_part[wave * 16 + i] = P[i];
+            } else if (n16 == 0) {
+              s_part[wave * 16 + 4 * g4 + i] = P[i];
+            }
           }
         }
-        __syncthreads();
-        if (tid < nb) {
-          Partial T = s_part[tid];
-          for (int q = 1; q < 4; ++q) T = partial_merge(T, s_part[q * 16 + tid]);
-          uint64_t* sp = a.stats + (((size_t)j * batch + mt * 16 + tid) * G + w) * kStatWords;
-          st64(sp + 0, tagged(T.L.m, tag)); st64(sp + 1, tagged(T.L.s, tag));
-          st64(sp + 2, tagged(T.S.m, tag)); st64(sp + 3, tagged(T.S.s, tag));
-          st64(sp + 4, tagged(T.F.m, tag)); st64(sp + 5, tagged(T.F.s, tag));
-          st64(sp + 6, tagged(T.t1, tag)); st64(sp + 7, tagged(T.t2, tag));
-          st64(sp + 8, tagged(__int_as_float(T.i1), tag));
+        if (gru && mtiles == 1 && j + 1 < Bk) {
+          pending_stats = j;
+        } else {
+          __syncthreads();
+          publish_stats(j, mt, nb, 0);
         }
       }
       __syncthreads();
@@ -809,9 +915,9 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   }
 }
 
-template <int KK, typename LT, bool PRIOR>
+template <int KK, typename LT, bool PRIOR, bool NARROW>
 hipError_t launch_k(const PersistArgs& pa, int G, size_t lds, hipStream_t st) {
-  auto kern = k_draft_persistent<KK, LT, PRIOR>;
+  auto kern = k_draft_persistent<KK, LT, PRIOR, NARROW>;
   // the dynamic LDS limit is raised to the maximum once per device (a per-call attribute
   // change costs microseconds of host time)
   static std::atomic<uint64_t> raised{0};
@@ -832,9 +938,10 @@ hipError_t launch_k(const PersistArgs& pa, int G, size_t lds, hipStream_t st) {
 
 template <typename LT, bool PRIOR>
 hipError_t launch_kk(const PersistArgs& pa, int G, size_t lds, hipStream_t st) {
+  const bool narrow = pa.batch <= 4;
   switch (pa.r / 32) {
-    case 4: return launch_k<4, LT, PRIOR>(pa, G, lds, st);
-    case 8: return launch_k<8, LT, PRIOR>(pa, G, lds, st);
+    case 4: return narrow ? launch_k<4, LT, PRIOR, true>(pa, G, lds, st) : launch_k<4, LT, PRIOR, false>(pa, G, lds, st);
+    case 8: return narrow ? launch_k<8, LT, PRIOR, true>(pa, G, lds, st) : launch_k<8, LT, PRIOR, false>(pa, G, lds, st);
   }
   return hipErrorInvalidValue;
 }

@@ -133,3 +133,44 @@ def test_combine_deterministic():
         t1, s1, _ = B.combine_logits(L, S, None, 1.0, 0.5, 0.0)
         torch.cuda.synchronize()
         assert torch.equal(t0, t1) and torch.equal(s0, s1)
+
+
+@pytest.mark.parametrize("rows,V,dtype,seed,prior", [
+    (16, QV, "bf16", 60, False),
+    (256, QV, "bf16", 61, True),
+    (7, 4099, "bf16", 62, False),
+    (5, 4099, "f32", 63, True),
+    (3, 1, "bf16", 64, False),
+])
+def test_combine_tokens_only_matches(rows, V, dtype, seed, prior):
+    """Without statistics the kernel keeps only the running maximum: the tokens must be the
+    same bits as with statistics, and agree with the oracle up to near-ties."""
+    L = W.make_logit_rows(rows, V, dtype, seed, "onehot", 3.0, purpose=20)
+    S = W.make_logit_rows(rows, V, dtype, seed, "normal", 2.0, purpose=21)
+    P = W.make_zipf_log_prior(V, seed) if prior else None
+    be = 0.5 if prior else 0.0
+    lt, st = B.as_tensor(L), B.as_tensor(S)
+    pt = None if P is None else torch.from_numpy(np.ascontiguousarray(P, dtype=np.float32)).cuda()
+    t_stats, _, _ = B.combine_logits(lt, st, pt, 1.0, 0.5, be, want_stats=True)
+    t_only, s_only, _ = B.combine_logits(lt, st, pt, 1.0, 0.5, be, want_stats=False)
+    torch.cuda.synchronize()
+    assert s_only is None
+    assert torch.equal(t_stats, t_only)
+    tok = t_only.cpu().numpy()
+    for i in range(0, rows, max(1, rows // 8)):
+        r = O.combine_row(np.asarray(L[i], np.float32), np.asarray(S[i], np.float32), P, 1.0, 0.5, be)
+        assert tok[i] == r.token or r.gap < TOL, (i, tok[i], r.token, r.gap)
+
+
+def test_combine_tokens_only_ties_and_masks():
+    rows, V = 12, 30000
+    g = np.random.default_rng(65)
+    L = g.normal(0, 1, (rows, V)).astype(np.float32)
+    for i in range(rows):
+        L[i, np.sort(g.choice(V, size=1 + i % 4, replace=False))] = 9.0
+    L[g.random((rows, V)) < 0.2] = -np.inf
+    S = g.normal(0, 1, (rows, V)).astype(np.float32)
+    t, _, _ = B.combine_logits(B.as_tensor(L), B.as_tensor(S), None, 1.0, 0.0, 0.0, want_stats=False)
+    torch.cuda.synchronize()
+    Lm = np.where(np.isneginf(L), -np.inf, L)
+    assert np.array_equal(t.cpu().numpy(), np.argmax(Lm, axis=1))
