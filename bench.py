@@ -228,6 +228,26 @@ def main():
     launches_us = e2.elapsed_time(e3) / 20 * 1e3
     log(f"per-position launches: {launches_us:.1f} us per block")
 
+    # ---- the Markov local head (App. A) on the same workload: rho = E_M[previous token] ------
+    import math
+    em, wm = W.make_markov_head(wl.V, wl.r, "bf16", wl.seed, scale=math.sqrt(3.0 / math.sqrt(wl.r)))
+    mhead = B.LocalHead.markov_from_weights(em, wm, dev).prepare()
+    mws = B.draft_workspace(mhead, wl.batch, wl.B, dev)
+    for _ in range(5):
+        B.draft_block(mhead, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=mws)
+    e2.record()
+    for _ in range(n_k):
+        B.draft_block(mhead, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=mws)
+    e3.record()
+    torch.cuda.synchronize()
+    assert B.workspace_error(mws) == 0, "persistent kernel reported a stalled hand-off"
+    m_us = e2.elapsed_time(e3) / n_k * 1e3
+    markov = {"head": "markov (E_M, W_M: V x r bf16)", "r": wl.r,
+              "path": "persistent" if mhead.path(wl.batch, wl.B, L.dtype, False) == 1 else "per-position launches",
+              "us_per_block": round(m_us, 2), "tokens_per_s": round(wl.batch * wl.B / (m_us * 1e-6), 1)}
+    log(f"markov head: {m_us:.1f} us per block -> {markov['tokens_per_s']:.0f} drafted tokens/s")
+    del mhead, mws
+
     # ---- standalone fused combine at the serving shape (cold: inputs larger than the MALL) ----
     R = args.combine_rows
     Lc = B.as_tensor(W.make_logit_rows(R, wl.V, "bf16", 77, "onehot", 3.0, purpose=20), dev)
@@ -282,6 +302,7 @@ def main():
         "cpu_baseline": cpu,
         "combine": combine,
         "draft_block_per_position_launches_us": round(launches_us, 2),
+        "markov_head": markov,
     }
     print(json.dumps(out), flush=True)
 

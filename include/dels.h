@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define DLS_ABI_VERSION 1
+#define DLS_ABI_VERSION 2
 
 typedef enum dls_status {
   DLS_OK = 0,
@@ -96,16 +96,26 @@ typedef struct dls_row_stats {
   float lse_fused;
 } dls_row_stats;
 
-/* RNN local head (App. A).  All five tensors share `dtype` (DLS_BF16 or DLS_F32).
+/* The two local heads of App. A. */
+typedef enum dls_head_kind {
+  DLS_HEAD_RNN = 0,     /* rho_i = SiLU(W_rank GRU(E_tgt(z_i))),  l_S = W_vocab rho_i */
+  DLS_HEAD_MARKOV = 1   /* rho_i = E_M(x_{i-1}),                  l_S = W_M rho_i     */
+} dls_head_kind;
+
+/* Local head (App. A).  All tensors share `dtype` (DLS_BF16 or DLS_F32).
+ * kind DLS_HEAD_RNN:
  *   emb     [V, d]   frozen target embedding E_tgt
  *   w_ih    [3H, d]  GRU input weights, rows (r, z, n)
  *   w_hh    [3H, H]  GRU recurrent weights, rows (r, z, n)
  *   w_rank  [r, H]   low-rank projection (followed by SiLU)
  *   w_vocab [V, r]   vocabulary head
- *   prepared         NULL, or a device buffer filled by dls_prepare_head from these same
- *                    tensors; it enables the persistent drafting kernel (see below)
+ * kind DLS_HEAD_MARKOV (d and H are ignored, w_ih, w_hh and w_rank may be NULL):
+ *   emb     [V, r]   E_M, the low-rank state of each previous token
+ *   w_vocab [V, r]   W_M, the low-rank vocabulary head
+ * prepared  NULL, or a device buffer filled by dls_prepare_head from these same tensors;
+ *           it enables the persistent drafting kernel (see below)
  * Limits: 1 <= V <= 2^24; d, H, r multiples of 8 with 8 <= d <= 16384,
- * 8 <= H <= 4096, 8 <= r <= 512. */
+ * 8 <= H <= 4096, 8 <= r <= 512 (RNN); 8 <= r <= 512, r a multiple of 8 (Markov). */
 typedef struct dls_local_head {
   int32_t V, d, H, r;
   dls_dtype dtype;
@@ -115,19 +125,23 @@ typedef struct dls_local_head {
   const void *w_rank;
   const void *w_vocab;
   const void *prepared;
+  int32_t kind;        /* dls_head_kind */
+  int32_t reserved;    /* 0 */
 } dls_local_head;
 
 /* ---------------------------------------------------------------------------------
  * One-time preparation of a bf16 head for the persistent drafting kernel (App. A head,
  * rearranged; nothing of the method changes):
- *  - the GRU input projection is folded into a table T[u] = W_ih E[u] of [V, 3H] float32
- *    values (E is frozen and the GRU has no bias, so the input term depends on the token
- *    only); T is accumulated in float32 from exact bf16 products;
- *  - W_vocab and W_hh are copied into the operand order of the bf16 matrix cores.
- * The buffer needs dls_prepare_head_size(head) bytes (V*3H*4 + V*r*2 + 3H*H*2 + small,
- * 1.98 GB for V = 151,936, H = 1024, r = 256) and stays valid while the head tensors
- * are unchanged.  Requirements: dtype DLS_BF16, H a multiple of 32, r in {32, 64, 128,
- * 256}; otherwise DLS_ERR_SHAPE / DLS_ERR_DTYPE.  Asynchronous on `stream`. */
+ *  - RNN: the GRU input projection is folded into a table T[u] = W_ih E[u] of [V, 3H]
+ *    float32 values (E is frozen and the GRU has no bias, so the input term depends on
+ *    the token only); T is accumulated in float32 from exact bf16 products;
+ *  - W_vocab (W_M) and, for the RNN head, W_hh are copied into the operand order of the
+ *    bf16 matrix cores.
+ * The buffer needs dls_prepare_head_size(head) bytes (RNN: V*3H*4 + V*r*2 + 3H*H*2 +
+ * small, 1.98 GB for V = 151,936, H = 1024, r = 256; Markov: V*r*2 + small) and stays
+ * valid while the head tensors are unchanged.  Requirements: dtype DLS_BF16, r in {32,
+ * 64, 128, 256}, and H a multiple of 32 for the RNN head; otherwise DLS_ERR_SHAPE /
+ * DLS_ERR_DTYPE.  Asynchronous on `stream`. */
 size_t dls_prepare_head_size(const dls_local_head *head);
 dls_status dls_prepare_head(const dls_local_head *head, void *prepared, size_t bytes, void *stream);
 
@@ -161,7 +175,7 @@ dls_status dls_combine_logits(const void *long_logits, const void *short_logits,
  * consistent afterwards.  If a persistent call ever sets the error word (the second
  * uint32 of the workspace, nonzero after a stalled hand-off between workgroups), later
  * persistent calls on that workspace do nothing until it is zero-filled again.
- *   head         RNN local head (see dls_local_head); pointers are device pointers
+ *   head         RNN or Markov local head (see dls_local_head); device pointers
  *   long_logits  [batch, B, V] of `long_dtype`; row j is the long logits of draft
  *                position j
  *   last_token   [batch] int32, the last accepted token; it is the head's first input

@@ -16,6 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libdels.so")
 
 DLS_F32, DLS_BF16 = 0, 1
+DLS_HEAD_RNN, DLS_HEAD_MARKOV = 0, 1
 DLS_FIRST_ROW_LONG_ONLY = 0x1
 STATUS = {0: "DLS_OK", 1: "DLS_ERR_ARG", 2: "DLS_ERR_SHAPE", 3: "DLS_ERR_DTYPE",
           4: "DLS_ERR_WORKSPACE", 5: "DLS_ERR_DEVICE", 6: "DLS_ERR_HIP"}
@@ -41,7 +42,8 @@ class LocalHeadC(ctypes.Structure):
     _fields_ = [("V", ctypes.c_int32), ("d", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("r", ctypes.c_int32), ("dtype", ctypes.c_int),
                 ("emb", ctypes.c_void_p), ("w_ih", ctypes.c_void_p), ("w_hh", ctypes.c_void_p),
-                ("w_rank", ctypes.c_void_p), ("w_vocab", ctypes.c_void_p), ("prepared", ctypes.c_void_p)]
+                ("w_rank", ctypes.c_void_p), ("w_vocab", ctypes.c_void_p), ("prepared", ctypes.c_void_p),
+                ("kind", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 _lib = None
@@ -122,7 +124,8 @@ def as_tensor(x, device="cuda") -> torch.Tensor:
 
 
 class LocalHead:
-    """Device copy of an RNN local head (App. A) and its C descriptor."""
+    """Device copy of a local head (App. A) and its C descriptor: the RNN head (E_tgt, W_ih,
+    W_hh, W_rank, W_vocab) or, built with LocalHead.markov, the Markov head (E_M, W_M)."""
 
     def __init__(self, emb, w_ih, w_hh, w_rank, w_vocab):
         ts = [emb, w_ih, w_hh, w_rank, w_vocab]
@@ -134,9 +137,27 @@ class LocalHead:
         H = self.w_hh.shape[1]
         r = self.w_rank.shape[0]
         self.V, self.d, self.H, self.r = V, d, H, r
+        self.kind = DLS_HEAD_RNN
         self.prepared = None
         self.c = LocalHeadC(V, d, H, r, _dtype_code(self.emb), self.emb.data_ptr(), self.w_ih.data_ptr(),
-                            self.w_hh.data_ptr(), self.w_rank.data_ptr(), self.w_vocab.data_ptr(), None)
+                            self.w_hh.data_ptr(), self.w_rank.data_ptr(), self.w_vocab.data_ptr(), None,
+                            DLS_HEAD_RNN, 0)
+
+    @classmethod
+    def markov(cls, e_m: torch.Tensor, w_m: torch.Tensor) -> "LocalHead":
+        """Markov head: rho = E_M[previous token] ([V, r]), l_S = W_M rho ([V, r])."""
+        if e_m.dtype != w_m.dtype or e_m.shape != w_m.shape:
+            raise TypeError("E_M and W_M must share dtype and shape [V, r]")
+        self = cls.__new__(cls)
+        self.emb, self.w_vocab = e_m.contiguous(), w_m.contiguous()
+        self.w_ih = self.w_hh = self.w_rank = None
+        self.V, self.r = self.emb.shape
+        self.d = self.H = 0
+        self.kind = DLS_HEAD_MARKOV
+        self.prepared = None
+        self.c = LocalHeadC(self.V, 0, 0, self.r, _dtype_code(self.emb), self.emb.data_ptr(), None, None, None,
+                            self.w_vocab.data_ptr(), None, DLS_HEAD_MARKOV, 0)
+        return self
 
     def prepare(self, stream=None) -> "LocalHead":
         """Fill the prepared form (folded input table, operand-ordered weights) on the device."""
@@ -153,6 +174,12 @@ class LocalHead:
         self.c.prepared = None
         return self
 
+    def twin(self) -> "LocalHead":
+        """A new descriptor over the same weight tensors (unprepared)."""
+        if self.kind == DLS_HEAD_MARKOV:
+            return LocalHead.markov(self.emb, self.w_vocab)
+        return LocalHead(self.emb, self.w_ih, self.w_hh, self.w_rank, self.w_vocab)
+
     def path(self, batch: int, B: int, long_dtype=torch.bfloat16, has_prior=False) -> int:
         """1 if dls_draft_block would use the persistent kernel, 0 for per-position launches."""
         code = DLS_BF16 if long_dtype == torch.bfloat16 else DLS_F32
@@ -162,9 +189,13 @@ class LocalHead:
     def from_weights(cls, hw, device="cuda") -> "LocalHead":
         return cls(*[as_tensor(a, device) for a in (hw.emb, hw.w_ih, hw.w_hh, hw.w_rank, hw.w_vocab)])
 
+    @classmethod
+    def markov_from_weights(cls, e_m, w_m, device="cuda") -> "LocalHead":
+        return cls.markov(as_tensor(e_m, device), as_tensor(w_m, device))
+
     def nbytes(self) -> int:
         return sum(t.numel() * t.element_size() for t in (self.emb, self.w_ih, self.w_hh, self.w_rank,
-                                                           self.w_vocab))
+                                                           self.w_vocab) if t is not None)
 
 
 # -----------------------------------------------------------------------------------

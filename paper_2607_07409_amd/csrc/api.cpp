@@ -87,21 +87,35 @@ dls_status check_fusion(const dls_fusion& f) {
 
 dls_status check_head(const dls_local_head* h) {
   if (!h) return fail(DLS_ERR_ARG, "head is NULL");
+  if (h->kind != DLS_HEAD_RNN && h->kind != DLS_HEAD_MARKOV) return fail(DLS_ERR_ARG, "unknown head kind %d", h->kind);
+  const bool markov = h->kind == DLS_HEAD_MARKOV;
   if (!valid_dtype(h->dtype)) return fail(DLS_ERR_DTYPE, "unknown head dtype %d", (int)h->dtype);
   if (h->V < 1 || h->V > (1 << 24)) return fail(DLS_ERR_SHAPE, "V=%d outside [1, 2^24]", h->V);
-  if (h->d < 8 || h->d > 16384 || h->d % 8)
+  if (!markov && (h->d < 8 || h->d > 16384 || h->d % 8))
     return fail(DLS_ERR_SHAPE, "d=%d must be a multiple of 8 in [8, 16384]", h->d);
-  if (h->H < 8 || h->H > 4096 || h->H % 8)
+  if (!markov && (h->H < 8 || h->H > 4096 || h->H % 8))
     return fail(DLS_ERR_SHAPE, "H=%d must be a multiple of 8 in [8, 4096]", h->H);
   if (h->r < 8 || h->r > 512 || h->r % 8)
     return fail(DLS_ERR_SHAPE, "r=%d must be a multiple of 8 in [8, 512]", h->r);
-  const void* ps[5] = {h->emb, h->w_ih, h->w_hh, h->w_rank, h->w_vocab};
-  const char* nm[5] = {"emb", "w_ih", "w_hh", "w_rank", "w_vocab"};
-  for (int i = 0; i < 5; ++i) {
+  const void* ps[5] = {h->emb, h->w_vocab, h->w_ih, h->w_hh, h->w_rank};
+  const char* nm[5] = {"emb", "w_vocab", "w_ih", "w_hh", "w_rank"};
+  for (int i = 0; i < (markov ? 2 : 5); ++i) {
     if (!ps[i]) return fail(DLS_ERR_ARG, "head.%s is NULL", nm[i]);
     if (!aligned(ps[i], 16)) return fail(DLS_ERR_ARG, "head.%s is not 16-byte aligned", nm[i]);
   }
   return DLS_OK;
+}
+
+// The head as the kernels see it: a Markov head has no GRU (d = H = 0, no GRU tensors).
+dls_local_head canon(const dls_local_head& h) {
+  dls_local_head c = h;
+  if (h.kind == DLS_HEAD_MARKOV) {
+    c.d = 0;
+    c.H = 0;
+    c.w_ih = c.w_hh = c.w_rank = nullptr;
+  }
+  c.reserved = 0;
+  return c;
 }
 
 }  // namespace
@@ -179,8 +193,9 @@ dls_status dls_combine_logits(const void* long_logits, const void* short_logits,
 }
 
 size_t dls_prepare_head_size(const dls_local_head* head) {
-  if (!head || head->V <= 0 || head->H <= 0 || head->r <= 0) return 0;
-  return dls::prepared_layout(*head).total;
+  if (!head || check_head(head) != DLS_OK) return 0;
+  g_last_error.clear();
+  return dls::prepared_layout(canon(*head)).total;
 }
 
 dls_status dls_prepare_head(const dls_local_head* head, void* prepared, size_t bytes, void* stream) {
@@ -188,22 +203,26 @@ dls_status dls_prepare_head(const dls_local_head* head, void* prepared, size_t b
   dls_status s = check_head(head);
   if (s != DLS_OK) return s;
   if (head->dtype != DLS_BF16) return fail(DLS_ERR_DTYPE, "only bf16 heads can be prepared");
-  if (head->H % 32) return fail(DLS_ERR_SHAPE, "H=%d must be a multiple of 32 to prepare", head->H);
+  if (head->kind == DLS_HEAD_RNN && head->H % 32)
+    return fail(DLS_ERR_SHAPE, "H=%d must be a multiple of 32 to prepare", head->H);
   if (!(head->r == 32 || head->r == 64 || head->r == 128 || head->r == 256))
     return fail(DLS_ERR_SHAPE, "r=%d must be 32, 64, 128 or 256 to prepare", head->r);
   if (!prepared || !aligned(prepared, 256)) return fail(DLS_ERR_ARG, "prepared buffer is NULL or not 256-byte aligned");
-  const size_t need = dls::prepared_layout(*head).total;
+  const dls_local_head ch = canon(*head);
+  const size_t need = dls::prepared_layout(ch).total;
   if (bytes < need) return fail(DLS_ERR_WORKSPACE, "prepared buffer %zu bytes < %zu required", bytes, need);
   if ((s = check_device()) != DLS_OK) return s;
-  hipError_t e = dls::launch_prepare(*head, prepared, (hipStream_t)stream);
+  hipError_t e = dls::launch_prepare(ch, prepared, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "prepare_head launch");
   return DLS_OK;
 }
 
 size_t dls_draft_block_workspace_size(const dls_local_head* head, int32_t batch, int32_t B) {
-  if (!head || batch <= 0 || B <= 0 || head->V <= 0 || head->H <= 0 || head->r <= 0) return 0;
+  if (!head || batch <= 0 || B <= 0 || check_head(head) != DLS_OK) return 0;
+  g_last_error.clear();
+  const dls_local_head ch = canon(*head);
   // persistent region first (its header must start zero-filled), per-launch region after it
-  return dls::persist_workspace(*head, batch, B).total + dls::draft_layout(*head, batch, B).total;
+  return dls::persist_workspace(ch, batch, B).total + dls::draft_layout(ch, batch, B).total;
 }
 
 dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,
@@ -231,21 +250,22 @@ dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, 
   int cus = 0;
   if ((s = check_device(&cus)) != DLS_OK) return s;
 
-  const dls::PersistWorkspace pw = dls::persist_workspace(*head, batch, B);
+  const dls_local_head ch = canon(*head);
+  const dls::PersistWorkspace pw = dls::persist_workspace(ch, batch, B);
   if (head->prepared) {
-    const dls::PersistPlan pl =
-        dls::persist_plan(*head, batch, B, long_dtype, prior != nullptr, persist_groups(cus));
+    const dls::PersistPlan pl = dls::persist_plan(ch, batch, B, long_dtype, prior != nullptr, persist_groups(cus));
     if (pl.ok) {
-      const dls::PreparedLayout PL = dls::prepared_layout(*head);
+      const dls::PreparedLayout PL = dls::prepared_layout(ch);
       const char* pp = (const char*)head->prepared;
       char* ws = (char*)workspace;
       dls::PersistArgs pa;
       pa.T = (const float*)(pp + PL.off_T);
       pa.wv = (const uint4*)(pp + PL.off_wv);
       pa.whh = (const uint4*)(pp + PL.off_whh);
-      pa.w_rank = (const dls::bf16_t*)head->w_rank;
+      pa.w_rank = (const dls::bf16_t*)ch.w_rank;
+      pa.e_m = ch.kind == DLS_HEAD_MARKOV ? (const dls::bf16_t*)ch.emb : nullptr;
       pa.V = head->V;
-      pa.H = head->H;
+      pa.H = ch.H;
       pa.r = head->r;
       pa.NT = pl.NT;
       pa.NG = pl.NG;
@@ -276,7 +296,7 @@ dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, 
   }
 
   dls::DraftArgs a;
-  a.head = *head;
+  a.head = ch;
   a.long_logits = long_logits;
   a.long_dtype = long_dtype;
   a.last_token = last_token;
@@ -288,7 +308,7 @@ dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, 
   a.out_tokens = out_tokens;
   a.out_stats = out_stats;
   a.ws = (char*)workspace + pw.total;
-  a.lay = dls::draft_layout(*head, batch, B);
+  a.lay = dls::draft_layout(ch, batch, B);
   hipError_t e = dls::launch_draft(a, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "draft_block launch");
   return DLS_OK;
@@ -302,7 +322,7 @@ int dls_draft_block_path(const dls_local_head* head, int32_t batch, int32_t B, d
   if (!head->prepared) return 0;
   int cus = 0;
   if (check_device(&cus) != DLS_OK) return -1;
-  const dls::PersistPlan pl = dls::persist_plan(*head, batch, B, long_dtype, has_prior != 0, persist_groups(cus));
+  const dls::PersistPlan pl = dls::persist_plan(canon(*head), batch, B, long_dtype, has_prior != 0, persist_groups(cus));
   if (!pl.ok) fail(DLS_OK, "%s", pl.why);
   return pl.ok ? 1 : 0;
 }

@@ -98,6 +98,7 @@ struct PersistArgs {
   const uint4* wv;           // W_vocab tiles in MFMA operand order
   const uint4* whh;          // W_hh in MFMA operand order, per 16-unit group
   const bf16_t* w_rank;      // [r][H]
+  const bf16_t* e_m;         // Markov head: E_M [V][r] (the GRU fields are unused then)
   int V, H, r, NT, NG, rpg, cap_a, rows_max;
   size_t lds_region_a;
   const void* L;             // long logits [batch][B][V]

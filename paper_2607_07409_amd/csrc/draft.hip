@@ -262,6 +262,20 @@ __global__ __launch_bounds__(kThreads) void k_select(const Partial* __restrict__
   }
 }
 
+// Markov head state: rho[b] = E_M[u_b] (App. A, Markov variant), widened to float32.
+// One thread per (sequence, rank column).
+template <typename WT>
+__global__ __launch_bounds__(kThreads) void k_markov_rho(const WT* __restrict__ e_m, int V, int r,
+                                                         const int32_t* __restrict__ tok, float* __restrict__ rho,
+                                                         int batch) {
+  const int i = blockIdx.x * kThreads + threadIdx.x;
+  if (i >= batch * r) return;
+  const int b = i / r, c = i % r;
+  const int t = tok[b];
+  const int u = (unsigned)t < (unsigned)V ? t : 0;   // out-of-range input reads as 0
+  rho[i] = to_f32(e_m[(size_t)u * r + c]);
+}
+
 template <typename WT, typename LT, bool PRIOR>
 hipError_t launch_draft_t(const DraftArgs& a, hipStream_t st) {
   const dls_local_head& hd = a.head;
@@ -290,7 +304,10 @@ hipError_t launch_draft_t(const DraftArgs& a, hipStream_t st) {
   bool first_head_step = true;
   for (int j = 0; j < B; ++j) {
     const bool long_only = literal && j == 0;
-    if (!long_only) {
+    if (!long_only && hd.kind == DLS_HEAD_MARKOV) {
+      k_markov_rho<WT><<<(batch * r + kThreads - 1) / kThreads, kThreads, 0, st>>>(emb, V, r, tok_in, rho, batch);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    } else if (!long_only) {
       k_gru<WT><<<(H + kWaves - 1) / kWaves, kThreads, 0, st>>>(emb, w_ih, w_hh, d, H, V, tok_in, hc,
                                                                  first_head_step ? 1 : 0, hn, batch);
       if ((e = hipGetLastError()) != hipSuccess) return e;

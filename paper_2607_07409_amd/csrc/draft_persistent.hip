@@ -364,7 +364,9 @@ __device__ __forceinline__ void plane_operand(const uint16_t* hi, const uint16_t
 }
 
 // NARROW: at most 4 sequences (one M tile whose useful rows all sit in lanes 0..15)
-template <int KK, typename LT, bool PRIOR, bool NARROW>
+// MARKOV: the Markov head of App. A, rho_j = E_M[u_j]: no GRU workgroups and no hand-off
+//         but the argmax keys; every workgroup merges the keys and reads the E_M row itself
+template <int KK, typename LT, bool PRIOR, bool NARROW, bool MARKOV>
 __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr int TPW = kOps / KK;   // AGPR tiles per wave
@@ -659,6 +661,19 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       }
     }
 
+    // ======================= Markov head: the previous token (all workgroups) =======================
+    if (MARKOV && !long_only) {
+      if (j > 0) {
+        if (!merge_position(j - 1)) return;
+      } else {
+        for (int b = tid; b < batch; b += kT) {
+          const int u = a.last[b];
+          s_tok[b] = (unsigned)u < (unsigned)V ? u : 0;   // out-of-range input reads as 0
+        }
+        __syncthreads();
+      }
+    }
+
     // ======================= vocabulary head + fused combine (all workgroups) =======================
     for (int mt = 0; mt < mtiles; ++mt) {
       const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
@@ -682,7 +697,20 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       }
       // rho of the slots, staged as bf16 hi + lo planes, then held as the A operands
       uint4 ahi[KK], alo[KK];
-      if (!long_only) {
+      if (MARKOV && !long_only) {
+        // rho = E_M[u]: bf16 values, exact in the hi plane (the lo half would be zero)
+        for (int i = tid; i < nb * (r / 8); i += kT) {
+          const int slot = i / (r / 8), c = i % (r / 8);
+          *(uint4*)(s_hi + slot * (r + 8) + 8 * c) =
+              *(const uint4*)(a.e_m + (size_t)s_tok[mt * 16 + slot] * r + 8 * c);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+          ahi[kk] = *(const uint4*)(s_hi + (n16 < nb ? n16 : 0) * (r + 8) + 32 * kk + 8 * g4);
+          alo[kk] = make_uint4(0, 0, 0, 0);
+        }
+      } else if (!long_only) {
         const uint64_t* rsrc = a.rbuf + ((size_t)(w % kRhoCopies) * 2 + par) * batch * r + (size_t)mt * 16 * r;
         wait_producers(rsrc, (size_t)rpg, a.NG, tag, err);
         const bool ok = stage_split(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err);
@@ -779,10 +807,10 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
 #pragma unroll
             for (int kk = 0; kk < KK; ++kk) {
               c0 = mfma_va(ahi[kk], wr[q * KK + kk], c0);
-              c1 = mfma_va(alo[kk], wr[q * KK + kk], c1);
+              if (!MARKOV) c1 = mfma_va(alo[kk], wr[q * KK + kk], c1);
               if (two) {
                 c2 = mfma_va(ahi[kk], wr[q2 * KK + kk], c2);
-                c3 = mfma_va(alo[kk], wr[q2 * KK + kk], c3);
+                if (!MARKOV) c3 = mfma_va(alo[kk], wr[q2 * KK + kk], c3);
               }
             }
           }
@@ -809,7 +837,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
           for (int kk = 0; kk < KK; ++kk) {
             const uint4 bw = s_wtiles[((size_t)lq * KK + kk) * 64 + lane];
             c0 = mfma_vv(ahi[kk], bw, c0);
-            c1 = mfma_vv(alo[kk], bw, c1);
+            if (!MARKOV) c1 = mfma_vv(alo[kk], bw, c1);
           }
         }
         return c0 + c1;
@@ -915,9 +943,9 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   }
 }
 
-template <int KK, typename LT, bool PRIOR, bool NARROW>
+template <int KK, typename LT, bool PRIOR, bool NARROW, bool MARKOV>
 hipError_t launch_k(const PersistArgs& pa, int G, size_t lds, hipStream_t st) {
-  auto kern = k_draft_persistent<KK, LT, PRIOR, NARROW>;
+  auto kern = k_draft_persistent<KK, LT, PRIOR, NARROW, MARKOV>;
   // the dynamic LDS limit is raised to the maximum once per device (a per-call attribute
   // change costs microseconds of host time)
   static std::atomic<uint64_t> raised{0};
@@ -936,14 +964,23 @@ hipError_t launch_k(const PersistArgs& pa, int G, size_t lds, hipStream_t st) {
   return hipLaunchCooperativeKernel((const void*)kern, dim3(G), dim3(kT), args, (unsigned)lds, st);
 }
 
-template <typename LT, bool PRIOR>
+template <typename LT, bool PRIOR, bool MARKOV>
 hipError_t launch_kk(const PersistArgs& pa, int G, size_t lds, hipStream_t st) {
   const bool narrow = pa.batch <= 4;
   switch (pa.r / 32) {
-    case 4: return narrow ? launch_k<4, LT, PRIOR, true>(pa, G, lds, st) : launch_k<4, LT, PRIOR, false>(pa, G, lds, st);
-    case 8: return narrow ? launch_k<8, LT, PRIOR, true>(pa, G, lds, st) : launch_k<8, LT, PRIOR, false>(pa, G, lds, st);
+    case 4:
+      return narrow ? launch_k<4, LT, PRIOR, true, MARKOV>(pa, G, lds, st)
+                    : launch_k<4, LT, PRIOR, false, MARKOV>(pa, G, lds, st);
+    case 8:
+      return narrow ? launch_k<8, LT, PRIOR, true, MARKOV>(pa, G, lds, st)
+                    : launch_k<8, LT, PRIOR, false, MARKOV>(pa, G, lds, st);
   }
   return hipErrorInvalidValue;
+}
+
+template <typename LT, bool PRIOR>
+hipError_t launch_km(const PersistArgs& pa, int G, size_t lds, hipStream_t st) {
+  return pa.e_m ? launch_kk<LT, PRIOR, true>(pa, G, lds, st) : launch_kk<LT, PRIOR, false>(pa, G, lds, st);
 }
 
 }  // namespace
@@ -959,18 +996,19 @@ PersistPlan persist_plan(const dls_local_head& h, int32_t batch, int32_t B, dls_
     pl.why = "shape outside the persistent kernel's range";
     return pl;
   }
-  const int NG = h.H / 16;
-  if (h.H > kStageK && h.H % kStageK) {
+  const bool markov = h.kind == DLS_HEAD_MARKOV;   // no GRU workgroups
+  const int NG = markov ? 0 : h.H / 16;
+  if (!markov && h.H > kStageK && h.H % kStageK) {
     pl.why = "H above 256 must be a multiple of 256";
     return pl;
   }
-  if (NG > G || h.r % NG || h.r / NG > 16) {
+  if (!markov && (NG > G || h.r % NG || h.r / NG > 16)) {
     pl.why = "hidden size / rank do not split over the workgroups";
     return pl;
   }
   pl.G = G;
   pl.NG = NG;
-  pl.rpg = h.r / NG;
+  pl.rpg = markov ? 0 : h.r / NG;
   pl.NT = (h.V + 15) / 16;
   pl.cap_a = 4 * (kOps / KK);
   int rows_max = 0, nl_max = 0;
@@ -984,7 +1022,7 @@ PersistPlan persist_plan(const dls_local_head& h, int32_t batch, int32_t B, dls_
       return pl;
     }
   }
-  const size_t region_gru = (size_t)3 * (h.H / 32) * 1024 + (size_t)pl.rpg * h.H * 2;
+  const size_t region_gru = markov ? 0 : (size_t)3 * (h.H / 32) * 1024 + (size_t)pl.rpg * h.H * 2;
   const size_t region_tiles = (size_t)nl_max * KK * 1024;
   pl.lds_region_a = (std::max(region_gru, region_tiles) + 15) & ~(size_t)15;
   pl.rows_max = rows_max;
@@ -1021,8 +1059,8 @@ PersistWorkspace persist_workspace(const dls_local_head& h, int32_t batch, int32
 hipError_t launch_persistent(const PersistArgs& pa, const PersistPlan& pl, dls_dtype long_dtype, hipStream_t st) {
   const bool pr = pa.prior != nullptr;
   if (long_dtype == DLS_BF16)
-    return pr ? launch_kk<bf16_t, true>(pa, pl.G, pl.lds, st) : launch_kk<bf16_t, false>(pa, pl.G, pl.lds, st);
-  return pr ? launch_kk<float, true>(pa, pl.G, pl.lds, st) : launch_kk<float, false>(pa, pl.G, pl.lds, st);
+    return pr ? launch_km<bf16_t, true>(pa, pl.G, pl.lds, st) : launch_km<bf16_t, false>(pa, pl.G, pl.lds, st);
+  return pr ? launch_km<float, true>(pa, pl.G, pl.lds, st) : launch_km<float, false>(pa, pl.G, pl.lds, st);
 }
 
 }  // namespace dls

@@ -132,14 +132,17 @@ hipError_t launch_prepare(const dls_local_head& h, void* buf, hipStream_t st) {
   k_write_header<<<1, 1, 0, st>>>(hdr, (PreparedHeader*)base);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int Q = 3 * h.H;
-  const int waves = ((h.V + 31) / 32) * (Q / 32);
-  k_fold_input<<<(waves + 3) / 4, 256, 0, st>>>((const bf16_t*)h.emb, (const bf16_t*)h.w_ih, h.V, h.d, Q,
-                                               (float*)(base + L.off_T));
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const bool markov = h.kind == DLS_HEAD_MARKOV;   // no GRU: W_M only
+  if (!markov) {
+    const int Q = 3 * h.H;
+    const int waves = ((h.V + 31) / 32) * (Q / 32);
+    k_fold_input<<<(waves + 3) / 4, 256, 0, st>>>((const bf16_t*)h.emb, (const bf16_t*)h.w_ih, h.V, h.d, Q,
+                                                 (float*)(base + L.off_T));
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   k_pack_vocab<<<2048, 256, 0, st>>>((const bf16_t*)h.w_vocab, h.V, h.r, L.NT, (uint4*)(base + L.off_wv));
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  k_pack_whh<<<512, 256, 0, st>>>((const bf16_t*)h.w_hh, h.H, (uint4*)(base + L.off_whh));
+  if (!markov) k_pack_whh<<<512, 256, 0, st>>>((const bf16_t*)h.w_hh, h.H, (uint4*)(base + L.off_whh));
   return hipGetLastError();
 }
 

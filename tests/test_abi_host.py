@@ -44,9 +44,9 @@ def test_struct_layout_matches_c(tmp_path):
 #include <stddef.h>
 #include "{HEADER}"
 int main(void) {{
-  printf("%zu %zu %zu %zu %zu %zu %zu\\n", sizeof(dls_local_head), sizeof(dls_row_stats), sizeof(dls_fusion),
+  printf("%zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(dls_local_head), sizeof(dls_row_stats), sizeof(dls_fusion),
          offsetof(dls_local_head, dtype), offsetof(dls_local_head, emb), offsetof(dls_local_head, w_vocab),
-         offsetof(dls_fusion, flags));
+         offsetof(dls_fusion, flags), offsetof(dls_local_head, kind));
   return 0;
 }}''')
     exe = tmp_path / "lay"
@@ -54,13 +54,13 @@ int main(void) {{
     got = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True).stdout.split()]
     want = [ctypes.sizeof(b.LocalHeadC), ctypes.sizeof(b.RowStats), ctypes.sizeof(b.Fusion),
             b.LocalHeadC.dtype.offset, b.LocalHeadC.emb.offset, b.LocalHeadC.w_vocab.offset,
-            b.Fusion.flags.offset]
+            b.Fusion.flags.offset, b.LocalHeadC.kind.offset]
     assert got == want
 
 
 def test_header_compiles_as_cpp(tmp_path):
     src = tmp_path / "h.cpp"
-    src.write_text(f'#include "{HEADER}"\nint main() {{ return dls_abi_version() == 1 ? 0 : 1; }}\n')
+    src.write_text(f'#include "{HEADER}"\nint main() {{ return dls_abi_version() == 2 ? 0 : 1; }}\n')
     subprocess.run(["g++", "-std=c++17", "-Wall", "-Werror", "-c", str(src), "-o", str(tmp_path / "h.o")],
                    check=True)
 
@@ -70,12 +70,20 @@ def test_status_strings():
     for code, name in b.STATUS.items():
         assert L.dls_status_string(code).decode() == name
     assert L.dls_status_string(99).decode() == "DLS_UNKNOWN_STATUS"
-    assert L.dls_abi_version() == 1
+    assert L.dls_abi_version() == 2
 
 
 def _head(**kw):
     h = dict(V=1000, d=64, H=32, r=16, dtype=b.DLS_BF16, emb=FAKE[0].value, w_ih=FAKE[1].value,
              w_hh=FAKE[2].value, w_rank=FAKE[3].value, w_vocab=FAKE[4].value)
+    h.update(kw)
+    return b.LocalHeadC(**h)
+
+
+def _markov(**kw):
+    """A Markov head: only E_M (emb) and W_M (w_vocab); d, H and the GRU pointers unused."""
+    h = dict(V=1000, d=0, H=0, r=16, dtype=b.DLS_BF16, emb=FAKE[0].value, w_ih=None, w_hh=None, w_rank=None,
+             w_vocab=FAKE[4].value, kind=b.DLS_HEAD_MARKOV)
     h.update(kw)
     return b.LocalHeadC(**h)
 
@@ -111,6 +119,10 @@ def test_draft_block_rejects_bad_arguments():
         (dict(head=_head(), ws=None), "DLS_ERR_ARG"),
         (dict(head=_head(), f=b.Fusion(1.0, float("nan"), 0.0, 0)), "DLS_ERR_ARG"),
         (dict(head=_head(), f=b.Fusion(1.0, 0.5, 0.0, 0x10)), "DLS_ERR_ARG"),
+        (dict(head=_head(kind=7)), "DLS_ERR_ARG"),
+        (dict(head=_markov(r=12)), "DLS_ERR_SHAPE"),
+        (dict(head=_markov(emb=None)), "DLS_ERR_ARG"),
+        (dict(head=_markov(w_vocab=None)), "DLS_ERR_ARG"),
     ]
     for kw, want in cases:
         head = kw.pop("head")
@@ -125,6 +137,8 @@ def test_draft_block_rejects_bad_arguments():
 @pytest.mark.skipif(HAS_GPU, reason="would launch on fake pointers when a GPU is present")
 def test_valid_arguments_stop_at_device_check():
     rc, msg = _draft(_head())
+    assert b.STATUS[rc] == "DLS_ERR_DEVICE", msg
+    rc, msg = _draft(_markov())          # a valid Markov head with d = H = 0 and no GRU tensors
     assert b.STATUS[rc] == "DLS_ERR_DEVICE", msg
     # the literal first-row reading does not need the last token
     rc, _ = _draft(_head(), last=None, f=b.fusion(first_row_long_only=True))
@@ -175,3 +189,15 @@ def test_workspace_size_queries():
     s64 = L.dls_draft_block_workspace_size(ctypes.byref(h), 64, 16)
     assert 0 < s1 < s64
     assert L.dls_draft_block_workspace_size(None, 1, 16) == 0
+
+
+def test_markov_sizes():
+    """A Markov head needs no GRU buffers: its prepared form is W_M in operand order only."""
+    L = b.lib()
+    m = _markov(V=151936, r=256)
+    assert L.dls_draft_block_workspace_size(ctypes.byref(m), 1, 16) > 0
+    pm = L.dls_prepare_head_size(ctypes.byref(m))
+    nt = (151936 + 15) // 16
+    assert nt * 16 * 256 * 2 <= pm <= nt * 16 * 256 * 2 + 4096
+    h = _head(V=151936, d=2560, H=1024, r=256)
+    assert L.dls_prepare_head_size(ctypes.byref(h)) > pm + 151936 * 3 * 1024 * 4
