@@ -248,6 +248,25 @@ def main():
     log(f"markov head: {m_us:.1f} us per block -> {markov['tokens_per_s']:.0f} drafted tokens/s")
     del mhead, mws
 
+    # ---- unigram log-prior estimation (App. A) from a Zipf-distributed token stream --------
+    n_p = 1 << 26
+    gen = torch.Generator(device=dev).manual_seed(5)
+    ptok = torch.randint(0, wl.V, (n_p,), dtype=torch.int32, device=dev, generator=gen)
+    plogp = torch.empty(wl.V, dtype=torch.float32, device=dev)
+    pcnt = torch.empty(wl.V + 1, dtype=torch.int64, device=dev)
+    for _ in range(3):
+        B.unigram_log_prior(ptok, wl.V, 1.0, out=(plogp, pcnt))
+    e2.record()
+    for _ in range(10):
+        B.unigram_log_prior(ptok, wl.V, 1.0, out=(plogp, pcnt))
+    e3.record()
+    torch.cuda.synchronize()
+    p_us = e2.elapsed_time(e3) / 10 * 1e3
+    prior_est = {"tokens": n_p, "V": wl.V, "us_per_call": round(p_us, 1),
+                 "tokens_per_s": round(n_p / (p_us * 1e-6), 1), "input_GBs": round(4 * n_p / (p_us * 1e-6) / 1e9, 1)}
+    log(f"unigram prior over {n_p} tokens: {p_us:.1f} us ({prior_est['input_GBs']:.0f} GB/s of token ids)")
+    del ptok
+
     # ---- standalone fused combine at the serving shape (cold: inputs larger than the MALL) ----
     R = args.combine_rows
     Lc = B.as_tensor(W.make_logit_rows(R, wl.V, "bf16", 77, "onehot", 3.0, purpose=20), dev)
@@ -303,6 +322,7 @@ def main():
         "combine": combine,
         "draft_block_per_position_launches_us": round(launches_us, 2),
         "markov_head": markov,
+        "prior_estimation": prior_est,
     }
     print(json.dumps(out), flush=True)
 

@@ -207,6 +207,22 @@ dls_status dls_draft_block(const dls_local_head *head, const void *long_logits,
 dls_status dls_accept_len(const int32_t *draft, const int32_t *target, int32_t batch,
                           int32_t B, int32_t *out_len, void *stream);
 
+/* ---------------------------------------------------------------------------------
+ * Unigram log-prior (App. A, prior estimation): the counts c(v) of the tokens that lie
+ * in [0, V) (others are skipped), then
+ *   out_log_prior[v] = log((c(v) + smoothing) / (N + smoothing * V)),
+ * N the number of counted tokens, evaluated in float64 and rounded to float32.  The
+ * result is the `prior` argument of dls_combine_logits and dls_draft_block.
+ *   tokens         [n] int32 (device); the caller selects which tokens count (the paper
+ *                  counts the loss-masked response tokens of the training data)
+ *   out_counts     [V + 1] uint64 (device, caller-owned): c(0..V-1), then N; overwritten
+ *   out_log_prior  [V] float32 (device)
+ *   smoothing      the paper's lambda (1.0 by default); > 0, or 0 (then unseen tokens
+ *                  get -inf)
+ * Limits: 0 <= n <= 2^40, 1 <= V <= 2^24.  Asynchronous on `stream`. */
+dls_status dls_unigram_log_prior(const int32_t *tokens, int64_t n, int32_t V, float smoothing,
+                                 uint64_t *out_counts, float *out_log_prior, void *stream);
+
 /* Names and messages. */
 const char *dls_status_string(dls_status status);
 const char *dls_last_error(void);

@@ -73,6 +73,8 @@ def lib() -> ctypes.CDLL:
         L.dls_prepare_head.argtypes = [ctypes.POINTER(LocalHeadC), _vp, _sz, _vp]
         L.dls_draft_block_path.restype = ctypes.c_int
         L.dls_draft_block_path.argtypes = [ctypes.POINTER(LocalHeadC), _i32, _i32, ctypes.c_int, ctypes.c_int]
+        L.dls_unigram_log_prior.restype = ctypes.c_int
+        L.dls_unigram_log_prior.argtypes = [_vp, _i64, _i32, ctypes.c_float, _vp, _vp, _vp]
         L.dls_accept_len.restype = ctypes.c_int
         L.dls_accept_len.argtypes = [_vp, _vp, _i32, _i32, _vp, _vp]
         L.dls_status_string.restype = ctypes.c_char_p
@@ -271,3 +273,19 @@ def accept_len(draft: torch.Tensor, target: torch.Tensor, out=None, stream=None)
         out = torch.empty(batch, dtype=torch.int32, device=draft.device)
     _check(L.dls_accept_len(_ptr(draft), _ptr(target), batch, B, _ptr(out), _stream(stream)))
     return out
+
+
+def unigram_log_prior(tokens: torch.Tensor, V: int, smoothing: float = 1.0, out=None, stream=None):
+    """Unigram log-prior of a token stream (App. A): returns (log_prior [V] float32,
+    counts [V + 1] int64 holding c(v) and the number of counted tokens)."""
+    L = lib()
+    n = tokens.numel()
+    dev = tokens.device
+    if out is None:
+        counts = torch.empty(V + 1, dtype=torch.int64, device=dev)
+        logp = torch.empty(V, dtype=torch.float32, device=dev)
+    else:
+        logp, counts = out
+    _check(L.dls_unigram_log_prior(_ptr(tokens) if n else None, n, V, smoothing, _ptr(counts), _ptr(logp),
+                                   _stream(stream)))
+    return logp, counts

@@ -327,6 +327,22 @@ int dls_draft_block_path(const dls_local_head* head, int32_t batch, int32_t B, d
   return pl.ok ? 1 : 0;
 }
 
+dls_status dls_unigram_log_prior(const int32_t* tokens, int64_t n, int32_t V, float smoothing, uint64_t* out_counts,
+                                 float* out_log_prior, void* stream) {
+  g_last_error.clear();
+  if (n < 0 || n > ((int64_t)1 << 40)) return fail(DLS_ERR_SHAPE, "n=%lld outside [0, 2^40]", (long long)n);
+  if (V < 1 || V > (1 << 24)) return fail(DLS_ERR_SHAPE, "V=%d outside [1, 2^24]", V);
+  if (!(smoothing >= 0.f) || !std::isfinite(smoothing)) return fail(DLS_ERR_ARG, "smoothing must be finite and >= 0");
+  if (!out_counts || !out_log_prior || (n > 0 && !tokens)) return fail(DLS_ERR_ARG, "required pointer is NULL");
+  if (!aligned(out_counts, 8) || !aligned(out_log_prior, 4) || (tokens && !aligned(tokens, 4)))
+    return fail(DLS_ERR_ARG, "misaligned pointer");
+  dls_status s = check_device();
+  if (s != DLS_OK) return s;
+  hipError_t e = dls::launch_unigram_prior(tokens, n, V, smoothing, out_counts, out_log_prior, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "unigram_log_prior launch");
+  return DLS_OK;
+}
+
 dls_status dls_accept_len(const int32_t* draft, const int32_t* target, int32_t batch, int32_t B, int32_t* out_len,
                           void* stream) {
   g_last_error.clear();

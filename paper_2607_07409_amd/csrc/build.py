@@ -12,7 +12,7 @@ PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
 OBJ_DIR = os.path.join(ROOT, "_build", "dels")
 LIB = os.path.join(PKG, "libdels.so")
-SOURCES = ["api.cpp", "combine.hip", "draft.hip", "accept.hip", "prepare.hip", "draft_persistent.hip"]
+SOURCES = ["api.cpp", "combine.hip", "draft.hip", "accept.hip", "prepare.hip", "draft_persistent.hip", "prior.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-Wall", "-Wno-unused-function",
          # no packed fp32 arithmetic in any generated code

@@ -72,6 +72,8 @@ hipError_t launch_draft(const DraftArgs& a, hipStream_t st);
 
 hipError_t launch_accept(const int32_t* draft, const int32_t* target, int32_t batch, int32_t B,
                          int32_t* out, hipStream_t st);
+hipError_t launch_unigram_prior(const int32_t* tokens, int64_t n, int32_t V, float smoothing, uint64_t* counts,
+                                float* out, hipStream_t st);
 
 // ------------------------------------------------------------------------------------------
 // prepared heads and the persistent drafting kernel

@@ -201,3 +201,21 @@ def test_markov_sizes():
     assert nt * 16 * 256 * 2 <= pm <= nt * 16 * 256 * 2 + 4096
     h = _head(V=151936, d=2560, H=1024, r=256)
     assert L.dls_prepare_head_size(ctypes.byref(h)) > pm + 151936 * 3 * 1024 * 4
+
+
+def test_unigram_prior_rejects_bad_arguments():
+    L = b.lib()
+
+    def call(tokens=FAKE[0], n=100, V=1000, smoothing=1.0, counts=FAKE[1], out=FAKE[2]):
+        return b.STATUS[L.dls_unigram_log_prior(tokens, n, V, smoothing, counts, out, None)]
+
+    assert call(n=-1) == "DLS_ERR_SHAPE"
+    assert call(V=0) == "DLS_ERR_SHAPE"
+    assert call(smoothing=-1.0) == "DLS_ERR_ARG"
+    assert call(smoothing=float("nan")) == "DLS_ERR_ARG"
+    assert call(tokens=None) == "DLS_ERR_ARG"
+    assert call(counts=None) == "DLS_ERR_ARG"
+    assert call(counts=ctypes.c_void_p(FAKE[1].value + 4)) == "DLS_ERR_ARG"
+    if not HAS_GPU:
+        assert call() == "DLS_ERR_DEVICE"
+        assert call(tokens=None, n=0) == "DLS_ERR_DEVICE"
