@@ -198,6 +198,21 @@ dls_status dls_draft_block(const dls_local_head *head, const void *long_logits,
                            dls_row_stats *out_stats, void *workspace, size_t ws_bytes,
                            void *stream);
 
+/* Per-position fusion weights (Sec. 5.6 learns one alpha_j and one beta_j for each
+ * draft position; App. C lists them): host arrays of B values that replace fusion.alpha
+ * and fusion.beta at position j.  NULL keeps the scalar for every position.  Values must
+ * be finite.  Otherwise dls_draft_block_scheduled is dls_draft_block. */
+typedef struct dls_fusion_schedule {
+  const float *alpha;   /* [B] host, or NULL */
+  const float *beta;    /* [B] host, or NULL */
+} dls_fusion_schedule;
+dls_status dls_draft_block_scheduled(const dls_local_head *head, const void *long_logits,
+                                     dls_dtype long_dtype, const int32_t *last_token,
+                                     const float *prior, int32_t batch, int32_t B, dls_fusion fusion,
+                                     dls_fusion_schedule schedule, int32_t *out_tokens,
+                                     dls_row_stats *out_stats, void *workspace, size_t ws_bytes,
+                                     void *stream);
+
 /* ---------------------------------------------------------------------------------
  * Prefix-acceptance length (verification step of Algorithm 1): out_len[b] is the
  * number of leading positions j with draft[b, j] == target[b, j], in [0, B].  The

@@ -217,13 +217,20 @@ class DraftResult:
     margin: np.ndarray          # fused[argmax] - fused[token]
 
 
+def _at(w, j: int) -> float:
+    """A fusion weight at draft position j: one value for all positions, or one per position
+    (Sec. 5.6 learns alpha_j and beta_j for each draft position)."""
+    return float(w[j]) if np.ndim(w) else float(w)
+
+
 def draft_block(head, long_logits, last_token: Sequence[int], prior, w_long: float,
-                alpha: float, beta: float, first_row_long_only: bool = False,
+                alpha, beta, first_row_long_only: bool = False,
                 force: Optional[np.ndarray] = None, sequences: Optional[Sequence[int]] = None
                 ) -> DraftResult:
     """Greedy DeLS-Spec drafting of one block per sequence (Algorithm 1, decoding steps).
 
     long_logits: [batch, B, V] (anything indexable to rows); last_token: [batch].
+    alpha, beta: scalars, or [B] sequences of per-position weights.
     force: optional [batch, B] tokens that replace the decoded ones (statistics are then
     reported for the forced token), used to keep a replay aligned after a near-tie.
     sequences: optional subset of sequence indices to run (others are left at zero).
@@ -241,10 +248,10 @@ def draft_block(head, long_logits, last_token: Sequence[int], prior, w_long: flo
         for j in range(B):
             f = None if force is None else int(force[b, j])
             if first_row_long_only and j == 0:
-                res = combine_row(rows[0], None, None, w_long, alpha, beta, force_token=f)
+                res = combine_row(rows[0], None, None, w_long, _at(alpha, 0), _at(beta, 0), force_token=f)
             else:
                 state, s = head.step(state, u)
-                res = combine_row(rows[j], s, prior, w_long, alpha, beta, force_token=f)
+                res = combine_row(rows[j], s, prior, w_long, _at(alpha, j), _at(beta, j), force_token=f)
             out.tokens[b, j] = res.token
             out.score[b, j] = res.score
             out.logprob[b, j] = res.logprob

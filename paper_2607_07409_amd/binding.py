@@ -34,6 +34,10 @@ class Fusion(ctypes.Structure):
                 ("flags", ctypes.c_uint32)]
 
 
+class Schedule(ctypes.Structure):
+    _fields_ = [("alpha", ctypes.c_void_p), ("beta", ctypes.c_void_p)]
+
+
 class RowStats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_float) for n in STATS_FIELDS]
 
@@ -67,6 +71,9 @@ def lib() -> ctypes.CDLL:
         L.dls_draft_block.restype = ctypes.c_int
         L.dls_draft_block.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
                                       Fusion, _vp, _vp, _vp, _sz, _vp]
+        L.dls_draft_block_scheduled.restype = ctypes.c_int
+        L.dls_draft_block_scheduled.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
+                                                Fusion, Schedule, _vp, _vp, _vp, _sz, _vp]
         L.dls_prepare_head_size.restype = _sz
         L.dls_prepare_head_size.argtypes = [ctypes.POINTER(LocalHeadC)]
         L.dls_prepare_head.restype = ctypes.c_int
@@ -248,7 +255,7 @@ def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional
                 w_long=1.0, alpha=0.3, beta=0.3, first_row_long_only=False, want_stats=True, out=None,
                 workspace=None, stream=None):
     """Draft one block per sequence.  long_logits [batch, B, V]; returns (tokens [batch, B], stats
-    [batch, B, 6] or None)."""
+    [batch, B, 6] or None).  alpha and beta are scalars or [B] per-position weights."""
     L = lib()
     batch, B, V = long_logits.shape
     dev = long_logits.device
@@ -259,9 +266,23 @@ def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional
         tok, st = out
     if workspace is None:
         workspace = draft_workspace(head, batch, B, dev)
-    _check(L.dls_draft_block(ctypes.byref(head.c), _ptr(long_logits), _dtype_code(long_logits), _ptr(last_token),
-                             _ptr(prior), batch, B, fusion(w_long, alpha, beta, first_row_long_only), _ptr(tok),
-                             _ptr(st), _ptr(workspace), workspace.numel(), _stream(stream)))
+    scheduled = np.ndim(alpha) > 0 or np.ndim(beta) > 0
+    f = fusion(w_long, 0.0 if np.ndim(alpha) else alpha, 0.0 if np.ndim(beta) else beta, first_row_long_only)
+    if scheduled:
+        # per-position weights: host arrays of B values (kept alive across the call)
+        al = np.ascontiguousarray(alpha, np.float32) if np.ndim(alpha) else None
+        be = np.ascontiguousarray(beta, np.float32) if np.ndim(beta) else None
+        for arr in (al, be):
+            if arr is not None and arr.shape != (B,):
+                raise ValueError(f"per-position weights need {B} values")
+        sch = Schedule(None if al is None else al.ctypes.data, None if be is None else be.ctypes.data)
+        _check(L.dls_draft_block_scheduled(ctypes.byref(head.c), _ptr(long_logits), _dtype_code(long_logits),
+                                           _ptr(last_token), _ptr(prior), batch, B, f, sch, _ptr(tok), _ptr(st),
+                                           _ptr(workspace), workspace.numel(), _stream(stream)))
+    else:
+        _check(L.dls_draft_block(ctypes.byref(head.c), _ptr(long_logits), _dtype_code(long_logits),
+                                 _ptr(last_token), _ptr(prior), batch, B, f, _ptr(tok), _ptr(st), _ptr(workspace),
+                                 workspace.numel(), _stream(stream)))
     return tok, st
 
 

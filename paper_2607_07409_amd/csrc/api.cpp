@@ -225,11 +225,14 @@ size_t dls_draft_block_workspace_size(const dls_local_head* head, int32_t batch,
   return dls::persist_workspace(ch, batch, B).total + dls::draft_layout(ch, batch, B).total;
 }
 
-dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,
-                           const int32_t* last_token, const float* prior, int32_t batch, int32_t B,
-                           dls_fusion fusion, int32_t* out_tokens, dls_row_stats* out_stats, void* workspace,
-                           size_t ws_bytes, void* stream) {
-  g_last_error.clear();
+}  // extern "C"
+
+namespace {
+
+dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,
+                      const int32_t* last_token, const float* prior, int32_t batch, int32_t B, dls_fusion fusion,
+                      const float* alphas, const float* betas, int32_t* out_tokens, dls_row_stats* out_stats,
+                      void* workspace, size_t ws_bytes, void* stream) {
   dls_status s = check_head(head);
   if (s != DLS_OK) return s;
   if (!valid_dtype(long_dtype)) return fail(DLS_ERR_DTYPE, "unknown long-logit dtype %d", (int)long_dtype);
@@ -237,6 +240,10 @@ dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, 
   if (B < 0 || B > 64) return fail(DLS_ERR_SHAPE, "B=%d outside [0, 64]", B);
   if ((s = check_fusion(fusion)) != DLS_OK) return s;
   if (batch == 0 || B == 0) return DLS_OK;
+  for (int j = 0; j < B; ++j) {
+    if ((alphas && !std::isfinite(alphas[j])) || (betas && !std::isfinite(betas[j])))
+      return fail(DLS_ERR_ARG, "per-position fusion weight %d is not finite", j);
+  }
   const bool literal = (fusion.flags & DLS_FIRST_ROW_LONG_ONLY) != 0;
   if (!long_logits || !out_tokens || (!last_token && !literal))
     return fail(DLS_ERR_ARG, "required pointer is NULL");
@@ -279,8 +286,10 @@ dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, 
       pa.batch = batch;
       pa.B = B;
       pa.wl = fusion.w_long;
-      pa.al = fusion.alpha;
-      pa.be = prior ? fusion.beta : 0.f;
+      for (int j = 0; j < 64; ++j) {
+        pa.al_j[j] = j < B && alphas ? alphas[j] : fusion.alpha;
+        pa.be_j[j] = !prior ? 0.f : (j < B && betas ? betas[j] : fusion.beta);
+      }
       pa.literal = (fusion.flags & DLS_FIRST_ROW_LONG_ONLY) ? 1 : 0;
       pa.out_tokens = out_tokens;
       pa.out_stats = out_stats;
@@ -309,9 +318,33 @@ dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, 
   a.out_stats = out_stats;
   a.ws = (char*)workspace + pw.total;
   a.lay = dls::draft_layout(ch, batch, B);
+  a.alphas = alphas;
+  a.betas = betas;
   hipError_t e = dls::launch_draft(a, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "draft_block launch");
   return DLS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,
+                           const int32_t* last_token, const float* prior, int32_t batch, int32_t B,
+                           dls_fusion fusion, int32_t* out_tokens, dls_row_stats* out_stats, void* workspace,
+                           size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, nullptr, nullptr, out_tokens,
+                    out_stats, workspace, ws_bytes, stream);
+}
+
+dls_status dls_draft_block_scheduled(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,
+                                     const int32_t* last_token, const float* prior, int32_t batch, int32_t B,
+                                     dls_fusion fusion, dls_fusion_schedule schedule, int32_t* out_tokens,
+                                     dls_row_stats* out_stats, void* workspace, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, schedule.alpha,
+                    schedule.beta, out_tokens, out_stats, workspace, ws_bytes, stream);
 }
 
 int dls_draft_block_path(const dls_local_head* head, int32_t batch, int32_t B, dls_dtype long_dtype,

@@ -67,6 +67,8 @@ struct DraftArgs {
   dls_row_stats* out_stats;
   char* ws;
   DraftLayout lay;
+  const float* alphas;       // [B] host per-position weights, or NULL (f.alpha everywhere)
+  const float* betas;        // [B] host, or NULL (f.beta)
 };
 hipError_t launch_draft(const DraftArgs& a, hipStream_t st);
 
@@ -107,7 +109,8 @@ struct PersistArgs {
   const int32_t* last;
   const float* prior;
   int batch, B;
-  float wl, al, be;
+  float wl;
+  float al_j[64], be_j[64];  // fusion weights of each draft position (B <= 64)
   int literal;
   int32_t* out_tokens;
   dls_row_stats* out_stats;

@@ -295,7 +295,7 @@ hipError_t launch_draft_t(const DraftArgs& a, hipStream_t st) {
   const size_t bstride = (size_t)B * V;
   const bool literal = (a.f.flags & DLS_FIRST_ROW_LONG_ONLY) != 0;
   const size_t lds = (size_t)(kBC * r + kBC * a.lay.slice) * sizeof(float);
-  const float wl = a.f.w_long, al = a.f.alpha, be = a.f.beta;
+  const float wl = a.f.w_long;
   hipError_t e;
 
   const int32_t* tok_in = a.last_token;
@@ -304,6 +304,8 @@ hipError_t launch_draft_t(const DraftArgs& a, hipStream_t st) {
   bool first_head_step = true;
   for (int j = 0; j < B; ++j) {
     const bool long_only = literal && j == 0;
+    const float al = a.alphas ? a.alphas[j] : a.f.alpha;
+    const float be = a.prior ? (a.betas ? a.betas[j] : a.f.beta) : 0.f;
     if (!long_only && hd.kind == DLS_HEAD_MARKOV) {
       k_markov_rho<WT><<<(batch * r + kThreads - 1) / kThreads, kThreads, 0, st>>>(emb, V, r, tok_in, rho, batch);
       if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -453,7 +453,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   __syncthreads();
 
   const LT* L = (const LT*)a.L;
-  const float wl = a.wl, al = a.al, be = a.be;
+  const float wl = a.wl;
 
   // Tokens of position jm (the argmax keys of all workgroups, max-reduced through LDS atomics)
   // into s_tok; workgroup 0 also writes the drafted tokens.  Workgroup-uniform result.
@@ -524,6 +524,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     const uint32_t tag = (epoch << 8) | (uint32_t)(j + 1);
     const uint32_t tag8 = (uint32_t)(j + 1);
     const int par = j & 1;
+    const float al = a.al_j[j], be = a.be_j[j];   // this position's fusion weights
     const bool long_only = a.literal && j == 0;
     const int hs = a.literal ? j - 1 : j;          // head step index (the first one starts from h = 0)
 
@@ -932,7 +933,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       P = block_merge(P, s_part, 4);
       if (tid == 0) {
         int dummy;
-        finalize_row(P, wl, al, a.literal && jm == 0, &dummy, a.out_stats + (size_t)b * Bk + jm, nullptr);
+        finalize_row(P, wl, a.al_j[jm], a.literal && jm == 0, &dummy, a.out_stats + (size_t)b * Bk + jm, nullptr);
       }
       __syncthreads();
     }

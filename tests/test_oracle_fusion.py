@@ -247,3 +247,30 @@ def test_decision_precision_float32():
     assert O.combine_row(L, np.zeros(3), None, 1.0, 0.0, 0.0).token == 0
     L2 = np.array([1.0, 1.0 + 1e-5, 0.0])
     assert O.combine_row(L2, np.zeros(3), None, 1.0, 0.0, 0.0).token == 1
+
+
+def test_per_position_weights():
+    """Per-position alpha_j / beta_j (Sec. 5.6): a constant schedule is the scalar run; a schedule
+    is the same as drafting each row with its own scalars, fed the same previous tokens; alpha_j = 0
+    at a row gives that row the long logits' argmax (minus the prior term)."""
+    g = np.random.default_rng(23)
+    head = _rnn_head(5, scale=2.0)
+    L = g.normal(0, 1, (2, 6, 97))
+    P = np.log(g.dirichlet(np.ones(97)))
+    sc = O.draft_block(head, L, [4, 9], P, 1.0, 0.4, 0.2)
+    cs = O.draft_block(head, L, [4, 9], P, 1.0, [0.4] * 6, [0.2] * 6)
+    np.testing.assert_array_equal(sc.tokens, cs.tokens)
+    np.testing.assert_array_equal(sc.score, cs.score)
+    al = [0.0, 0.3, 1.0, 0.0, 2.0, 0.5]
+    be = [0.1, 0.0, 0.7, 0.3, 0.0, 1.0]
+    res = O.draft_block(head, L, [4, 9], P, 1.0, al, be)
+    for b, last in enumerate([4, 9]):
+        state, u = head.init_state(), last
+        for j in range(6):
+            state, s = head.step(state, u)
+            r = O.combine_row(L[b, j], s, P, 1.0, al[j], be[j])
+            assert res.tokens[b, j] == r.token and abs(res.score[b, j] - r.score) < 1e-12
+            if al[j] == 0.0:
+                fused = (L[b, j] - be[j] * P).astype(np.float32)
+                assert res.tokens[b, j] == int(np.argmax(fused))
+            u = r.token
