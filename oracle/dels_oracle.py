@@ -106,11 +106,18 @@ def top2_gap(fused: np.ndarray) -> float:
 
 
 def combine_row(long_row, short_row, prior, w_long: float, alpha: float, beta: float,
-                force_token: Optional[int] = None, want_scores: bool = False) -> RowResult:
-    """Fuse one row of long and short logits, decode greedily and report its statistics.
+                force_token: Optional[int] = None, want_scores: bool = False,
+                temperature: float = 0.0, gumbel: Optional[np.ndarray] = None) -> RowResult:
+    """Fuse one row of long and short logits, decode and report its statistics.
 
     With short_row = None the row is decoded from the long logits alone (no prior
     either), as for the first position of Algorithm 1.
+
+    temperature = 0 decodes greedily.  temperature T > 0 samples from softmax(l / T) (the
+    Decode step of Algorithm 1 at T; the paper reports T = 0 and T = 1) by the Gumbel-max
+    rule: the token is the argmax of l / T + g for the given standard Gumbel noise g [V].
+    The statistics then refer to softmax(l / T): lse_fused = log sum exp(l / T),
+    logprob = l_tok / T - lse_fused, and the gap and margin are those of l / T + g.
     """
     long_row = np.asarray(long_row, dtype=F64)
     if short_row is None:
@@ -122,13 +129,19 @@ def combine_row(long_row, short_row, prior, w_long: float, alpha: float, beta: f
         lse_s = logsumexp(short_row)
         a_eff = alpha
     lse_l = logsumexp(long_row)
-    lse_f = logsumexp(fused)
-    best = greedy_token(fused)
+    if temperature > 0:
+        scaled = fused / F64(temperature)
+        decide = scaled + np.asarray(gumbel, dtype=F64)     # Gumbel-max
+    else:
+        scaled = fused
+        decide = fused
+    lse_f = logsumexp(scaled)
+    best = greedy_token(decide)
     tok = best if force_token is None else int(force_token)
     norm = F64(w_long) * lse_l + (F64(a_eff) * lse_s if short_row is not None else 0.0)
-    res = RowResult(token=tok, score=float(fused[tok] - norm), logprob=float(fused[tok] - lse_f),
-                    gap=top2_gap(fused), lse_long=lse_l, lse_short=lse_s, lse_fused=lse_f,
-                    argmax=best, margin=float(fused[best] - fused[tok]))
+    res = RowResult(token=tok, score=float(fused[tok] - norm), logprob=float(scaled[tok] - lse_f),
+                    gap=top2_gap(decide), lse_long=lse_l, lse_short=lse_s, lse_fused=lse_f,
+                    argmax=best, margin=float(decide[best] - decide[tok]))
     if want_scores:
         res.scores = fused - norm
     return res
@@ -140,6 +153,47 @@ def combine_rows(long_rows, short_rows, prior, w_long, alpha, beta, want_scores=
     short_rows = np.asarray(short_rows, dtype=F64)
     return [combine_row(long_rows[i], short_rows[i], prior, w_long, alpha, beta,
                         want_scores=want_scores) for i in range(long_rows.shape[0])]
+
+
+# ----------------------------------------------------------------------------------------
+# sampling noise: Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as
+# easy as 1, 2, 3", SC 2011) keyed by the seed, one counter per 4 vocabulary entries of a row
+# ----------------------------------------------------------------------------------------
+PHILOX_M0, PHILOX_M1 = 0xD2511F53, 0xCD9E8D57      # round multipliers
+PHILOX_W0, PHILOX_W1 = 0x9E3779B9, 0xBB67AE85      # key increments (Weyl sequence)
+MASK32 = 0xFFFFFFFF
+
+
+def philox4x32(counter, key, rounds: int = 10) -> np.ndarray:
+    """Philox4x32 over counters [..., 4] (uint32) with key (k0, k1): each round multiplies
+    words 0 and 2 by the round constants (64-bit products), and mixes the high halves with
+    the other words and the key; the key advances by the Weyl constants between rounds."""
+    c = [np.asarray(counter, dtype=np.uint64)[..., i] for i in range(4)]
+    k0, k1 = np.uint64(key[0] & MASK32), np.uint64(key[1] & MASK32)
+    m = np.uint64(MASK32)
+    for r in range(rounds):
+        if r > 0:
+            k0 = (k0 + np.uint64(PHILOX_W0)) & m
+            k1 = (k1 + np.uint64(PHILOX_W1)) & m
+        p0 = np.uint64(PHILOX_M0) * c[0]
+        p1 = np.uint64(PHILOX_M1) * c[2]
+        c = [(p1 >> np.uint64(32)) ^ c[1] ^ k0, p1 & m, (p0 >> np.uint64(32)) ^ c[3] ^ k1, p0 & m]
+    return np.stack(c, axis=-1).astype(np.uint32)
+
+
+def uniforms_row(seed: int, b: int, j: int, V: int) -> np.ndarray:
+    """The uniform of vocabulary entry v of row (sequence b, position j): word v % 4 of
+    Philox4x32-10 at counter (v // 4, j, b, 0) with key (seed low, seed high), as
+    ((x >> 9) + 1/2) / 2^23, which lies in (0, 1) and is exact in float32."""
+    q = np.arange((V + 3) // 4, dtype=np.uint64)
+    ctr = np.stack([q, np.full_like(q, j), np.full_like(q, b), np.zeros_like(q)], axis=-1)
+    x = philox4x32(ctr, (seed & MASK32, (seed >> 32) & MASK32)).reshape(-1)[:V].astype(np.uint64)
+    return ((x >> np.uint64(9)).astype(F64) + 0.5) * 2.0 ** -23
+
+
+def gumbel_row(seed: int, b: int, j: int, V: int) -> np.ndarray:
+    """Standard Gumbel noise g = -log(-log u) of a row."""
+    return -np.log(-np.log(uniforms_row(seed, b, j, V)))
 
 
 # ----------------------------------------------------------------------------------------
@@ -225,12 +279,14 @@ def _at(w, j: int) -> float:
 
 def draft_block(head, long_logits, last_token: Sequence[int], prior, w_long: float,
                 alpha, beta, first_row_long_only: bool = False,
-                force: Optional[np.ndarray] = None, sequences: Optional[Sequence[int]] = None
-                ) -> DraftResult:
+                force: Optional[np.ndarray] = None, sequences: Optional[Sequence[int]] = None,
+                temperature: float = 0.0, seed: int = 0) -> DraftResult:
     """Greedy DeLS-Spec drafting of one block per sequence (Algorithm 1, decoding steps).
 
     long_logits: [batch, B, V] (anything indexable to rows); last_token: [batch].
     alpha, beta: scalars, or [B] sequences of per-position weights.
+    temperature > 0 samples every row (see combine_row) with the Gumbel noise of
+    gumbel_row(seed, b, j, V).
     force: optional [batch, B] tokens that replace the decoded ones (statistics are then
     reported for the forced token), used to keep a replay aligned after a near-tie.
     sequences: optional subset of sequence indices to run (others are left at zero).
@@ -247,11 +303,14 @@ def draft_block(head, long_logits, last_token: Sequence[int], prior, w_long: flo
         u = int(last_token[b])
         for j in range(B):
             f = None if force is None else int(force[b, j])
+            g = gumbel_row(seed, b, j, rows.shape[1]) if temperature > 0 else None
             if first_row_long_only and j == 0:
-                res = combine_row(rows[0], None, None, w_long, _at(alpha, 0), _at(beta, 0), force_token=f)
+                res = combine_row(rows[0], None, None, w_long, _at(alpha, 0), _at(beta, 0), force_token=f,
+                                  temperature=temperature, gumbel=g)
             else:
                 state, s = head.step(state, u)
-                res = combine_row(rows[j], s, prior, w_long, _at(alpha, j), _at(beta, j), force_token=f)
+                res = combine_row(rows[j], s, prior, w_long, _at(alpha, j), _at(beta, j), force_token=f,
+                                  temperature=temperature, gumbel=g)
             out.tokens[b, j] = res.token
             out.score[b, j] = res.score
             out.logprob[b, j] = res.logprob

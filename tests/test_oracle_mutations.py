@@ -12,7 +12,8 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 PIN_TESTS = [os.path.join(ROOT, "tests", f) for f in
-             ("test_oracle_fusion.py", "test_oracle_head.py", "test_oracle_accept.py")]
+             ("test_oracle_fusion.py", "test_oracle_head.py", "test_oracle_accept.py",
+              "test_oracle_sampling.py")]
 
 MUTATIONS = {
     "prior_sign": ("f = f - F64(beta) * np.asarray(prior", "f = f + F64(beta) * np.asarray(prior"),
@@ -28,7 +29,7 @@ MUTATIONS = {
     "lse_no_shift": ("return float(m + np.log(np.sum(np.exp(x - m))))",
                      "return float(m + np.log(np.sum(np.exp(x))))"),
     "score_norm_drop_wlong": ("norm = F64(w_long) * lse_l", "norm = lse_l"),
-    "logprob_wrong_lse": ("logprob=float(fused[tok] - lse_f)", "logprob=float(fused[tok] - lse_l)"),
+    "logprob_wrong_lse": ("logprob=float(scaled[tok] - lse_f)", "logprob=float(scaled[tok] - lse_l)"),
     "gap_top1_only": ("return float(top[1] - top[0])", "return float(top[1])"),
     "accept_off_by_one": ("while a < B and draft[b, a] == target[b, a]",
                           "while a < B - 1 and draft[b, a] == target[b, a]"),
@@ -40,6 +41,13 @@ MUTATIONS = {
                                   "                state, s = head.step(head.init_state(), u)"),
     "gain_ratio_denominator": ("(tau_dels - tau_base) / (tau_joint - tau_base)",
                                "(tau_dels - tau_base) / (tau_joint)"),
+    "philox_multiplier_swap": ("p0 = np.uint64(PHILOX_M0) * c[0]", "p0 = np.uint64(PHILOX_M1) * c[0]"),
+    "philox_no_key_bump": ("k0 = (k0 + np.uint64(PHILOX_W0)) & m", "k0 = k0 & m"),
+    "gumbel_single_log": ("return -np.log(-np.log(uniforms_row(seed, b, j, V)))",
+                          "return -np.log(uniforms_row(seed, b, j, V))"),
+    "temperature_ignored": ("scaled = fused / F64(temperature)", "scaled = fused"),
+    "uniform_no_half": ("return ((x >> np.uint64(9)).astype(F64) + 0.5) * 2.0 ** -23",
+                        "return ((x >> np.uint64(9)).astype(F64)) * 2.0 ** -23"),
 }
 
 
