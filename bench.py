@@ -228,6 +228,23 @@ def main():
     launches_us = e2.elapsed_time(e3) / 20 * 1e3
     log(f"per-position launches: {launches_us:.1f} us per block")
 
+    # ---- temperature sampling (T = 1, Gumbel-max with Philox noise) on the same block --------
+    for _ in range(3):
+        B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws, temperature=1.0,
+                      seed=12345)
+    e2.record()
+    for i in range(n_k):
+        B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws, temperature=1.0,
+                      seed=12345 + i)
+    e3.record()
+    torch.cuda.synchronize()
+    assert B.workspace_error(ws) == 0, "persistent kernel reported a stalled hand-off"
+    s_us = e2.elapsed_time(e3) / n_k * 1e3
+    sampling = {"temperature": 1.0, "us_per_block": round(s_us, 2),
+                "tokens_per_s": round(wl.batch * wl.B / (s_us * 1e-6), 1),
+                "overhead_vs_greedy": round(s_us / blk_us - 1.0, 4)}
+    log(f"sampling at T = 1: {s_us:.1f} us per block -> {sampling['tokens_per_s']:.0f} drafted tokens/s")
+
     # ---- the Markov local head (App. A) on the same workload: rho = E_M[previous token] ------
     import math
     em, wm = W.make_markov_head(wl.V, wl.r, "bf16", wl.seed, scale=math.sqrt(3.0 / math.sqrt(wl.r)))
@@ -321,6 +338,7 @@ def main():
         "cpu_baseline": cpu,
         "combine": combine,
         "draft_block_per_position_launches_us": round(launches_us, 2),
+        "sampling": sampling,
         "markov_head": markov,
         "prior_estimation": prior_est,
     }

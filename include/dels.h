@@ -213,6 +213,29 @@ dls_status dls_draft_block_scheduled(const dls_local_head *head, const void *lon
                                      dls_row_stats *out_stats, void *workspace, size_t ws_bytes,
                                      void *stream);
 
+/* Temperature sampling (the Decode step of Algorithm 1 at temperature T; the paper
+ * reports T = 0 and T = 1).  temperature = 0 is greedy decoding, exactly as in
+ * dls_draft_block.  A finite T > 0 draws each drafted token from softmax(l / T) by the
+ * Gumbel-max rule: the token is the argmax over v of l_v / T + g_v, with g_v standard
+ * Gumbel noise -log(-log u_v).  u_v of row (sequence b, position j) is word v mod 4 of
+ * Philox4x32-10 (Salmon et al., SC 2011) at counter (v / 4, j, b, 0) under the key
+ * (seed mod 2^32, seed / 2^32), mapped as ((x >> 9) + 1/2) / 2^23; the draws therefore
+ * depend on (seed, b, j, v) only, not on the batch size, the path or the launch shape.
+ * With T > 0 the row statistics refer to the sampled distribution: logprob =
+ * l_t / T - lse_fused, lse_fused = log-sum-exp of l / T, gap = top-1 minus top-2 of
+ * l / T + g; score keeps its definition (it does not depend on T). */
+typedef struct dls_sampling {
+  float temperature;   /* 0 (greedy) or finite > 0 */
+  uint32_t reserved;   /* 0 */
+  uint64_t seed;
+} dls_sampling;
+dls_status dls_draft_block_sampled(const dls_local_head *head, const void *long_logits,
+                                   dls_dtype long_dtype, const int32_t *last_token,
+                                   const float *prior, int32_t batch, int32_t B, dls_fusion fusion,
+                                   dls_fusion_schedule schedule, dls_sampling sampling,
+                                   int32_t *out_tokens, dls_row_stats *out_stats, void *workspace,
+                                   size_t ws_bytes, void *stream);
+
 /* ---------------------------------------------------------------------------------
  * Prefix-acceptance length (verification step of Algorithm 1): out_len[b] is the
  * number of leading positions j with draft[b, j] == target[b, j], in [0, B].  The

@@ -38,6 +38,10 @@ class Schedule(ctypes.Structure):
     _fields_ = [("alpha", ctypes.c_void_p), ("beta", ctypes.c_void_p)]
 
 
+class Sampling(ctypes.Structure):
+    _fields_ = [("temperature", ctypes.c_float), ("reserved", ctypes.c_uint32), ("seed", ctypes.c_uint64)]
+
+
 class RowStats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_float) for n in STATS_FIELDS]
 
@@ -74,6 +78,9 @@ def lib() -> ctypes.CDLL:
         L.dls_draft_block_scheduled.restype = ctypes.c_int
         L.dls_draft_block_scheduled.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
                                                 Fusion, Schedule, _vp, _vp, _vp, _sz, _vp]
+        L.dls_draft_block_sampled.restype = ctypes.c_int
+        L.dls_draft_block_sampled.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
+                                              Fusion, Schedule, Sampling, _vp, _vp, _vp, _sz, _vp]
         L.dls_prepare_head_size.restype = _sz
         L.dls_prepare_head_size.argtypes = [ctypes.POINTER(LocalHeadC)]
         L.dls_prepare_head.restype = ctypes.c_int
@@ -253,9 +260,11 @@ def workspace_error(workspace: torch.Tensor) -> int:
 
 def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional[torch.Tensor], prior=None,
                 w_long=1.0, alpha=0.3, beta=0.3, first_row_long_only=False, want_stats=True, out=None,
-                workspace=None, stream=None):
+                workspace=None, stream=None, temperature=0.0, seed=0):
     """Draft one block per sequence.  long_logits [batch, B, V]; returns (tokens [batch, B], stats
-    [batch, B, 6] or None).  alpha and beta are scalars or [B] per-position weights."""
+    [batch, B, 6] or None).  alpha and beta are scalars or [B] per-position weights.
+    temperature 0 decodes greedily; T > 0 samples from softmax(l / T) with the Philox noise of
+    `seed` (a 64-bit integer)."""
     L = lib()
     batch, B, V = long_logits.shape
     dev = long_logits.device
@@ -267,8 +276,9 @@ def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional
     if workspace is None:
         workspace = draft_workspace(head, batch, B, dev)
     scheduled = np.ndim(alpha) > 0 or np.ndim(beta) > 0
+    sampled = temperature != 0.0
     f = fusion(w_long, 0.0 if np.ndim(alpha) else alpha, 0.0 if np.ndim(beta) else beta, first_row_long_only)
-    if scheduled:
+    if scheduled or sampled:
         # per-position weights: host arrays of B values (kept alive across the call)
         al = np.ascontiguousarray(alpha, np.float32) if np.ndim(alpha) else None
         be = np.ascontiguousarray(beta, np.float32) if np.ndim(beta) else None
@@ -276,9 +286,15 @@ def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional
             if arr is not None and arr.shape != (B,):
                 raise ValueError(f"per-position weights need {B} values")
         sch = Schedule(None if al is None else al.ctypes.data, None if be is None else be.ctypes.data)
-        _check(L.dls_draft_block_scheduled(ctypes.byref(head.c), _ptr(long_logits), _dtype_code(long_logits),
-                                           _ptr(last_token), _ptr(prior), batch, B, f, sch, _ptr(tok), _ptr(st),
-                                           _ptr(workspace), workspace.numel(), _stream(stream)))
+        if sampled:
+            smp = Sampling(float(temperature), 0, int(seed) & 0xFFFFFFFFFFFFFFFF)
+            _check(L.dls_draft_block_sampled(ctypes.byref(head.c), _ptr(long_logits), _dtype_code(long_logits),
+                                             _ptr(last_token), _ptr(prior), batch, B, f, sch, smp, _ptr(tok),
+                                             _ptr(st), _ptr(workspace), workspace.numel(), _stream(stream)))
+        else:
+            _check(L.dls_draft_block_scheduled(ctypes.byref(head.c), _ptr(long_logits), _dtype_code(long_logits),
+                                               _ptr(last_token), _ptr(prior), batch, B, f, sch, _ptr(tok),
+                                               _ptr(st), _ptr(workspace), workspace.numel(), _stream(stream)))
     else:
         _check(L.dls_draft_block(ctypes.byref(head.c), _ptr(long_logits), _dtype_code(long_logits),
                                  _ptr(last_token), _ptr(prior), batch, B, f, _ptr(tok), _ptr(st), _ptr(workspace),

@@ -231,8 +231,8 @@ namespace {
 
 dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,
                       const int32_t* last_token, const float* prior, int32_t batch, int32_t B, dls_fusion fusion,
-                      const float* alphas, const float* betas, int32_t* out_tokens, dls_row_stats* out_stats,
-                      void* workspace, size_t ws_bytes, void* stream) {
+                      const float* alphas, const float* betas, dls_sampling sampling, int32_t* out_tokens,
+                      dls_row_stats* out_stats, void* workspace, size_t ws_bytes, void* stream) {
   dls_status s = check_head(head);
   if (s != DLS_OK) return s;
   if (!valid_dtype(long_dtype)) return fail(DLS_ERR_DTYPE, "unknown long-logit dtype %d", (int)long_dtype);
@@ -244,6 +244,15 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_d
     if ((alphas && !std::isfinite(alphas[j])) || (betas && !std::isfinite(betas[j])))
       return fail(DLS_ERR_ARG, "per-position fusion weight %d is not finite", j);
   }
+  const float T = sampling.temperature;
+  if (sampling.reserved != 0) return fail(DLS_ERR_ARG, "sampling.reserved must be 0");
+  if (!(T == 0.f || (T > 0.f && T <= 1e30f && std::isfinite(1.f / T))))
+    return fail(DLS_ERR_ARG, "temperature %g must be 0 or a finite positive value with a finite inverse", (double)T);
+  dls::Sampler smp;
+  smp.inv_temp = T > 0.f ? 1.f / T : 0.f;
+  smp.temp = T > 0.f ? T : 1.f;
+  smp.seed_lo = (uint32_t)sampling.seed;
+  smp.seed_hi = (uint32_t)(sampling.seed >> 32);
   const bool literal = (fusion.flags & DLS_FIRST_ROW_LONG_ONLY) != 0;
   if (!long_logits || !out_tokens || (!last_token && !literal))
     return fail(DLS_ERR_ARG, "required pointer is NULL");
@@ -291,6 +300,7 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_d
         pa.be_j[j] = !prior ? 0.f : (j < B && betas ? betas[j] : fusion.beta);
       }
       pa.literal = (fusion.flags & DLS_FIRST_ROW_LONG_ONLY) ? 1 : 0;
+      pa.smp = smp;
       pa.out_tokens = out_tokens;
       pa.out_stats = out_stats;
       pa.hdr = (uint32_t*)ws;
@@ -320,6 +330,7 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_d
   a.lay = dls::draft_layout(ch, batch, B);
   a.alphas = alphas;
   a.betas = betas;
+  a.smp = smp;
   hipError_t e = dls::launch_draft(a, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "draft_block launch");
   return DLS_OK;
@@ -334,8 +345,8 @@ dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, 
                            dls_fusion fusion, int32_t* out_tokens, dls_row_stats* out_stats, void* workspace,
                            size_t ws_bytes, void* stream) {
   g_last_error.clear();
-  return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, nullptr, nullptr, out_tokens,
-                    out_stats, workspace, ws_bytes, stream);
+  return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, nullptr, nullptr,
+                    dls_sampling{0.f, 0u, 0ull}, out_tokens, out_stats, workspace, ws_bytes, stream);
 }
 
 dls_status dls_draft_block_scheduled(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,
@@ -344,7 +355,17 @@ dls_status dls_draft_block_scheduled(const dls_local_head* head, const void* lon
                                      dls_row_stats* out_stats, void* workspace, size_t ws_bytes, void* stream) {
   g_last_error.clear();
   return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, schedule.alpha,
-                    schedule.beta, out_tokens, out_stats, workspace, ws_bytes, stream);
+                    schedule.beta, dls_sampling{0.f, 0u, 0ull}, out_tokens, out_stats, workspace, ws_bytes, stream);
+}
+
+dls_status dls_draft_block_sampled(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,
+                                   const int32_t* last_token, const float* prior, int32_t batch, int32_t B,
+                                   dls_fusion fusion, dls_fusion_schedule schedule, dls_sampling sampling,
+                                   int32_t* out_tokens, dls_row_stats* out_stats, void* workspace, size_t ws_bytes,
+                                   void* stream) {
+  g_last_error.clear();
+  return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, schedule.alpha,
+                    schedule.beta, sampling, out_tokens, out_stats, workspace, ws_bytes, stream);
 }
 
 int dls_draft_block_path(const dls_local_head* head, int32_t batch, int32_t B, dls_dtype long_dtype,

@@ -12,7 +12,10 @@ PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
 OBJ_DIR = os.path.join(ROOT, "_build", "dels")
 LIB = os.path.join(PKG, "libdels.so")
-SOURCES = ["api.cpp", "combine.hip", "draft.hip", "accept.hip", "prepare.hip", "draft_persistent.hip", "prior.hip"]
+SOURCES = ["api.cpp", "combine.hip", "draft.hip", "accept.hip", "prepare.hip", "draft_persistent.hip", "prior.hip",
+           # the persistent kernel's instantiations, one unit per rank size and decoding mode
+           "persist_greedy_r128.hip", "persist_greedy_r256.hip", "persist_sampled_r128.hip",
+           "persist_sampled_r256.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-Wall", "-Wno-unused-function",
          # no packed fp32 arithmetic in any generated code

@@ -206,4 +206,57 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// ------------------------------------------------------------------------------
+// Temperature sampling of a draft row by the Gumbel-max rule: the token is the argmax of
+// l / T + g with standard Gumbel noise g.  The noise of vocabulary entry v of row (sequence
+// b, position j) is word v % 4 of Philox4x32-10 (Salmon et al. 2011) at counter
+// (v / 4, j, b, 0) with key (seed low, seed high); u = ((x >> 9) + 1/2) / 2^23 in (0, 1);
+// g = -log(-log u).
+// ------------------------------------------------------------------------------
+struct Sampler {
+  float inv_temp;   // 1 / T; 0 decodes greedily
+  float temp;       // T (1 when greedy)
+  uint32_t seed_lo, seed_hi;
+};
+
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
+    const uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
+    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+  }
+  return c;
+}
+
+// Gumbel noise of one Philox output word x: u = ((x >> 9) + 1/2) / 2^23, g = -log(-log u).
+__device__ __forceinline__ float gumbel_from_word(uint32_t x) {
+  const uint32_t m = x >> 9;
+  // e = -log u.  For u >= 3/4 the series -log(1 - w) = w + w^2/2 + w^3/3 + ... in the exact
+  // w = 1 - u <= 1/4 keeps float32 accuracy where the logarithm of u itself would lose it;
+  // thirteen terms suffice.  Both forms are evaluated and one is selected (no divergence).
+  const float w = ((float)((1u << 23) - m) - 0.5f) * 0x1p-23f;
+  float s = 1.0f / 13.0f;
+#pragma unroll
+  for (int k = 12; k >= 1; --k) s = __builtin_fmaf(s, w, 1.0f / (float)k);
+  const float e_series = s * w;
+  const float e_log = -fast_log2(((float)m + 0.5f) * 0x1p-23f) * kLn2;
+  const float e = m >= (3u << 21) ? e_series : e_log;
+  return -fast_log2(e) * kLn2;
+}
+
+__device__ __forceinline__ uint4 philox_row(const Sampler& sm, int b, int j, int v) {
+  return philox4x32_10(make_uint4((uint32_t)v >> 2, (uint32_t)j, (uint32_t)b, 0u), sm.seed_lo, sm.seed_hi);
+}
+
+__device__ __forceinline__ float gumbel_at(const Sampler& sm, int b, int j, int v) {
+  const uint4 x4 = philox_row(sm, b, j, v);
+  const int w4 = v & 3;
+  return gumbel_from_word(w4 == 0 ? x4.x : (w4 == 1 ? x4.y : (w4 == 2 ? x4.z : x4.w)));
+}
+
 }  // namespace dls

@@ -11,17 +11,21 @@
 namespace dls {
 
 // Turn the merged statistics of a whole row into the decoded token and row statistics.
-// has_short = false marks a row decoded from the long logits alone.
+// long_only marks a row decoded from the long logits alone.  A sampled row (temperature T)
+// folded l / T into the fused log-sum-exp and l / T + g into the top-2: g_tok is the noise
+// of the chosen token, so P.t1 - g_tok is l_tok / T.  Greedy rows pass g_tok = 0, temp = 1.
 __device__ __forceinline__ void finalize_row(const Partial& P, float wl, float al, bool long_only,
-                                             int32_t* tok, dls_row_stats* st, float* norm) {
+                                             int32_t* tok, dls_row_stats* st, float* norm, float g_tok = 0.f,
+                                             float temp = 1.f) {
   const int t = P.i1 == 0x7fffffff ? 0 : P.i1;   // every value -inf: the first index
   *tok = t;
   const float lse_l = lse_value(P.L);
   const float lse_s = long_only ? __builtin_nanf("") : lse_value(P.S);
   const float nr = long_only ? wl * lse_l : __builtin_fmaf(al, lse_s, wl * lse_l);
   if (st) {
-    st->score = P.t1 - nr;
-    st->logprob = P.t1 - lse_value(P.F);
+    const float ft = P.t1 - g_tok;   // l_tok / T
+    st->score = ft * temp - nr;
+    st->logprob = ft - lse_value(P.F);
     st->gap = P.t1 - P.t2;
     st->lse_long = lse_l;
     st->lse_short = lse_s;
@@ -69,6 +73,7 @@ struct DraftArgs {
   DraftLayout lay;
   const float* alphas;       // [B] host per-position weights, or NULL (f.alpha everywhere)
   const float* betas;        // [B] host, or NULL (f.beta)
+  Sampler smp;               // temperature sampling (smp.inv_temp = 0: greedy)
 };
 hipError_t launch_draft(const DraftArgs& a, hipStream_t st);
 
@@ -112,6 +117,7 @@ struct PersistArgs {
   float wl;
   float al_j[64], be_j[64];  // fusion weights of each draft position (B <= 64)
   int literal;
+  Sampler smp;               // temperature sampling (smp.inv_temp = 0: greedy)
   int32_t* out_tokens;
   dls_row_stats* out_stats;
   uint32_t* hdr;             // [0] call epoch, [1] error word
@@ -129,7 +135,7 @@ struct PersistPlan {
 struct PersistWorkspace {
   size_t off_keys, off_h, off_rho, off_stats, total;
 };
-__host__ __device__ void persist_tile_range(int w, int G, int NG, int NT, int cap_a, int* t0, int* n);
+__host__ __device__ inline void persist_tile_range(int w, int G, int NG, int NT, int cap_a, int* t0, int* n);
 PersistPlan persist_plan(const dls_local_head& h, int32_t batch, int32_t B, dls_dtype long_dtype, bool prior, int G);
 PersistWorkspace persist_workspace(const dls_local_head& h, int32_t batch, int32_t B);
 hipError_t launch_persistent(const PersistArgs& pa, const PersistPlan& pl, dls_dtype long_dtype, hipStream_t st);

@@ -160,7 +160,8 @@ __global__ __launch_bounds__(kThreads) void k_lmhead(const WT* __restrict__ w_vo
                                                      const LT* __restrict__ long_j, size_t long_bstride,
                                                      const float* __restrict__ prior, float wl, float al,
                                                      float be, int slice, int long_only,
-                                                     Partial* __restrict__ partials, int batch) {
+                                                     Partial* __restrict__ partials, int batch, Sampler smp,
+                                                     int j) {
   constexpr int N = Chunk<WT>::N;
   extern __shared__ float smem[];
   float* s_rho = smem;                       // kBC * r
@@ -214,7 +215,9 @@ __global__ __launch_bounds__(kThreads) void k_lmhead(const WT* __restrict__ w_vo
       }
       __syncthreads();
     }
-    // combine over the slice, one sequence at a time
+    // combine over the slice, one sequence at a time; sampling folds l / T into the fused
+    // log-sum-exp and l / T + g into the top-2
+    const bool sample = smp.inv_temp != 0.f;
     for (int b = 0; b < nb; ++b) {
       const LT* lrow = long_j + (size_t)(b0 + b) * long_bstride;
       Partial P = partial_empty();
@@ -231,8 +234,14 @@ __global__ __launch_bounds__(kThreads) void k_lmhead(const WT* __restrict__ w_vo
           lse_fold<1>(P.S, &s, s);
         }
         lse_fold<1>(P.L, &a, a);
-        lse_fold<1>(P.F, &f, f);
-        top2_push(P, f, v);
+        if (sample) {
+          f *= smp.inv_temp;
+          lse_fold<1>(P.F, &f, f);
+          top2_push(P, f + gumbel_at(smp, b0 + b, j, v), v);
+        } else {
+          lse_fold<1>(P.F, &f, f);
+          top2_push(P, f, v);
+        }
       }
       P = block_merge(P, sh, kWaves);
       if (threadIdx.x == 0) partials[(size_t)(b0 + b) * gridDim.x + blockIdx.x] = P;
@@ -248,7 +257,7 @@ __global__ __launch_bounds__(kThreads) void k_select(const Partial* __restrict__
                                                      float al, int long_only, int j, int B,
                                                      int32_t* __restrict__ out_tokens,
                                                      dls_row_stats* __restrict__ out_stats,
-                                                     int32_t* __restrict__ tok_next) {
+                                                     int32_t* __restrict__ tok_next, Sampler smp) {
   __shared__ Partial sh[kWaves];
   const int b = blockIdx.x;
   Partial P = partial_empty();
@@ -256,7 +265,10 @@ __global__ __launch_bounds__(kThreads) void k_select(const Partial* __restrict__
   P = block_merge(P, sh, kWaves);
   if (threadIdx.x == 0) {
     int32_t t;
-    finalize_row(P, wl, al, long_only != 0, &t, out_stats ? out_stats + (size_t)b * B + j : nullptr, nullptr);
+    const bool sample = smp.inv_temp != 0.f;
+    const int ti = P.i1 == 0x7fffffff ? 0 : P.i1;
+    finalize_row(P, wl, al, long_only != 0, &t, out_stats ? out_stats + (size_t)b * B + j : nullptr, nullptr,
+                 sample ? gumbel_at(smp, b, j, ti) : 0.f, smp.temp);
     out_tokens[(size_t)b * B + j] = t;
     tok_next[b] = t;
   }
@@ -320,10 +332,10 @@ hipError_t launch_draft_t(const DraftArgs& a, hipStream_t st) {
     }
     k_lmhead<WT, LT, PRIOR><<<a.lay.groups, kThreads, lds, st>>>(
         w_vocab, V, r, rho, L + (size_t)j * V, bstride, a.prior, wl, al, be, a.lay.slice, long_only ? 1 : 0,
-        part, batch);
+        part, batch, a.smp, j);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     k_select<<<batch, kThreads, 0, st>>>(part, a.lay.groups, wl, al, long_only ? 1 : 0, j, B, a.out_tokens,
-                                         a.out_stats, tok);
+                                         a.out_stats, tok, a.smp);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     tok_in = tok;
   }

@@ -1,990 +1,14 @@
-// Persistent, weight-stationary DeLS-Spec block drafting (Algorithm 1 decoding loop with
-// the App. A RNN head) for bf16 heads prepared by dls_prepare_head.
-//
-// One workgroup per CU stays resident for the whole block.  Each workgroup owns a
-// contiguous range of 16-row vocabulary tiles of W_vocab: the first tiles live in the
-// AGPRs of its four waves (fed straight into v_mfma_f32_16x16x32_bf16 as the B operand),
-// the rest in LDS.  The first NG = H/16 workgroups ("GRU workgroups") also own 16 hidden
-// units each (their W_hh rows in LDS) and r/NG rows of W_rank.  Per draft position j:
-//
-//   GRU wgs  merge the argmax keys of position j-1 -> tokens u_j (all sequences)
-//            gi = T[u_j] (folded table) + gh (from the previous step) -> gates -> h_{j+1}
-//            of the owned units, published
-//            rho_i = SiLU(W_rank h_{j+1}) for the owned rank rows (MFMA), published; then
-//            gh = W_hh h_{j+1} for the next position from the same staged h (MFMA)
-//   all wgs  S = W_vocab rho on the owned tiles (MFMA), fused with the long logits
-//            (prefetched into LDS while waiting), online LSEs and top-2; one packed argmax
-//            key per (sequence, workgroup) published first, the LSE partials after it
-//
-// fp32 activations enter the bf16 matrix cores as two bf16 halves (hi + lo), split once
-// when they are staged into LDS.
-//
-// Cross-workgroup data moves through device-coherent 64-bit words that carry a tag
-// (epoch of the call, position); a consumer spins on the word itself until the tag
-// matches, so each hand-off costs one propagation, with no counters and no cache
-// flushes.  Every wait is bounded; on expiry an error word is set and all waves leave.
-#include <atomic>
-
-#include "dels_internal.hpp"
+// Host side of the persistent drafting kernel: the launch plan (tile ownership, LDS
+// budget), the workspace layout and the dispatch to the instantiations (one translation
+// unit per rank size and decoding mode, built in parallel).
+#include "draft_persistent.hpp"
 
 namespace dls {
 
-namespace {
-
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
-typedef __attribute__((ext_vector_type(4))) float f32x4_t;
-typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
-
-constexpr int kT = 256;          // threads per workgroup (one wave per SIMD)
-constexpr int kOps = 56;         // MFMA B operands of 16 bytes per lane held in AGPRs (224 of
-                                 // the 256; the rest take the accumulators)
-constexpr long kMaxSpins = 1L << 22;
-constexpr int kInflight = 8;     // hand-off loads a thread issues before checking any of them
-constexpr int kStageK = 256;     // K chunk of staged hand-off values (16 slots x 256 floats in LDS)
-constexpr int kStatWords = 9;    // tagged words of one published partial
-constexpr int kRhoCopies = 8;    // replicas of the published rank vector (spreads the readers)
-
-__device__ __forceinline__ uint64_t ld64(const uint64_t* p) {
-  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st64(uint64_t* p, uint64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint32_t ld32(const uint32_t* p) {
-  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st32(uint32_t* p, uint32_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void stf(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float ldf(const float* p) {
-  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// all earlier vector-memory operations of this wave have completed
-__device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-
-__device__ __forceinline__ uint64_t tagged(float v, uint32_t tag) {
-  return ((uint64_t)tag << 32) | __float_as_uint(v);
-}
-
-// wait until (word >> 32) == tag; false after the spin budget or when another wave failed
-__device__ __forceinline__ bool wait_tag(const uint64_t* p, uint32_t tag, uint32_t* err, uint64_t& v) {
-  v = ld64(p);
-  if ((uint32_t)(v >> 32) == tag) return true;
-  for (long s = 1;; ++s) {
-    __builtin_amdgcn_s_sleep(2);
-    v = ld64(p);
-    if ((uint32_t)(v >> 32) == tag) return true;
-    if ((s & 63) == 0 && ld32(err)) return false;
-    if (s > kMaxSpins) {
-      st32(err, 1u);
-      return false;
-    }
-  }
-}
-// keys carry an 8-bit position tag in their low byte
-__device__ __forceinline__ bool wait_key(const uint64_t* p, uint32_t tag8, uint32_t* err, uint64_t& v) {
-  v = ld64(p);
-  if ((uint32_t)(v & 0xffu) == tag8) return true;
-  for (long s = 1;; ++s) {
-    __builtin_amdgcn_s_sleep(2);
-    v = ld64(p);
-    if ((uint32_t)(v & 0xffu) == tag8) return true;
-    if ((s & 63) == 0 && ld32(err)) return false;
-    if (s > kMaxSpins) {
-      st32(err, 1u);
-      return false;
-    }
-  }
-}
-
-// argmax key: orderable fused value | (2^24 - 1 - index) | position tag
-__device__ __forceinline__ uint64_t make_key(float t1, int i1, uint32_t tag8) {
-  t1 += 0.0f;   // -0 -> +0, so that equal values compare equal
-  const uint32_t u = __float_as_uint(t1);
-  const uint32_t o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-  const uint32_t ix = (i1 == 0x7fffffff) ? 0u : (0xffffffu - (uint32_t)i1);
-  return ((uint64_t)o << 32) | ((uint64_t)ix << 8) | tag8;
-}
-__device__ __forceinline__ float key_value(uint64_t k) {
-  const uint32_t o = (uint32_t)(k >> 32);
-  return __uint_as_float((o & 0x80000000u) ? (o & 0x7fffffffu) : ~o);
-}
-__device__ __forceinline__ int key_index(uint64_t k, int V) {
-  const int i = (int)(0xffffffu - (uint32_t)((k >> 8) & 0xffffffu));
-  return i < V ? i : 0;   // no finite value anywhere: the first index
-}
-__device__ __forceinline__ uint64_t key_max(uint64_t a, uint64_t b) { return (a >> 8) >= (b >> 8) ? a : b; }
-
-// fp32 -> bf16 hi + bf16 lo (v = hi + lo to ~2^-17 relative)
-__device__ __forceinline__ uint32_t bf16_rne(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
-__device__ __forceinline__ void split_pair(float x0, float x1, uint32_t& hi, uint32_t& lo) {
-  const uint32_t h0 = bf16_rne(x0), h1 = bf16_rne(x1);
-  const uint32_t l0 = bf16_rne(x0 - __uint_as_float(h0 << 16));
-  const uint32_t l1 = bf16_rne(x1 - __uint_as_float(h1 << 16));
-  hi = h0 | (h1 << 16);
-  lo = l0 | (l1 << 16);
-}
-__device__ __forceinline__ void split8(const float* x, uint4& hi, uint4& lo) {
-  split_pair(x[0], x[1], hi.x, lo.x);
-  split_pair(x[2], x[3], hi.y, lo.y);
-  split_pair(x[4], x[5], hi.z, lo.z);
-  split_pair(x[6], x[7], hi.w, lo.w);
-}
-
-__device__ __forceinline__ bf16x8_t as_bf(uint4 v) {
-  union { uint4 u; bf16x8_t b; } c;
-  c.u = v;
-  return c.b;
-}
-__device__ __forceinline__ f32x4_t mfma_vv(uint4 a, uint4 b, f32x4_t c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(a), as_bf(b), c, 0, 0, 0);
-}
-// B operand resident in AGPRs (the matrix core reads it from there; the compiler keeps
-// track of the MFMA result hazards)
-__device__ __forceinline__ f32x4_t mfma_va(uint4 a, u32x4 b_agpr, f32x4_t c) {
-  union { u32x4 u; bf16x8_t b; } bb;
-  bb.u = b_agpr;
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(a), bb.b, c, 0, 0, 0);
-}
-__device__ __forceinline__ u32x4 to_agpr(uint4 v) {
-  u32x4 r = {v.x, v.y, v.z, v.w};
-  asm volatile("; weights -> agpr" : "=a"(r) : "0"(r));
-  return r;
-}
-
-__device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + __expf(-x)); }
-
-// Online log-sum-exp with one exponential per element: exp(-|x - m|) serves both the case of
-// a new maximum (rescale the sum) and of a smaller value (add it).  -inf adds nothing.
-__device__ __forceinline__ void lse_push(Lse& a, float x) {
-  const float d = x - a.m;
-  const float e = fast_exp2(-fabsf(d) * kLog2e);
-  const bool up = d > 0.f;
-  const float s_new = up ? __builtin_fmaf(a.s, e, 1.0f) : a.s + e;
-  a.s = (x == -INFINITY) ? a.s : s_new;
-  a.m = up ? x : a.m;
-}
-
-// value of the lane N places further along in the same row of 16 lanes (DPP row rotate)
-template <int N>
-__device__ __forceinline__ float row_ror(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x120 + N, 0xf, 0xf, false));
-}
-template <int N>
-__device__ __forceinline__ int row_ror_i(int v) {
-  return __builtin_amdgcn_update_dpp(0, v, 0x120 + N, 0xf, 0xf, false);
-}
-template <int N>
-__device__ __forceinline__ uint64_t row_ror_u64(uint64_t v) {
-  const uint32_t lo = (uint32_t)row_ror_i<N>((int)(uint32_t)v), hi = (uint32_t)row_ror_i<N>((int)(uint32_t)(v >> 32));
-  return ((uint64_t)hi << 32) | lo;
-}
-// largest key over the 16 lanes of a row (every lane of the row gets it)
-__device__ __forceinline__ uint64_t row_key_max(uint64_t k) {
-  k = key_max(k, row_ror_u64<8>(k));
-  k = key_max(k, row_ror_u64<4>(k));
-  k = key_max(k, row_ror_u64<2>(k));
-  k = key_max(k, row_ror_u64<1>(k));
-  return k;
-}
-// largest key over the wave (every lane gets it)
-__device__ __forceinline__ uint64_t wave_key_max(uint64_t k) {
-  k = row_key_max(k);
-  k = key_max(k, __shfl_xor(k, 16));
-  k = key_max(k, __shfl_xor(k, 32));
-  return k;
-}
-
-// lane permutations for allred_partial: DPP rotations within each row of 16 lanes, then
-// (FULL) xor shuffles across the four rows
-template <bool FULL>
-struct RowRor {
-  template <typename F>
-  __device__ __forceinline__ void each(F f) const {
-    f(8); f(4); f(2); f(1);
-    if (FULL) { f(16); f(32); }
-  }
-  __device__ __forceinline__ int i(int v, int m) const {
-    switch (m) {
-      case 8: return row_ror_i<8>(v);
-      case 4: return row_ror_i<4>(v);
-      case 2: return row_ror_i<2>(v);
-      case 1: return row_ror_i<1>(v);
-      default: return __shfl_xor(v, m);
-    }
-  }
-  __device__ __forceinline__ float operator()(float v, int m) const { return __int_as_float(i(__float_as_int(v), m)); }
-};
-
-}  // namespace
-
-// ------------------------------------------------------------------------------------------
-// tile ownership (shared with the host)
-// ------------------------------------------------------------------------------------------
-__host__ __device__ void persist_tile_range(int w, int G, int NG, int NT, int cap_a, int* t0, int* n) {
-  if (NT <= G * cap_a) {
-    const int q = NT / G, rm = NT % G;
-    *t0 = w * q + (w < rm ? w : rm);
-    *n = q + (w < rm ? 1 : 0);
-    return;
-  }
-  const int ga = NG * cap_a;
-  if (w < NG) {
-    *t0 = w * cap_a;
-    *n = cap_a;
-    return;
-  }
-  const int rest = NT - ga, m = G - NG, i = w - NG;
-  const int q = rest / m, rm = rest % m;
-  *t0 = ga + i * q + (i < rm ? i : rm);
-  *n = q + (i < rm ? 1 : 0);
-}
-
-namespace {
-
-// Copy n 16-byte words from global memory into LDS, 8 loads in flight per thread (indices past
-// the end re-read the last word, so that every load is unconditional).
-__device__ __forceinline__ void copy_to_lds(uint4* dst, const uint4* src, int n) {
-  for (int base = 0; base < n; base += kT * 8) {
-    uint4 v[8];
-#pragma unroll
-    for (int m = 0; m < 8; ++m) {
-      const int i = base + m * kT + (int)threadIdx.x;
-      v[m] = src[i < n ? i : n - 1];
-    }
-#pragma unroll
-    for (int m = 0; m < 8; ++m) {
-      const int i = base + m * kT + (int)threadIdx.x;
-      if (i < n) dst[i] = v[m];
-    }
-  }
-}
-
-// Wave 0 spins until the first word of each producer p < np (at src0 + p * pstride) carries
-// the tag, one lane per producer, while the other waves wait at the barrier: the data itself
-// is then read once.  Keeps the polling traffic on a hand-off to one load per producer.
-__device__ __forceinline__ void wait_producers(const uint64_t* src0, size_t pstride, int np, uint32_t tag,
-                                               uint32_t* err) {
-  if (threadIdx.x < 64) {
-    const int l = (int)threadIdx.x;
-    bool done = l >= np;
-    for (long s = 0;; ++s) {
-      if (!done) done = (uint32_t)(ld64(src0 + (size_t)l * pstride) >> 32) == tag;
-      if (__all(done)) break;
-      __builtin_amdgcn_s_sleep(4);
-      if ((s & 63) == 63 && ld32(err)) break;
-      if (s > kMaxSpins) {
-        st32(err, 1u);
-        break;
-      }
-    }
-  }
-  __syncthreads();
-}
-
-// Operand planes: staged hand-off values as bf16 hi and lo halves, 16 slots x (K + 8) each
-// (the 8-element pad spreads the slots' rows over the LDS banks).
-constexpr int kPlane = 16 * (kStageK + 8);
-
-// one staged value: its bf16 hi and lo halves (hi + lo = x to about 2^-17 relative)
-__device__ __forceinline__ void put_split(uint16_t* hi, uint16_t* lo, int idx, uint32_t bits) {
-  const float x = __uint_as_float(bits);
-  const uint32_t h = bf16_rne(x);
-  hi[idx] = (uint16_t)h;
-  lo[idx] = (uint16_t)bf16_rne(x - __uint_as_float(h << 16));
-}
-
-// Stage rows x width tagged words (row stride `stride` words) into the operand planes at
-// [row * pitch + c].  Every thread issues kInflight loads back to back before checking any tag
-// (one round trip per stage); words that were not ready yet are re-polled one by one.
-__device__ __forceinline__ bool stage_split(const uint64_t* src, int rows, int width, size_t stride, uint32_t tag,
-                                            uint16_t* hi, uint16_t* lo, int pitch, uint32_t* err) {
-  const int q = kT / width, rm = kT % width;
-  int row = (int)threadIdx.x / width, col = (int)threadIdx.x % width;
-  bool ok = true;
-  for (int base = 0; base < rows * width; base += kT * kInflight) {
-    uint64_t v[kInflight];
-    int rr[kInflight], cc[kInflight];
-#pragma unroll
-    for (int m = 0; m < kInflight; ++m) {
-      rr[m] = row;
-      cc[m] = col;
-      v[m] = row < rows ? ld64(src + (size_t)row * stride + col) : 0ull;
-      col += rm;
-      row += q;
-      if (col >= width) {
-        col -= width;
-        ++row;
-      }
-    }
-    uint32_t bad = 0;
-#pragma unroll
-    for (int m = 0; m < kInflight; ++m) {
-      if (rr[m] < rows) {
-        if ((uint32_t)(v[m] >> 32) == tag) put_split(hi, lo, rr[m] * pitch + cc[m], (uint32_t)v[m]);
-        else bad |= 1u << m;
-      }
-    }
-#pragma unroll 1
-    for (int m = 0; bad; ++m, bad >>= 1) {
-      if (bad & 1u) {
-        const int e = base + m * kT + (int)threadIdx.x;
-        const int r0 = e / width, c0 = e % width;
-        uint64_t x;
-        ok &= wait_tag(src + (size_t)r0 * stride + c0, tag, err, x);
-        put_split(hi, lo, r0 * pitch + c0, (uint32_t)x);
-      }
-    }
-  }
-  return ok;
-}
-
-// Workgroup barrier that also tells whether any thread failed.  A failure is final (all waves
-// leave), so the LDS flag is set once and never cleared.
-__device__ __forceinline__ bool fail_barrier(bool failed, volatile int* s_fail) {
-  if (failed) *s_fail = 1;
-  __syncthreads();
-  return *s_fail != 0;
-}
-
-// A operand (16 slots x 32 k) at column k of the planes: lane (slot n16, group g4) takes
-// k + 8 g4 .. +7 of its slot.  Lanes of slots >= nb read slot 0 instead: an MFMA output row
-// depends on its own A row only, and the rows of empty slots are never used.
-__device__ __forceinline__ void plane_operand(const uint16_t* hi, const uint16_t* lo, int pitch, int nb, int n16,
-                                              int g4, int k, uint4& ahi, uint4& alo) {
-  const int o = (n16 < nb ? n16 : 0) * pitch + k + 8 * g4;
-  ahi = *(const uint4*)(hi + o);
-  alo = *(const uint4*)(lo + o);
-}
-
-// NARROW: at most 4 sequences (one M tile whose useful rows all sit in lanes 0..15)
-// MARKOV: the Markov head of App. A, rho_j = E_M[u_j]: no GRU workgroups and no hand-off
-//         but the argmax keys; every workgroup merges the keys and reads the E_M row itself
-template <int KK, typename LT, bool PRIOR, bool NARROW, bool MARKOV>
-__global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
-  extern __shared__ __attribute__((aligned(16))) char smem[];
-  constexpr int TPW = kOps / KK;   // AGPR tiles per wave
-  const int w = blockIdx.x, G = gridDim.x, tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6, n16 = lane & 15, g4 = lane >> 4;
-  const int V = a.V, H = a.H, r = a.r, batch = a.batch, Bk = a.B, rpg = a.rpg;
-  const bool gru = w < a.NG;
-  const int KKH = H / 32;
-  uint32_t* err = a.hdr + 1;
-  if (ld32(err)) return;
-  const uint32_t epoch_full = ld32(a.hdr);
-  const uint32_t epoch = epoch_full & 0xffffffu;
-  const int set = (int)(epoch & 1u);
-  const size_t kstride = (size_t)kMaxBatch * G;       // one (set, parity) plane of keys
-
-  int t0, nt;
-  persist_tile_range(w, G, a.NG, a.NT, a.cap_a, &t0, &nt);
-  const int na = nt < a.cap_a ? nt : a.cap_a;
-  const int nl = nt - na;
-  const int v_base = 16 * t0;
-  const int nrows = 16 * nt;
-  const int mtiles = (batch + 15) / 16;
-  const int ll_slots = batch < 16 ? batch : 16;
-
-  // ---- LDS carve-up (offsets identical to the host's size computation)
-  char* p = smem;
-  uint4* s_wtiles = (uint4*)p;                      // nl tiles x KK x 64 (non-GRU wgs)
-  uint4* s_whh = (uint4*)p;                         // 3 x KKH x 64 (GRU wgs)
-  bf16_t* s_wrank = (bf16_t*)(p + (size_t)3 * KKH * 1024);   // rpg x H (GRU wgs)
-  p += a.lds_region_a;
-  LT* s_ll = (LT*)p;                                // ll_slots x rows_max long logits
-  p += ((size_t)ll_slots * a.rows_max * sizeof(LT) + 15) & ~(size_t)15;
-  float* s_prior = (float*)p;                       // rows_max
-  p += (size_t)a.rows_max * 4 * (PRIOR ? 1 : 0);
-  // operand planes; at other times the gh partials (12 x 64 x f32x4) and the gathered gi (16 x 48)
-  uint16_t* s_hi = (uint16_t*)p;
-  uint16_t* s_lo = s_hi + kPlane;
-  f32x4_t* s_red = (f32x4_t*)p;
-  float* s_gi = (float*)p;
-  p += (size_t)2 * kPlane * 2;
-  f32x4_t* s_rred = (f32x4_t*)p;                    // rank partials [wave][g4][rpg]
-  p += (size_t)16 * rpg * 16;
-  float* s_gh = (float*)p;                          // per M tile: 16 slots x 48 (W_hh h for the next step)
-  p += (size_t)mtiles * 16 * 48 * 4;
-  Partial* s_part = (Partial*)p;                    // 4 waves x 16 slots
-  p += (size_t)4 * 16 * sizeof(Partial);
-  uint64_t* s_wkey = (uint64_t*)p;                  // 4 waves x 16 slots; the merge's per-sequence maxima
-  uint64_t* s_best = s_wkey;
-  p += (size_t)kMaxBatch * 8;
-  int* s_tok = (int*)p;                             // kMaxBatch
-  p += (size_t)kMaxBatch * 4;
-  volatile int* s_fail = (volatile int*)p;          // sticky failure flag
-  if (tid == 0) *s_fail = 0;
-
-  // ---- clear this workgroup's key slots of the other set (read by the next call)
-  for (int i = tid; i < 2 * kMaxBatch; i += kT) {
-    const int par = i / kMaxBatch, b = i % kMaxBatch;
-    st64(a.keys + (size_t)(1 - set) * 2 * kstride + par * kstride + (size_t)b * G + w, 0ull);
-  }
-
-  // ---- resident weights
-  u32x4 wr[TPW * KK];
-#pragma unroll
-  for (int q = 0; q < TPW; ++q) {
-    const int lt = wave * TPW + q;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (lt < na) v = a.wv[((size_t)(t0 + lt) * KK + kk) * 64 + lane];
-      wr[q * KK + kk] = to_agpr(v);
-    }
-  }
-  if (gru) {
-    copy_to_lds(s_whh, a.whh + (size_t)w * 3 * KKH * 64, 3 * KKH * 64);
-    for (int i = tid; i < rpg * H / 8; i += kT) {
-      const int row = i / (H / 8), c = i % (H / 8);
-      *(uint4*)(s_wrank + (size_t)row * H + 8 * c) = *(const uint4*)(a.w_rank + (size_t)(w * rpg + row) * H + 8 * c);
-    }
-  } else {
-    copy_to_lds(s_wtiles, a.wv + ((size_t)(t0 + na) * KK) * 64, nl * KK * 64);
-  }
-  if (PRIOR)
-    for (int i = tid; i < nrows; i += kT) s_prior[i] = v_base + i < V ? a.prior[v_base + i] : 0.f;
-  __syncthreads();
-
-  const LT* L = (const LT*)a.L;
-  const float wl = a.wl;
-
-  // Tokens of position jm (the argmax keys of all workgroups, max-reduced through LDS atomics)
-  // into s_tok; workgroup 0 also writes the drafted tokens.  Workgroup-uniform result.
-  auto merge_position = [&](int jm) -> bool {
-    const uint32_t tag8 = (uint32_t)(jm + 1);
-    const uint64_t* kp = a.keys + (size_t)set * 2 * kstride + (size_t)(jm & 1) * kstride;
-    for (int b = tid; b < batch; b += kT) s_best[b] = 0ull;
-    __syncthreads();
-    bool ok = true;
-    if (tid < G) {
-      for (int b0 = 0; b0 < batch; b0 += kInflight) {
-        uint64_t v[kInflight];
-#pragma unroll
-        for (int m = 0; m < kInflight; ++m)
-          v[m] = b0 + m < batch ? ld64(kp + (size_t)(b0 + m) * G + tid) : 0ull;
-        uint32_t bad = 0;
-#pragma unroll
-        for (int m = 0; m < kInflight; ++m) {
-          if (b0 + m < batch) {
-            if ((uint32_t)(v[m] & 0xffu) == tag8) atomicMax((unsigned long long*)&s_best[b0 + m], v[m]);
-            else bad |= 1u << m;
-          }
-        }
-#pragma unroll 1
-        for (int m = 0; bad; ++m, bad >>= 1) {
-          if (bad & 1u) {
-            uint64_t k;
-            ok &= wait_key(kp + (size_t)(b0 + m) * G + tid, tag8, err, k);
-            atomicMax((unsigned long long*)&s_best[b0 + m], k);
-          }
-        }
-      }
-    }
-    if (fail_barrier(!ok, s_fail)) return false;
-    if (tid < batch) {
-      const int tok = key_index(s_best[tid], V);
-      s_tok[tid] = tok;
-      if (w == 0) a.out_tokens[(size_t)tid * Bk + jm] = tok;
-    }
-    __syncthreads();
-    return true;
-  };
-
-  // Publish the row-statistics partial of this workgroup for position jp (slots of M tile mtp,
-  // per-wave partials in s_part): merged over the waves, then nine tagged words per slot,
-  // written by the lanes of wave `by` (a wave's loads wait for its earlier stores, so the
-  // stores go to a wave that loads nothing critical soon after).
-  auto publish_stats = [&](int jp, int mtp, int nbp, int by) {
-    const int sl = tid - 64 * by;
-    if (sl >= 0 && sl < nbp) {
-      Partial T = s_part[sl];
-      for (int q = 1; q < 4; ++q) T = partial_merge(T, s_part[q * 16 + sl]);
-      const uint32_t stag = (epoch << 8) | (uint32_t)(jp + 1);
-      uint64_t* sp = a.stats + (((size_t)jp * batch + mtp * 16 + sl) * G + w) * kStatWords;
-      st64(sp + 0, tagged(T.L.m, stag)); st64(sp + 1, tagged(T.L.s, stag));
-      st64(sp + 2, tagged(T.S.m, stag)); st64(sp + 3, tagged(T.S.s, stag));
-      st64(sp + 4, tagged(T.F.m, stag)); st64(sp + 5, tagged(T.F.s, stag));
-      st64(sp + 6, tagged(T.t1, stag)); st64(sp + 7, tagged(T.t2, stag));
-      st64(sp + 8, tagged(__int_as_float(T.i1), stag));
-    }
-  };
-  // GRU workgroups with a single M tile hand their statistics of position j over during
-  // position j + 1: right after the argmax key they are on the critical path to the next
-  // merge.  -1: nothing pending.
-  int pending_stats = -1;
-
-  for (int j = 0; j < Bk; ++j) {
-    const uint32_t tag = (epoch << 8) | (uint32_t)(j + 1);
-    const uint32_t tag8 = (uint32_t)(j + 1);
-    const int par = j & 1;
-    const float al = a.al_j[j], be = a.be_j[j];   // this position's fusion weights
-    const bool long_only = a.literal && j == 0;
-    const int hs = a.literal ? j - 1 : j;          // head step index (the first one starts from h = 0)
-
-    // ======================= GRU and rank (GRU workgroups) =======================
-    if (gru && !long_only) {
-      const uint32_t tag_prev = (epoch << 8) | (uint32_t)j;   // h published at position j-1
-      const uint64_t* hprev = a.hbuf + (size_t)((j - 1) & 1) * batch * H;
-      uint64_t* hnew = a.hbuf + (size_t)par * batch * H;
-      if (j > 0) {
-        if (!merge_position(j - 1)) return;
-      } else {
-        for (int b = tid; b < batch; b += kT) {
-          const int u = a.last[b];
-          s_tok[b] = (unsigned)u < (unsigned)V ? u : 0;   // out-of-range input reads as 0
-        }
-        __syncthreads();
-      }
-      // gates of the owned units: gi = T[u] (folded input projection), gh from the previous step
-      for (int mt = 0; mt < mtiles; ++mt) {
-        const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
-        uint64_t hv[4];   // the owned units' previous state, in flight together with the gather
-        if (wave == 0) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            hv[i] = (hs > 0 && 4 * g4 + i < nb) ? ld64(hprev + (size_t)(mt * 16 + 4 * g4 + i) * H + 16 * w + n16)
-                                                 : 0ull;
-        }
-        for (int i = tid; i < 16 * 48; i += kT) {
-          const int slot = i / 48, q = (i % 48) / 16, u = i % 16;
-          s_gi[i] = slot < nb ? a.T[(size_t)s_tok[mt * 16 + slot] * 3 * H + q * H + 16 * w + u] : 0.f;
-        }
-        __syncthreads();
-        bool ok = true;
-        if (wave == 0) {
-          const float* gh = s_gh + mt * 16 * 48;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int slot = 4 * g4 + i, bb = mt * 16 + slot;
-            if (slot < nb) {
-              float hp = 0.f, ghr = 0.f, ghz = 0.f, ghn = 0.f;
-              if (hs > 0) {
-                if ((uint32_t)(hv[i] >> 32) != tag_prev)
-                  ok &= wait_tag(hprev + (size_t)bb * H + 16 * w + n16, tag_prev, err, hv[i]);
-                hp = __uint_as_float((uint32_t)hv[i]);
-                ghr = gh[slot * 48 + n16];
-                ghz = gh[slot * 48 + 16 + n16];
-                ghn = gh[slot * 48 + 32 + n16];
-              }
-              const float* gi = s_gi + slot * 48;
-              const float rg = sigm(gi[n16] + ghr);
-              const float zg = sigm(gi[16 + n16] + ghz);
-              const float ng = tanhf_(gi[32 + n16] + rg * ghn);
-              st64(hnew + (size_t)bb * H + 16 * w + n16, tagged((1.f - zg) * ng + zg * hp, tag));
-            }
-          }
-        }
-        if (fail_barrier(!ok, s_fail)) return;
-      }
-      // rho_i = SiLU(W_rank h_{j+1}) for the owned rank rows (MFMA over the staged h, K split
-      // over the waves), then W_hh h_{j+1} for the next position from the same staged h
-      for (int mt = 0; mt < mtiles; ++mt) {
-        const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
-        const int HC = nb * (H + 8) <= kPlane ? H : kStageK;
-        const int pitch = HC + 8;
-        const uint64_t* hsrc = hnew + (size_t)mt * 16 * H;
-        wait_producers(hsrc, 16, a.NG, tag, err);
-        bool ok = true;
-        f32x4_t racc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        for (int k0 = 0; k0 < H; k0 += HC) {
-          if (k0) __syncthreads();
-          ok &= stage_split(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
-          __syncthreads();
-          if (pending_stats >= 0) {   // s_part still holds it: nothing has used the space since
-            publish_stats(pending_stats, 0, batch, 3);
-            pending_stats = -1;
-          }
-          for (int kk = wave; kk < HC / 32; kk += 4) {
-            uint4 ahi, alo;
-            plane_operand(s_hi, s_lo, pitch, nb, n16, g4, 32 * kk, ahi, alo);
-            const uint4 bw = n16 < rpg ? *(const uint4*)(s_wrank + (size_t)n16 * H + k0 + 32 * kk + 8 * g4)
-                                       : make_uint4(0, 0, 0, 0);
-            racc = mfma_vv(ahi, bw, racc);
-            racc = mfma_vv(alo, bw, racc);
-          }
-        }
-        if (n16 < rpg) s_rred[(wave * 4 + g4) * rpg + n16] = racc;
-        if (fail_barrier(!ok, s_fail)) return;
-        if (wave == 0 && n16 < rpg) {
-          f32x4_t sm = s_rred[g4 * rpg + n16];
-          for (int q = 1; q < 4; ++q) sm += s_rred[(q * 4 + g4) * rpg + n16];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int slot = 4 * g4 + i;
-            if (slot < nb) {
-              const uint64_t word = tagged(siluf_(sm[i]), tag);
-              for (int c = 0; c < kRhoCopies; ++c)
-                st64(a.rbuf + ((size_t)c * 2 + par) * batch * r + (size_t)(mt * 16 + slot) * r + w * rpg + n16, word);
-            }
-          }
-        }
-        if (j + 1 < Bk) {
-          f32x4_t gacc[3];
-          for (int q = 0; q < 3; ++q) gacc[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-          for (int k0 = 0; k0 < H; k0 += HC) {
-            if (HC < H) {   // several chunks: stage each again (all of h is there by now)
-              __syncthreads();
-              ok &= stage_split(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
-              __syncthreads();
-            }
-            for (int kk = wave; kk < HC / 32; kk += 4) {
-              uint4 ahi, alo;
-              plane_operand(s_hi, s_lo, pitch, nb, n16, g4, 32 * kk, ahi, alo);
-#pragma unroll
-              for (int q = 0; q < 3; ++q) {
-                const uint4 bh = s_whh[(q * KKH + k0 / 32 + kk) * 64 + lane];
-                gacc[q] = mfma_vv(ahi, bh, gacc[q]);
-                gacc[q] = mfma_vv(alo, bh, gacc[q]);
-              }
-            }
-          }
-          __syncthreads();   // planes read: their space takes the partial sums
-          for (int q = 0; q < 3; ++q) s_red[(wave * 3 + q) * 64 + lane] = gacc[q];
-          __syncthreads();
-          if (wave == 0) {
-            float* gh = s_gh + mt * 16 * 48;
-            for (int q = 0; q < 3; ++q) {
-              f32x4_t sm = s_red[q * 64 + lane];
-              for (int k = 1; k < 4; ++k) sm += s_red[(k * 3 + q) * 64 + lane];
-#pragma unroll
-              for (int i = 0; i < 4; ++i) gh[(4 * g4 + i) * 48 + q * 16 + n16] = sm[i];
-            }
-          }
-        }
-        if (fail_barrier(!ok, s_fail)) return;
-      }
-    }
-
-    // ======================= Markov head: the previous token (all workgroups) =======================
-    if (MARKOV && !long_only) {
-      if (j > 0) {
-        if (!merge_position(j - 1)) return;
-      } else {
-        for (int b = tid; b < batch; b += kT) {
-          const int u = a.last[b];
-          s_tok[b] = (unsigned)u < (unsigned)V ? u : 0;   // out-of-range input reads as 0
-        }
-        __syncthreads();
-      }
-    }
-
-    // ======================= vocabulary head + fused combine (all workgroups) =======================
-    for (int mt = 0; mt < mtiles; ++mt) {
-      const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
-      // long logits of the owned rows (independent of rho: in flight while rho is awaited)
-      for (int slot = 0; slot < nb; ++slot) {
-        const LT* src = L + ((size_t)(mt * 16 + slot) * Bk + j) * V + v_base;
-        LT* dst = s_ll + (size_t)slot * a.rows_max;
-        for (int r0 = 0; r0 < nrows; r0 += 4 * kT) {
-          LT x[4];
-#pragma unroll
-          for (int m = 0; m < 4; ++m) {
-            const int row = r0 + m * kT + tid;
-            x[m] = (row < nrows && v_base + row < V) ? src[row] : LT(0);
-          }
-#pragma unroll
-          for (int m = 0; m < 4; ++m) {
-            const int row = r0 + m * kT + tid;
-            if (row < nrows) dst[row] = x[m];
-          }
-        }
-      }
-      // rho of the slots, staged as bf16 hi + lo planes, then held as the A operands
-      uint4 ahi[KK], alo[KK];
-      if (MARKOV && !long_only) {
-        // rho = E_M[u]: bf16 values, exact in the hi plane (the lo half would be zero)
-        for (int i = tid; i < nb * (r / 8); i += kT) {
-          const int slot = i / (r / 8), c = i % (r / 8);
-          *(uint4*)(s_hi + slot * (r + 8) + 8 * c) =
-              *(const uint4*)(a.e_m + (size_t)s_tok[mt * 16 + slot] * r + 8 * c);
-        }
-        __syncthreads();
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          ahi[kk] = *(const uint4*)(s_hi + (n16 < nb ? n16 : 0) * (r + 8) + 32 * kk + 8 * g4);
-          alo[kk] = make_uint4(0, 0, 0, 0);
-        }
-      } else if (!long_only) {
-        const uint64_t* rsrc = a.rbuf + ((size_t)(w % kRhoCopies) * 2 + par) * batch * r + (size_t)mt * 16 * r;
-        wait_producers(rsrc, (size_t)rpg, a.NG, tag, err);
-        const bool ok = stage_split(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err);
-        if (fail_barrier(!ok, s_fail)) return;
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) plane_operand(s_hi, s_lo, r + 8, nb, n16, g4, 32 * kk, ahi[kk], alo[kk]);
-      } else {
-        __syncthreads();   // s_ll complete
-      }
-      // With at most 4 sequences every useful MFMA output sits in lanes 0..15 (rows = slots).
-      // Such "narrow" tiles are stashed in LDS (the planes, free once the A operands are in
-      // registers) and folded four tiles at a time, one tile per 16-lane group.
-      constexpr bool narrow = NARROW;
-      float* s_stash = (float*)s_hi + wave * 256;   // [4 tiles][4 slots][16 rows]
-      if (narrow) __syncthreads();
-
-      Partial P[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) P[i] = partial_empty();
-
-      // narrow: keep the useful rows (slots < nb) of a tile's result at stash position tq
-      auto stash = [&](const f32x4_t& acc, int tq) {
-        if (g4 == 0) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (i < nb) s_stash[(tq * 4 + i) * 16 + n16] = acc[i];
-        }
-      };
-      // narrow: fold stashed tiles base + stride * tq (tq < ntile), lane group tq taking tile tq
-      auto fold_narrow = [&](int base, int stride, int ntile) {
-        if (g4 < ntile) {
-          const int row = 16 * (base + stride * g4) + n16;
-          const int v = v_base + row;
-          if (v < V) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              if (i < nb) {
-                const float x = to_f32(s_ll[i * a.rows_max + row]);
-                float f;
-                if (long_only) {
-                  f = wl * x;
-                } else {
-                  const float sv = s_stash[(g4 * 4 + i) * 16 + n16];
-                  f = __builtin_fmaf(al, sv, wl * x);
-                  if (PRIOR) f = __builtin_fmaf(-be, s_prior[row], f);
-                  lse_push(P[i].S, sv);
-                }
-                lse_push(P[i].L, x);
-                lse_push(P[i].F, f);
-                top2_push(P[i], f, v);
-              }
-            }
-          }
-        }
-      };
-
-      auto fold_tile = [&](const f32x4_t& acc, int lt) {
-        const int row = 16 * lt + n16;
-        const int v = v_base + row;
-        const bool vin = v < V;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int slot = 4 * g4 + i;
-          if (i < nb) {   // uniform: skips slot sets no lane holds
-            if (slot < nb && vin) {
-              const float x = to_f32(s_ll[slot * a.rows_max + row]);
-              float f;
-              if (long_only) {
-                f = wl * x;
-              } else {
-                const float s = acc[i];
-                f = __builtin_fmaf(al, s, wl * x);
-                if (PRIOR) f = __builtin_fmaf(-be, s_prior[row], f);
-                lse_push(P[i].S, s);
-              }
-              lse_push(P[i].L, x);
-              lse_push(P[i].F, f);
-              top2_push(P[i], f, v);
-            }
-          }
-        }
-      };
-
-      // AGPR-resident tiles of this wave, two at a time: four independent MFMA chains
-      // (hi and lo halves of rho for each tile) keep the matrix pipe busy
-#pragma unroll
-      for (int q = 0; q < TPW; q += 2) {
-        const int lt = wave * TPW + q;
-        const bool two = q + 1 < TPW;   // constant once unrolled (TPW may be odd)
-        const int q2 = two ? q + 1 : q;
-        if (lt < na) {
-          f32x4_t c0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, c1 = c0, c2 = c0, c3 = c0;
-          if (!long_only) {
-#pragma unroll
-            for (int kk = 0; kk < KK; ++kk) {
-              c0 = mfma_va(ahi[kk], wr[q * KK + kk], c0);
-              if (!MARKOV) c1 = mfma_va(alo[kk], wr[q * KK + kk], c1);
-              if (two) {
-                c2 = mfma_va(ahi[kk], wr[q2 * KK + kk], c2);
-                if (!MARKOV) c3 = mfma_va(alo[kk], wr[q2 * KK + kk], c3);
-              }
-            }
-          }
-          if (narrow) {
-            stash(c0 + c1, q % 4);
-            if (two) stash(c2 + c3, q % 4 + 1);
-          } else {
-            fold_tile(c0 + c1, lt);
-            if (two && lt + 1 < na) fold_tile(c2 + c3, lt + 1);
-          }
-        }
-        if (narrow && (q % 4 == 2 || q + 2 >= TPW)) {   // a group of four tiles (or the last) is stashed
-          const int g0 = q - q % 4;
-          const int cnt = (TPW - g0 < 4 ? TPW - g0 : 4);
-          const int avail = na - (wave * TPW + g0);
-          fold_narrow(wave * TPW + g0, 1, avail < cnt ? (avail > 0 ? avail : 0) : cnt);
-        }
-      }
-      // LDS-resident tiles, round robin over the waves (narrow: four at a time)
-      auto lds_tile = [&](int lq) -> f32x4_t {
-        f32x4_t c0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, c1 = c0;
-        if (!long_only) {
-#pragma unroll
-          for (int kk = 0; kk < KK; ++kk) {
-            const uint4 bw = s_wtiles[((size_t)lq * KK + kk) * 64 + lane];
-            c0 = mfma_vv(ahi[kk], bw, c0);
-            if (!MARKOV) c1 = mfma_vv(alo[kk], bw, c1);
-          }
-        }
-        return c0 + c1;
-      };
-      if (narrow) {
-        for (int m0 = 0; wave + 4 * m0 < nl; m0 += 4) {
-          int cnt = 0;
-          for (int tq = 0; tq < 4; ++tq) {
-            const int lq = wave + 4 * (m0 + tq);
-            if (lq < nl) {
-              stash(lds_tile(lq), tq);
-              ++cnt;
-            }
-          }
-          fold_narrow(na + wave + 4 * m0, 4, cnt);
-        }
-      } else {
-        for (int lq = wave; lq < nl; lq += 4) fold_tile(lds_tile(lq), na + lq);
-      }
-      // argmax key of each slot: max over the 16 lanes of a row (DPP), then over the waves
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (i < nb) {
-          if (narrow) {   // slot i spread over the whole wave
-            const uint64_t k = wave_key_max(make_key(P[i].t1, P[i].i1, tag8));
-            if (lane == 0) s_wkey[wave * 16 + i] = k;
-          } else {
-            const uint64_t k = row_key_max(make_key(P[i].t1, P[i].i1, tag8));
-            if (n16 == 0) s_wkey[wave * 16 + 4 * g4 + i] = k;
-          }
-        }
-      }
-      __syncthreads();
-      if (tid < nb) {
-        uint64_t k = s_wkey[tid];
-        for (int q = 1; q < 4; ++q) k = key_max(k, s_wkey[q * 16 + tid]);
-        st64(a.keys + (size_t)set * 2 * kstride + par * kstride + (size_t)(mt * 16 + tid) * G + w, k);
-      }
-      // the full partials (LSEs, top-2) for the row statistics: off the critical path
-      if (a.out_stats) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (i < nb) {
-            P[i] = allred_partial(P[i], RowRor<NARROW>{});   // over the row (narrow: the wave)
-            if (narrow) {
-              if (lane == 0) s_part[wave * 16 + i] = P[i];
-            } else if (n16 == 0) {
-              s_part[wave * 16 + 4 * g4 + i] = P[i];
-            }
-          }
-        }
-        if (gru && mtiles == 1 && j + 1 < Bk) {
-          pending_stats = j;
-        } else {
-          __syncthreads();
-          publish_stats(j, mt, nb, 0);
-        }
-      }
-      __syncthreads();
-    }
-  }
-
-  // ---- the last position's tokens (workgroup 0)
-  if (w == 0) {
-    if (!merge_position(Bk - 1)) return;
-  }
-  // ---- row statistics: row (b, j) is merged by workgroup (b * B + j) % G from the tagged partials
-  if (a.out_stats) {
-    for (int q = w; q < batch * Bk; q += G) {
-      const int b = q / Bk, jm = q % Bk;
-      const uint32_t stag = (epoch << 8) | (uint32_t)(jm + 1);
-      Partial P = partial_empty();
-      bool ok = true;
-      if (tid < G) {
-        const uint64_t* sp = a.stats + (((size_t)jm * batch + b) * G + tid) * kStatWords;
-        uint64_t w9[kStatWords];
-#pragma unroll
-        for (int e = 0; e < kStatWords; ++e) w9[e] = ld64(sp + e);
-        float q9[kStatWords];
-#pragma unroll
-        for (int e = 0; e < kStatWords; ++e) {
-          if ((uint32_t)(w9[e] >> 32) != stag) ok &= wait_tag(sp + e, stag, err, w9[e]);
-          q9[e] = __uint_as_float((uint32_t)w9[e]);
-        }
-        P.L.m = q9[0]; P.L.s = q9[1];
-        P.S.m = q9[2]; P.S.s = q9[3];
-        P.F.m = q9[4]; P.F.s = q9[5];
-        P.t1 = q9[6]; P.t2 = q9[7];
-        P.i1 = __float_as_int(q9[8]);
-      }
-      if (fail_barrier(!ok, s_fail)) return;
-      P = block_merge(P, s_part, 4);
-      if (tid == 0) {
-        int dummy;
-        finalize_row(P, wl, a.al_j[jm], a.literal && jm == 0, &dummy, a.out_stats + (size_t)b * Bk + jm, nullptr);
-      }
-      __syncthreads();
-    }
-  }
-  if (w == 0 && tid == 0) {
-    vm_wait();
-    st32(a.hdr, epoch_full + 1u);
-  }
-}
-
-template <int KK, typename LT, bool PRIOR, bool NARROW, bool MARKOV>
-hipError_t launch_k(const PersistArgs& pa, int G, size_t lds, hipStream_t st) {
-  auto kern = k_draft_persistent<KK, LT, PRIOR, NARROW, MARKOV>;
-  // the dynamic LDS limit is raised to the maximum once per device (a per-call attribute
-  // change costs microseconds of host time)
-  static std::atomic<uint64_t> raised{0};
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  const uint64_t bit = dev < 64 ? (uint64_t)1 << dev : 0;
-  if (!bit || !(raised.load(std::memory_order_acquire) & bit)) {
-    e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
-    if (e != hipSuccess) return e;
-    raised.fetch_or(bit, std::memory_order_acq_rel);
-  }
-  (void)lds;
-  PersistArgs copy = pa;
-  void* args[] = {&copy};
-  return hipLaunchCooperativeKernel((const void*)kern, dim3(G), dim3(kT), args, (unsigned)lds, st);
-}
-
-template <typename LT, bool PRIOR, bool MARKOV>
-hipError_t launch_kk(const PersistArgs& pa, int G, size_t lds, hipStream_t st) {
-  const bool narrow = pa.batch <= 4;
-  switch (pa.r / 32) {
-    case 4:
-      return narrow ? launch_k<4, LT, PRIOR, true, MARKOV>(pa, G, lds, st)
-                    : launch_k<4, LT, PRIOR, false, MARKOV>(pa, G, lds, st);
-    case 8:
-      return narrow ? launch_k<8, LT, PRIOR, true, MARKOV>(pa, G, lds, st)
-                    : launch_k<8, LT, PRIOR, false, MARKOV>(pa, G, lds, st);
-  }
-  return hipErrorInvalidValue;
-}
-
-template <typename LT, bool PRIOR>
-hipError_t launch_km(const PersistArgs& pa, int G, size_t lds, hipStream_t st) {
-  return pa.e_m ? launch_kk<LT, PRIOR, true>(pa, G, lds, st) : launch_kk<LT, PRIOR, false>(pa, G, lds, st);
-}
-
-}  // namespace
+extern template hipError_t launch_persistent_kk<4, false>(const PersistArgs&, int, size_t, dls_dtype, hipStream_t);
+extern template hipError_t launch_persistent_kk<8, false>(const PersistArgs&, int, size_t, dls_dtype, hipStream_t);
+extern template hipError_t launch_persistent_kk<4, true>(const PersistArgs&, int, size_t, dls_dtype, hipStream_t);
+extern template hipError_t launch_persistent_kk<8, true>(const PersistArgs&, int, size_t, dls_dtype, hipStream_t);
 
 PersistPlan persist_plan(const dls_local_head& h, int32_t batch, int32_t B, dls_dtype long_dtype, bool prior,
                          int G) {
@@ -1058,10 +82,16 @@ PersistWorkspace persist_workspace(const dls_local_head& h, int32_t batch, int32
 }
 
 hipError_t launch_persistent(const PersistArgs& pa, const PersistPlan& pl, dls_dtype long_dtype, hipStream_t st) {
-  const bool pr = pa.prior != nullptr;
-  if (long_dtype == DLS_BF16)
-    return pr ? launch_km<bf16_t, true>(pa, pl.G, pl.lds, st) : launch_km<bf16_t, false>(pa, pl.G, pl.lds, st);
-  return pr ? launch_km<float, true>(pa, pl.G, pl.lds, st) : launch_km<float, false>(pa, pl.G, pl.lds, st);
+  const bool sample = pa.smp.inv_temp != 0.f;
+  switch (pa.r / 32) {
+    case 4:
+      return sample ? launch_persistent_kk<4, true>(pa, pl.G, pl.lds, long_dtype, st)
+                    : launch_persistent_kk<4, false>(pa, pl.G, pl.lds, long_dtype, st);
+    case 8:
+      return sample ? launch_persistent_kk<8, true>(pa, pl.G, pl.lds, long_dtype, st)
+                    : launch_persistent_kk<8, false>(pa, pl.G, pl.lds, long_dtype, st);
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace dls

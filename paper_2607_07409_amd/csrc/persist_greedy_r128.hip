@@ -1,0 +1,7 @@
+// Instantiations of the persistent drafting kernel for rank r = 128 (greedy decoding).
+#include "draft_persistent.hpp"
+
+namespace dls {
+template hipError_t launch_persistent_kk<4, false>(const PersistArgs&, int, size_t, dls_dtype,
+                                                       hipStream_t);
+}  // namespace dls

@@ -44,9 +44,10 @@ def test_struct_layout_matches_c(tmp_path):
 #include <stddef.h>
 #include "{HEADER}"
 int main(void) {{
-  printf("%zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(dls_local_head), sizeof(dls_row_stats), sizeof(dls_fusion),
-         offsetof(dls_local_head, dtype), offsetof(dls_local_head, emb), offsetof(dls_local_head, w_vocab),
-         offsetof(dls_fusion, flags), offsetof(dls_local_head, kind));
+  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(dls_local_head), sizeof(dls_row_stats),
+         sizeof(dls_fusion), offsetof(dls_local_head, dtype), offsetof(dls_local_head, emb),
+         offsetof(dls_local_head, w_vocab), offsetof(dls_fusion, flags), offsetof(dls_local_head, kind),
+         sizeof(dls_sampling), offsetof(dls_sampling, seed));
   return 0;
 }}''')
     exe = tmp_path / "lay"
@@ -54,7 +55,7 @@ int main(void) {{
     got = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True).stdout.split()]
     want = [ctypes.sizeof(b.LocalHeadC), ctypes.sizeof(b.RowStats), ctypes.sizeof(b.Fusion),
             b.LocalHeadC.dtype.offset, b.LocalHeadC.emb.offset, b.LocalHeadC.w_vocab.offset,
-            b.Fusion.flags.offset, b.LocalHeadC.kind.offset]
+            b.Fusion.flags.offset, b.LocalHeadC.kind.offset, ctypes.sizeof(b.Sampling), b.Sampling.seed.offset]
     assert got == want
 
 
@@ -96,6 +97,36 @@ def _draft(head, **kw):
     rc = L.dls_draft_block(ctypes.byref(head), a["long"], a["ldt"], a["last"], a["prior"], a["batch"], a["B"],
                            a["f"], a["tok"], a["st"], a["ws"], a["wsb"], None)
     return rc, L.dls_last_error().decode()
+
+
+def _sampled(head, temperature, reserved=0, seed=0, **kw):
+    a = dict(long=FAKE[5], ldt=b.DLS_BF16, last=FAKE[6], prior=None, batch=2, B=4, f=b.fusion(),
+             tok=FAKE[7], st=FAKE[8], ws=FAKE[9], wsb=1 << 30)
+    a.update(kw)
+    L = b.lib()
+    rc = L.dls_draft_block_sampled(ctypes.byref(head), a["long"], a["ldt"], a["last"], a["prior"], a["batch"],
+                                   a["B"], a["f"], b.Schedule(None, None), b.Sampling(temperature, reserved, seed),
+                                   a["tok"], a["st"], a["ws"], a["wsb"], None)
+    return rc, L.dls_last_error().decode()
+
+
+def test_sampled_draft_rejects_bad_temperature():
+    for T in (-1.0, float("nan"), float("inf"), 1e-45, 1e31):
+        rc, msg = _sampled(_head(), T)
+        assert b.STATUS[rc] == "DLS_ERR_ARG", (T, msg)
+        assert "temperature" in msg
+    rc, msg = _sampled(_head(), 1.0, reserved=1)
+    assert b.STATUS[rc] == "DLS_ERR_ARG" and "reserved" in msg
+    # argument checks of the plain entry point apply too
+    assert b.STATUS[_sampled(_head(V=0), 1.0)[0]] == "DLS_ERR_SHAPE"
+    assert _sampled(_head(), 1.0, batch=0, long=None, tok=None)[0] == 0
+
+
+@pytest.mark.skipif(HAS_GPU, reason="would launch on fake pointers when a GPU is present")
+def test_sampled_valid_arguments_stop_at_device_check():
+    for T in (0.0, 1.0, 0.25, 1e-6):
+        rc, msg = _sampled(_head(), T, seed=(1 << 64) - 1)
+        assert b.STATUS[rc] == "DLS_ERR_DEVICE", (T, msg)
 
 
 def test_draft_block_rejects_bad_arguments():
