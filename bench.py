@@ -45,7 +45,7 @@ def compulsory_bytes_per_block(wl, esize=2):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_draft_persistent_qwen3-4b-b1_traffic.txt")
-KERNEL_SOURCES = ["paper_2607_07409_amd/csrc/draft_persistent.hip", "paper_2607_07409_amd/csrc/dels_internal.hpp",
+KERNEL_SOURCES = ["paper_2607_07409_amd/csrc/draft_persistent.hpp", "paper_2607_07409_amd/csrc/dels_internal.hpp",
                   "paper_2607_07409_amd/csrc/dels_device.hpp", "paper_2607_07409_amd/csrc/build.py"]
 
 
@@ -85,7 +85,11 @@ def main():
     ap.add_argument("--profile-only", action="store_true",
                     help="for hardware-counter runs: only --steps draft blocks and a 1 GiB device copy "
                          "(the copy calibrates the HBM byte counters); no JSON line")
+    ap.add_argument("--cooperative", action="store_true",
+                    help="launch the persistent kernel cooperatively in the timed step (default: an ordinary "
+                         "dispatch, DLS_EXCLUSIVE_DEVICE, since this process owns the device)")
     args = ap.parse_args()
+    EXC = not args.cooperative
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py: this build measures one GPU only (the drafting path has no multi-GPU form "
@@ -120,7 +124,7 @@ def main():
         st = torch.empty((wl.batch, wl.B, 6), dtype=torch.float32, device=dev)
         ws = B.draft_workspace(head, wl.batch, wl.B, dev)
         for _ in range(args.steps):
-            B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws)
+            B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws, exclusive_device=EXC)
         src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
@@ -169,7 +173,7 @@ def main():
     ws = B.draft_workspace(head, wl.batch, wl.B, dev)
 
     def step():
-        B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws)
+        B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws, exclusive_device=EXC)
         B.accept_len(tok, tgt, out=acc)
 
     log(f"warmup {args.warmup} steps")
@@ -195,7 +199,7 @@ def main():
     e2, e3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e2.record()
     for _ in range(n_k):
-        B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws)
+        B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws, exclusive_device=EXC)
     e3.record()
     torch.cuda.synchronize()
     blk_us = e2.elapsed_time(e3) / n_k * 1e3
@@ -216,6 +220,19 @@ def main():
                 "compulsory_frac": round(comp / (blk_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
     log(f"draft block {blk_us:.1f} us, {achieved:.0f} GB/s algorithmic ({achieved / HBM_PEAK_GBS:.1%} of HBM peak)")
 
+    # the same block with the other launch mode (cooperative vs ordinary dispatch), for comparison
+    for _ in range(3):
+        B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws,
+                      exclusive_device=not EXC)
+    e2.record()
+    for _ in range(n_k):
+        B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws,
+                      exclusive_device=not EXC)
+    e3.record()
+    torch.cuda.synchronize()
+    other_launch_us = e2.elapsed_time(e3) / n_k * 1e3
+    log(f"draft block with {'a cooperative' if EXC else 'an ordinary'} launch: {other_launch_us:.1f} us")
+
     # the same block through the per-position launches (no prepared head), for comparison
     ws2 = B.draft_workspace(base_head, wl.batch, wl.B, dev)
     for _ in range(3):
@@ -230,11 +247,13 @@ def main():
 
     # ---- temperature sampling (T = 1, Gumbel-max with Philox noise) on the same block --------
     for _ in range(3):
-        B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws, temperature=1.0,
+        B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws, exclusive_device=EXC,
+                      temperature=1.0,
                       seed=12345)
     e2.record()
     for i in range(n_k):
-        B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws, temperature=1.0,
+        B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws, exclusive_device=EXC,
+                      temperature=1.0,
                       seed=12345 + i)
     e3.record()
     torch.cuda.synchronize()
@@ -251,10 +270,10 @@ def main():
     mhead = B.LocalHead.markov_from_weights(em, wm, dev).prepare()
     mws = B.draft_workspace(mhead, wl.batch, wl.B, dev)
     for _ in range(5):
-        B.draft_block(mhead, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=mws)
+        B.draft_block(mhead, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=mws, exclusive_device=EXC)
     e2.record()
     for _ in range(n_k):
-        B.draft_block(mhead, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=mws)
+        B.draft_block(mhead, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=mws, exclusive_device=EXC)
     e3.record()
     torch.cuda.synchronize()
     assert B.workspace_error(mws) == 0, "persistent kernel reported a stalled hand-off"
@@ -333,11 +352,13 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "batch": wl.batch, "B": wl.B, "V": wl.V, "d": wl.d, "H": wl.H,
                    "r": wl.r, "weights": f"bf16 ({args.init} init)", "alpha": args.alpha, "beta": 0.0,
-                   "step": "draft_block + accept_len"},
+                   "step": "draft_block + accept_len",
+                   "launch": "ordinary dispatch (DLS_EXCLUSIVE_DEVICE)" if EXC else "cooperative"},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "combine": combine,
         "draft_block_per_position_launches_us": round(launches_us, 2),
+        ("draft_block_cooperative_launch_us" if EXC else "draft_block_ordinary_launch_us"): round(other_launch_us, 2),
         "sampling": sampling,
         "markov_head": markov,
         "prior_estimation": prior_est,

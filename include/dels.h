@@ -69,6 +69,15 @@ typedef enum dls_dtype { DLS_F32 = 0, DLS_BF16 = 1 } dls_dtype;
                                          from the long logits alone (no short logits, no
                                          prior) and the head only consumes drafted tokens;
                                          the last accepted token is then unused. */
+#define DLS_EXCLUSIVE_DEVICE 0x2u     /* The caller guarantees that no other kernel runs on the
+                                         device during the call.  The persistent drafting kernel
+                                         is then launched as an ordinary dispatch rather than a
+                                         cooperative one, which on MI355X saves about 17 us of
+                                         dispatch time per call.  If other work does hold compute
+                                         units, workgroups wait for them; a wait longer than the
+                                         hand-off spin budget (a fraction of a second) sets the
+                                         workspace error word.  Ignored by the per-position path
+                                         and by dls_combine_logits. */
 
 /* Fusion weights (Sec. 4.3).  The paper uses w_long = 1 and alpha = beta = 0.3;
    alpha = beta = 0 is the DFlash baseline (Sec. 5.6). */
@@ -76,7 +85,7 @@ typedef struct dls_fusion {
   float w_long;    /* weight on the long logits                       */
   float alpha;     /* weight on the short (local-head) logits         */
   float beta;      /* weight subtracted on the log unigram prior      */
-  uint32_t flags;  /* DLS_FIRST_ROW_LONG_ONLY or 0                    */
+  uint32_t flags;  /* DLS_FIRST_ROW_LONG_ONLY | DLS_EXCLUSIVE_DEVICE, or 0 */
 } dls_fusion;
 
 /* Per-row statistics of the fused distribution, for the decoded token t.

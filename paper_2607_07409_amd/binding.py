@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libdels.so")
 DLS_F32, DLS_BF16 = 0, 1
 DLS_HEAD_RNN, DLS_HEAD_MARKOV = 0, 1
 DLS_FIRST_ROW_LONG_ONLY = 0x1
+DLS_EXCLUSIVE_DEVICE = 0x2
 STATUS = {0: "DLS_OK", 1: "DLS_ERR_ARG", 2: "DLS_ERR_SHAPE", 3: "DLS_ERR_DTYPE",
           4: "DLS_ERR_WORKSPACE", 5: "DLS_ERR_DEVICE", 6: "DLS_ERR_HIP"}
 STATS_FIELDS = ("score", "logprob", "gap", "lse_long", "lse_short", "lse_fused")
@@ -123,8 +124,9 @@ def _dtype_code(t: torch.Tensor) -> int:
     raise TypeError(f"unsupported dtype {t.dtype}")
 
 
-def fusion(w_long=1.0, alpha=0.3, beta=0.3, first_row_long_only=False) -> Fusion:
-    return Fusion(w_long, alpha, beta, DLS_FIRST_ROW_LONG_ONLY if first_row_long_only else 0)
+def fusion(w_long=1.0, alpha=0.3, beta=0.3, first_row_long_only=False, exclusive_device=False) -> Fusion:
+    return Fusion(w_long, alpha, beta, (DLS_FIRST_ROW_LONG_ONLY if first_row_long_only else 0) |
+                  (DLS_EXCLUSIVE_DEVICE if exclusive_device else 0))
 
 
 # -----------------------------------------------------------------------------------
@@ -260,11 +262,12 @@ def workspace_error(workspace: torch.Tensor) -> int:
 
 def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional[torch.Tensor], prior=None,
                 w_long=1.0, alpha=0.3, beta=0.3, first_row_long_only=False, want_stats=True, out=None,
-                workspace=None, stream=None, temperature=0.0, seed=0):
+                workspace=None, stream=None, temperature=0.0, seed=0, exclusive_device=False):
     """Draft one block per sequence.  long_logits [batch, B, V]; returns (tokens [batch, B], stats
     [batch, B, 6] or None).  alpha and beta are scalars or [B] per-position weights.
     temperature 0 decodes greedily; T > 0 samples from softmax(l / T) with the Philox noise of
-    `seed` (a 64-bit integer)."""
+    `seed` (a 64-bit integer).  exclusive_device: the caller runs nothing else on the device
+    during the call (DLS_EXCLUSIVE_DEVICE: an ordinary instead of a cooperative dispatch)."""
     L = lib()
     batch, B, V = long_logits.shape
     dev = long_logits.device
@@ -277,7 +280,8 @@ def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional
         workspace = draft_workspace(head, batch, B, dev)
     scheduled = np.ndim(alpha) > 0 or np.ndim(beta) > 0
     sampled = temperature != 0.0
-    f = fusion(w_long, 0.0 if np.ndim(alpha) else alpha, 0.0 if np.ndim(beta) else beta, first_row_long_only)
+    f = fusion(w_long, 0.0 if np.ndim(alpha) else alpha, 0.0 if np.ndim(beta) else beta, first_row_long_only,
+               exclusive_device)
     if scheduled or sampled:
         # per-position weights: host arrays of B values (kept alive across the call)
         al = np.ascontiguousarray(alpha, np.float32) if np.ndim(alpha) else None

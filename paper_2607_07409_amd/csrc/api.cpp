@@ -81,7 +81,8 @@ size_t dsize(dls_dtype t) { return t == DLS_BF16 ? 2 : 4; }
 dls_status check_fusion(const dls_fusion& f) {
   if (!std::isfinite(f.w_long) || !std::isfinite(f.alpha) || !std::isfinite(f.beta))
     return fail(DLS_ERR_ARG, "fusion weights must be finite");
-  if (f.flags & ~DLS_FIRST_ROW_LONG_ONLY) return fail(DLS_ERR_ARG, "unknown fusion flags 0x%x", f.flags);
+  if (f.flags & ~(DLS_FIRST_ROW_LONG_ONLY | DLS_EXCLUSIVE_DEVICE))
+    return fail(DLS_ERR_ARG, "unknown fusion flags 0x%x", f.flags);
   return DLS_OK;
 }
 
@@ -301,6 +302,7 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_d
       }
       pa.literal = (fusion.flags & DLS_FIRST_ROW_LONG_ONLY) ? 1 : 0;
       pa.smp = smp;
+      pa.ordinary_launch = (fusion.flags & DLS_EXCLUSIVE_DEVICE) ? 1 : 0;
       pa.out_tokens = out_tokens;
       pa.out_stats = out_stats;
       pa.hdr = (uint32_t*)ws;

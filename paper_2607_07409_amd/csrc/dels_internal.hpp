@@ -118,6 +118,7 @@ struct PersistArgs {
   float al_j[64], be_j[64];  // fusion weights of each draft position (B <= 64)
   int literal;
   Sampler smp;               // temperature sampling (smp.inv_temp = 0: greedy)
+  int ordinary_launch;       // host only: ordinary instead of cooperative dispatch
   int32_t* out_tokens;
   dls_row_stats* out_stats;
   uint32_t* hdr;             // [0] call epoch, [1] error word

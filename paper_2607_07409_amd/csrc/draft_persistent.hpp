@@ -1028,6 +1028,10 @@ hipError_t launch_k(const PersistArgs& pa, int G, size_t lds, hipStream_t st) {
   (void)lds;
   PersistArgs copy = pa;
   void* args[] = {&copy};
+  // A cooperative dispatch makes the runtime check co-residency and keep other kernels off the
+  // device, at about 17 us per call; the caller may waive it (the grid never exceeds one
+  // workgroup per CU, so on an otherwise idle device every workgroup is resident at once).
+  if (pa.ordinary_launch) return hipLaunchKernel((const void*)kern, dim3(G), dim3(kT), args, lds, st);
   return hipLaunchCooperativeKernel((const void*)kern, dim3(G), dim3(kT), args, (unsigned)lds, st);
 }
 

@@ -174,6 +174,8 @@ def test_valid_arguments_stop_at_device_check():
     # the literal first-row reading does not need the last token
     rc, _ = _draft(_head(), last=None, f=b.fusion(first_row_long_only=True))
     assert b.STATUS[rc] == "DLS_ERR_DEVICE"
+    rc, _ = _draft(_head(), f=b.fusion(first_row_long_only=True, exclusive_device=True))   # both flags known
+    assert b.STATUS[rc] == "DLS_ERR_DEVICE"
     L = b.lib()
     rc = L.dls_combine_logits(FAKE[0], FAKE[1], b.DLS_BF16, None, 4, 1000, b.fusion(), FAKE[2], None, None,
                               FAKE[3], 1 << 20, None)

@@ -195,6 +195,27 @@ def test_persistent_repeat_and_paths_agree():
         assert np.all(ref.gap[near] < TOL)
 
 
+@pytest.mark.parametrize("shape", [0, 1, 3])
+def test_exclusive_device_launch_same_bits(shape):
+    """DLS_EXCLUSIVE_DEVICE (an ordinary instead of a cooperative dispatch of the persistent
+    kernel) returns the cooperative launch's bits, call after call on one workspace."""
+    p = _problem("qwen3-8b-b16", "stress", dtype="bf16", **SMALL[shape])
+    head = _head(p, True)
+    lt = B.as_tensor(p["long_h"])
+    last = torch.from_numpy(p["last"]).cuda()
+    prior = torch.from_numpy(p["prior"]).cuda()
+    ws = B.draft_workspace(head, lt.shape[0], lt.shape[1])
+    outs = []
+    for i in range(6):
+        tok, st = B.draft_block(head, lt, last, prior, 1.0, 0.5, 0.3, workspace=ws, exclusive_device=bool(i % 2))
+        outs.append((tok.clone(), st.clone()))
+    torch.cuda.synchronize()
+    assert B.workspace_error(ws) == 0
+    for tok, st in outs[1:]:
+        assert torch.equal(tok, outs[0][0]) and torch.equal(st.view(torch.int32), outs[0][1].view(torch.int32))
+    _check(p, 0.5, 0.3, with_prior=True, prepared=True, sequences=[0, p["wl"].batch - 1])
+
+
 @pytest.mark.parametrize("name", ["tiny", "qwen3-4b-b1", "qwen3-8b-b16"])
 def test_accept_len_on_drafts(name):
     """Targets agree with the oracle draft for a geometric prefix; the GPU acceptance length on its own
