@@ -286,8 +286,7 @@ def main():
 
     # ---- unigram log-prior estimation (App. A) from a Zipf-distributed token stream --------
     n_p = 1 << 26
-    gen = torch.Generator(device=dev).manual_seed(5)
-    ptok = torch.randint(0, wl.V, (n_p,), dtype=torch.int32, device=dev, generator=gen)
+    ptok = torch.from_numpy(W.make_token_stream(n_p, wl.V, 5)).to(dev)
     plogp = torch.empty(wl.V, dtype=torch.float32, device=dev)
     pcnt = torch.empty(wl.V + 1, dtype=torch.int64, device=dev)
     for _ in range(3):

@@ -29,11 +29,22 @@ Readings where the paper is silent (each is also listed in the design notes):
   head only sees drafted tokens (the literal form of Algorithm 1).
 * The acceptance length counts leading positions where draft == target
   (0..B); the paper's tau adds the bonus token, tau = accepted + 1.
+* Per-position fusion weights alpha_j, beta_j (Sec. 5.6) are indexed by the
+  row j of the block; a row decoded from the long logits alone ignores them.
+* The Markov head's state at row j is E_M of the token before it: the last
+  accepted token for row 0, the drafted token d_{j-1} afterwards.
+* Sampling at temperature T > 0 (the paper reports T = 0 and T = 1 but not how
+  it draws) is the Gumbel-max rule on l / T.  The noise of entry v of row
+  (sequence b, position j) comes from Philox4x32-10 keyed by the seed at
+  counter (v // 4, j, b, 0), word v % 4, u = ((x >> 9) + 1/2) / 2^23 and
+  g = -log(-log u), so that a draw depends on (seed, b, j, v) only.
 
 Parity pins (tests/test_oracle_*.py): exact-rational brute force on tiny
 vocabularies, the alpha = 0 / w_long = 0 limits, shift invariance, a
-hand-worked three-position example, torch.nn.GRU equivalence and closed forms
-for the acceptance length.
+hand-worked three-position example, torch.nn.GRU equivalence, closed forms
+for the acceptance length, brute-force counting for the prior, the published
+Philox4x32-10 known-answer vectors, the Gumbel moments and chi-square tests
+of the sampled distribution.
 """
 from __future__ import annotations
 

@@ -222,6 +222,21 @@ def zipf_ranks(V: int, seed: int) -> np.ndarray:
     return ranks
 
 
+def make_token_stream(n: int, V: int, seed: int, s: float = 1.1) -> np.ndarray:
+    """n int32 token ids with Zipf(s) frequencies over a seeded ranking of the vocabulary
+    (inverse-CDF draws, in chunks)."""
+    order = np.argsort(zipf_ranks(V, seed))          # token of rank k + 1
+    cdf = np.cumsum(1.0 / np.arange(1, V + 1, dtype=np.float64) ** s)
+    cdf /= cdf[-1]
+    g = _rng(seed, _P_LONG, 998)
+    out = np.empty(n, dtype=np.int32)
+    step = 1 << 22
+    for i in range(0, n, step):
+        m = min(step, n - i)
+        out[i:i + m] = order[np.minimum(np.searchsorted(cdf, g.random(m), side="right"), V - 1)]
+    return out
+
+
 def make_long_logits(wl: Workload, seed: Optional[int] = None):
     """[batch, B, V] long logits following the workload's recipe."""
     seed = wl.seed if seed is None else seed
