@@ -42,6 +42,30 @@ def test_unigram_prior(n, V, smoothing, seed):
     assert ulps.max() <= 1, ulps.max()
 
 
+@pytest.mark.parametrize("kind", ["uniform", "constant", "two_hot"])
+def test_unigram_prior_adversarial_streams(kind):
+    """Streams that defeat the per-workgroup LDS caches: uniform ids over the Qwen3 vocabulary
+    (most tokens fall back to device atomics), one id repeated (every increment hits one slot)
+    and two ids sharing a hash neighbourhood, interleaved."""
+    V = W.QWEN3_VOCAB
+    g = np.random.default_rng(91)
+    if kind == "uniform":
+        toks = g.integers(0, V, 6_000_000).astype(np.int32)
+    elif kind == "constant":
+        toks = np.full(3_000_001, 4242, np.int32)
+    else:
+        toks = np.where(g.random(2_000_000) < 0.5, 17, 18).astype(np.int32)
+    logp, counts = B.unigram_log_prior(torch.from_numpy(toks).cuda(), V, 1.0)
+    torch.cuda.synchronize()
+    want_counts = np.bincount(toks, minlength=V)
+    got = counts.cpu().numpy()
+    assert np.array_equal(got[:V], want_counts)
+    assert got[V] == toks.size
+    want = O.unigram_log_prior(want_counts, 1.0).astype(np.float32)
+    ulps = np.abs(logp.cpu().numpy().view(np.int32).astype(np.int64) - want.view(np.int32).astype(np.int64))
+    assert ulps.max() <= 1
+
+
 def test_unigram_prior_feeds_combine():
     """The estimated prior is the prior argument of the fused combine (beta term)."""
     V = 4099
