@@ -397,6 +397,10 @@ template <int KK, typename LT, bool PRIOR, bool NARROW, bool MARKOV, bool SAMPLE
 __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr int TPW = kOps / KK;   // AGPR tiles per wave
+  // At most 4 sequences use at most 4 of an MFMA's 16 A rows, so the hi and lo halves of rho
+  // share one operand (rows 0..3 hi, 4..7 lo): one MFMA chain per tile instead of two.  The
+  // two halves' products are summed when the tile is folded, in the same order as before.
+  constexpr bool PACK = NARROW && !MARKOV;
   const int w = blockIdx.x, G = gridDim.x, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, n16 = lane & 15, g4 = lane >> 4;
   const int V = a.V, H = a.H, r = a.r, batch = a.batch, Bk = a.B, rpg = a.rpg;
@@ -543,8 +547,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     }
   };
   // GRU workgroups with a single M tile hand their statistics of position j over during
-  // position j + 1: right after the argmax key they are on the critical path to the next
-  // merge.  -1: nothing pending.
+  // the gather of position j + 1: right after the argmax key they are on the critical path
+  // to the next merge.  -1: nothing pending.
   int pending_stats = -1;
 
   for (int j = 0; j < Bk; ++j) {
@@ -579,10 +583,19 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
             hv[i] = (hs > 0 && 4 * g4 + i < nb) ? ld64(hprev + (size_t)(mt * 16 + 4 * g4 + i) * H + 16 * w + n16)
                                                  : 0ull;
         }
-        for (int i = tid; i < 16 * 48; i += kT) {
-          const int slot = i / 48, q = (i % 48) / 16, u = i % 16;
-          s_gi[i] = slot < nb ? a.T[(size_t)s_tok[mt * 16 + slot] * 3 * H + q * H + 16 * w + u] : 0.f;
+        // with statistics of the previous position pending, wave 3 publishes them while the
+        // other waves gather (the gather is latency-bound; wave 3 loads nothing until the
+        // rank stage, so its stores delay no load of its own)
+        const int gthreads = pending_stats >= 0 ? 192 : kT;
+        if (tid < gthreads) {
+          for (int i = tid; i < 16 * 48; i += gthreads) {
+            const int slot = i / 48, q = (i % 48) / 16, u = i % 16;
+            s_gi[i] = slot < nb ? a.T[(size_t)s_tok[mt * 16 + slot] * 3 * H + q * H + 16 * w + u] : 0.f;
+          }
+        } else {
+          publish_stats(pending_stats, 0, batch, 3);
         }
+        pending_stats = -1;
         __syncthreads();
         bool ok = true;
         if (wave == 0) {
@@ -624,10 +637,6 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
           if (k0) __syncthreads();
           ok &= stage_split(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
           __syncthreads();
-          if (pending_stats >= 0) {   // s_part still holds it: nothing has used the space since
-            publish_stats(pending_stats, 0, batch, 3);
-            pending_stats = -1;
-          }
           for (int kk = wave; kk < HC / 32; kk += 4) {
             uint4 ahi, alo;
             plane_operand(s_hi, s_lo, pitch, nb, n16, g4, 32 * kk, ahi, alo);
@@ -743,8 +752,20 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         wait_producers(rsrc, (size_t)rpg, a.NG, tag, err);
         const bool ok = stage_split(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err);
         if (fail_barrier(!ok, s_fail)) return;
+        if (PACK) {
+          // rows 0..3 of the A operand carry the hi halves of slots 0..3, rows 4..7 the lo
+          // halves (rows past the batch repeat slot 0, rows 8..15 are unused)
+          const uint16_t* pl = (n16 & 4) ? s_lo : s_hi;
+          const int row = (n16 & 3) < nb ? (n16 & 3) : 0;
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) plane_operand(s_hi, s_lo, r + 8, nb, n16, g4, 32 * kk, ahi[kk], alo[kk]);
+          for (int kk = 0; kk < KK; ++kk) {
+            ahi[kk] = *(const uint4*)(pl + row * (r + 8) + 32 * kk + 8 * g4);
+            alo[kk] = make_uint4(0, 0, 0, 0);
+          }
+        } else {
+#pragma unroll
+          for (int kk = 0; kk < KK; ++kk) plane_operand(s_hi, s_lo, r + 8, nb, n16, g4, 32 * kk, ahi[kk], alo[kk]);
+        }
       } else {
         __syncthreads();   // s_ll complete
       }
@@ -756,7 +777,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       // wave, 16 KiB in all), so that the Gumbel noise is generated in one loop body rather
       // than in every unrolled tile.
       constexpr bool stash_wide = SAMPLE && !NARROW;
-      float* s_stash = (float*)s_hi + wave * (stash_wide ? 1024 : 256);   // [4 tiles][slots][16 rows]
+      float* s_stash = (float*)s_hi + wave * (stash_wide ? 1024 : (PACK ? 512 : 256));   // [halves][4 tiles][slots][16 rows]
       if (narrow || stash_wide) __syncthreads();
 
       Partial P[4];
@@ -782,6 +803,12 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
 #pragma unroll
           for (int i = 0; i < 4; ++i)
             if (i < nb) s_stash[(tq * 16 + 4 * g4 + i) * 16 + n16] = acc[i];
+        } else if (PACK) {   // lane group 0 holds the hi products, group 1 the lo products
+          if (g4 < 2) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (i < nb) s_stash[((g4 * 4 + tq) * 4 + i) * 16 + n16] = acc[i];
+          }
         } else if (g4 == 0) {
 #pragma unroll
           for (int i = 0; i < 4; ++i)
@@ -804,7 +831,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
                 if (long_only) {
                   f = wl * x;
                 } else {
-                  const float sv = s_stash[(g4 * 4 + i) * 16 + n16];
+                  const float sv = PACK ? s_stash[(g4 * 4 + i) * 16 + n16] + s_stash[((4 + g4) * 4 + i) * 16 + n16]
+                                        : s_stash[(g4 * 4 + i) * 16 + n16];
                   f = __builtin_fmaf(al, sv, wl * x);
                   if (PRIOR) f = __builtin_fmaf(-be, s_prior[row], f);
                   lse_push(P[i].S, sv);
@@ -869,16 +897,16 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
 #pragma unroll
             for (int kk = 0; kk < KK; ++kk) {
               c0 = mfma_va(ahi[kk], wr[q * KK + kk], c0);
-              if (!MARKOV) c1 = mfma_va(alo[kk], wr[q * KK + kk], c1);
+              if (!MARKOV && !PACK) c1 = mfma_va(alo[kk], wr[q * KK + kk], c1);
               if (two) {
                 c2 = mfma_va(ahi[kk], wr[q2 * KK + kk], c2);
-                if (!MARKOV) c3 = mfma_va(alo[kk], wr[q2 * KK + kk], c3);
+                if (!MARKOV && !PACK) c3 = mfma_va(alo[kk], wr[q2 * KK + kk], c3);
               }
             }
           }
           if (narrow || stash_wide) {
-            stash(c0 + c1, q % 4);
-            if (two) stash(c2 + c3, q % 4 + 1);
+            stash(PACK ? c0 : c0 + c1, q % 4);
+            if (two) stash(PACK ? c2 : c2 + c3, q % 4 + 1);
           } else {
             fold_tile(c0 + c1, lt);
             if (two && lt + 1 < na) fold_tile(c2 + c3, lt + 1);
@@ -901,10 +929,10 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
           for (int kk = 0; kk < KK; ++kk) {
             const uint4 bw = s_wtiles[((size_t)lq * KK + kk) * 64 + lane];
             c0 = mfma_vv(ahi[kk], bw, c0);
-            if (!MARKOV) c1 = mfma_vv(alo[kk], bw, c1);
+            if (!MARKOV && !PACK) c1 = mfma_vv(alo[kk], bw, c1);
           }
         }
-        return c0 + c1;
+        return PACK ? c0 : c0 + c1;
       };
       if (narrow || stash_wide) {
         for (int m0 = 0; wave + 4 * m0 < nl; m0 += 4) {
