@@ -267,28 +267,6 @@ __device__ __forceinline__ void copy_to_lds(uint4* dst, const uint4* src, int n)
   }
 }
 
-// Wave 0 spins until the first word of each producer p < np (at src0 + p * pstride) carries
-// the tag, one lane per producer, while the other waves wait at the barrier: the data itself
-// is then read once.  Keeps the polling traffic on a hand-off to one load per producer.
-__device__ __forceinline__ void wait_producers(const uint64_t* src0, size_t pstride, int np, uint32_t tag,
-                                               uint32_t* err) {
-  if (threadIdx.x < 64) {
-    const int l = (int)threadIdx.x;
-    bool done = l >= np;
-    for (long s = 0;; ++s) {
-      if (!done) done = (uint32_t)(ld64(src0 + (size_t)l * pstride) >> 32) == tag;
-      if (__all(done)) break;
-      __builtin_amdgcn_s_sleep(4);
-      if ((s & 63) == 63 && ld32(err)) break;
-      if (s > kMaxSpins) {
-        st32(err, 1u);
-        break;
-      }
-    }
-  }
-  __syncthreads();
-}
-
 // Operand planes: staged hand-off values as bf16 hi and lo halves, 16 slots x (K + 8) each
 // (the 8-element pad spreads the slots' rows over the LDS banks).
 constexpr int kPlane = 16 * (kStageK + 8);
@@ -344,6 +322,77 @@ __device__ __forceinline__ bool stage_split(const uint64_t* src, int rows, int w
     }
   }
   return ok;
+}
+
+// The same, polling: every thread re-reads only its words whose tag does not match yet, all
+// of them in flight together, until none is left (or the spin budget runs out).  A consumer
+// that arrives when the producers are about done pays one round trip per poll instead of a
+// separate wait followed by a bulk read.
+__device__ __forceinline__ bool stage_poll(const uint64_t* src, int rows, int width, size_t stride, uint32_t tag,
+                                           uint16_t* hi, uint16_t* lo, int pitch, uint32_t* err) {
+  const int q = kT / width, rm = kT % width;
+  int row = (int)threadIdx.x / width, col = (int)threadIdx.x % width;
+  bool ok = true;
+  for (int base = 0; base < rows * width; base += kT * kInflight) {
+    int rr[kInflight], cc[kInflight];
+    uint32_t pend = 0;
+#pragma unroll
+    for (int m = 0; m < kInflight; ++m) {
+      rr[m] = row;
+      cc[m] = col;
+      if (row < rows) pend |= 1u << m;
+      col += rm;
+      row += q;
+      if (col >= width) {
+        col -= width;
+        ++row;
+      }
+    }
+    for (long sp = 0; pend; ++sp) {
+      uint64_t v[kInflight];
+#pragma unroll
+      for (int m = 0; m < kInflight; ++m) v[m] = (pend >> m) & 1u ? ld64(src + (size_t)rr[m] * stride + cc[m]) : 0ull;
+#pragma unroll
+      for (int m = 0; m < kInflight; ++m) {
+        if (((pend >> m) & 1u) && (uint32_t)(v[m] >> 32) == tag) {
+          put_split(hi, lo, rr[m] * pitch + cc[m], (uint32_t)v[m]);
+          pend &= ~(1u << m);
+        }
+      }
+      if (!pend) break;
+      __builtin_amdgcn_s_sleep(2);
+      if ((sp & 63) == 63 && ld32(err)) {
+        ok = false;
+        break;
+      }
+      if (sp > kMaxSpins) {
+        st32(err, 1u);
+        ok = false;
+        break;
+      }
+    }
+  }
+  return ok;
+}
+
+// Wait until at least one of np producers has published (one lane per producer); the bulk of
+// a hand-off then follows within a fraction of a microsecond.
+__device__ __forceinline__ void wait_any_producer(const uint64_t* src0, size_t pstride, int np, uint32_t tag,
+                                                  uint32_t* err) {
+  if (threadIdx.x < 64) {
+    const int l = (int)threadIdx.x;
+    for (long sp = 0;; ++sp) {
+      const bool seen = l < np && (uint32_t)(ld64(src0 + (size_t)l * pstride) >> 32) == tag;
+      if (__any(seen)) break;
+      __builtin_amdgcn_s_sleep(4);
+      if ((sp & 63) == 63 && ld32(err)) break;
+      if (sp > kMaxSpins) {
+        st32(err, 1u);
+        break;
+      }
+    }
+  }
+  __syncthreads();
 }
 
 // Workgroup barrier that also tells whether any thread failed.  A failure is final (all waves
@@ -630,12 +679,12 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         const int HC = nb * (H + 8) <= kPlane ? H : kStageK;
         const int pitch = HC + 8;
         const uint64_t* hsrc = hnew + (size_t)mt * 16 * H;
-        wait_producers(hsrc, 16, a.NG, tag, err);
         bool ok = true;
         f32x4_t racc = f32x4_t{0.f, 0.f, 0.f, 0.f};
         for (int k0 = 0; k0 < H; k0 += HC) {
           if (k0) __syncthreads();
-          ok &= stage_split(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
+          // the other GRU workgroups publish h at about the same time: poll the words directly
+          ok &= stage_poll(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
           __syncthreads();
           for (int kk = wave; kk < HC / 32; kk += 4) {
             uint4 ahi, alo;
@@ -749,8 +798,10 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         }
       } else if (!long_only) {
         const uint64_t* rsrc = a.rbuf + ((size_t)(w % kRhoCopies) * 2 + par) * batch * r + (size_t)mt * 16 * r;
-        wait_producers(rsrc, (size_t)rpg, a.NG, tag, err);
-        const bool ok = stage_split(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err);
+        // GRU workgroups come here after W_hh h, when rho is about complete: they poll the words
+        // directly; the others wait (gently) for the first producer, then poll
+        if (!gru) wait_any_producer(rsrc, (size_t)rpg, a.NG, tag, err);
+        const bool ok = stage_poll(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err);
         if (fail_barrier(!ok, s_fail)) return;
         if (PACK) {
           // rows 0..3 of the A operand carry the hi halves of slots 0..3, rows 4..7 the lo
