@@ -41,6 +41,7 @@ constexpr int kOps = 56;         // MFMA B operands of 16 bytes per lane held in
                                  // the 256; the rest take the accumulators)
 constexpr long kMaxSpins = 1L << 22;
 constexpr int kInflight = 8;     // hand-off loads a thread issues before checking any of them
+                                 // (twice as many for batches of more than 4 sequences)
 constexpr int kStageK = 256;     // K chunk of staged hand-off values (16 slots x 256 floats in LDS)
 constexpr int kStatWords = 9;    // tagged words of one published partial
 constexpr int kRhoCopies = 8;    // replicas of the published rank vector (spreads the readers)
@@ -280,66 +281,22 @@ __device__ __forceinline__ void put_split(uint16_t* hi, uint16_t* lo, int idx, u
 }
 
 // Stage rows x width tagged words (row stride `stride` words) into the operand planes at
-// [row * pitch + c].  Every thread issues kInflight loads back to back before checking any tag
-// (one round trip per stage); words that were not ready yet are re-polled one by one.
-__device__ __forceinline__ bool stage_split(const uint64_t* src, int rows, int width, size_t stride, uint32_t tag,
-                                            uint16_t* hi, uint16_t* lo, int pitch, uint32_t* err) {
-  const int q = kT / width, rm = kT % width;
-  int row = (int)threadIdx.x / width, col = (int)threadIdx.x % width;
-  bool ok = true;
-  for (int base = 0; base < rows * width; base += kT * kInflight) {
-    uint64_t v[kInflight];
-    int rr[kInflight], cc[kInflight];
-#pragma unroll
-    for (int m = 0; m < kInflight; ++m) {
-      rr[m] = row;
-      cc[m] = col;
-      v[m] = row < rows ? ld64(src + (size_t)row * stride + col) : 0ull;
-      col += rm;
-      row += q;
-      if (col >= width) {
-        col -= width;
-        ++row;
-      }
-    }
-    uint32_t bad = 0;
-#pragma unroll
-    for (int m = 0; m < kInflight; ++m) {
-      if (rr[m] < rows) {
-        if ((uint32_t)(v[m] >> 32) == tag) put_split(hi, lo, rr[m] * pitch + cc[m], (uint32_t)v[m]);
-        else bad |= 1u << m;
-      }
-    }
-#pragma unroll 1
-    for (int m = 0; bad; ++m, bad >>= 1) {
-      if (bad & 1u) {
-        const int e = base + m * kT + (int)threadIdx.x;
-        const int r0 = e / width, c0 = e % width;
-        uint64_t x;
-        ok &= wait_tag(src + (size_t)r0 * stride + c0, tag, err, x);
-        put_split(hi, lo, r0 * pitch + c0, (uint32_t)x);
-      }
-    }
-  }
-  return ok;
-}
-
-// The same, polling: every thread re-reads only its words whose tag does not match yet, all
-// of them in flight together, until none is left (or the spin budget runs out).  A consumer
-// that arrives when the producers are about done pays one round trip per poll instead of a
-// separate wait followed by a bulk read.
+// [row * pitch + c], INF words per thread at a time: every thread re-reads only its words whose
+// tag does not match yet, all of them in flight together, until none is left (or the spin
+// budget runs out).  A consumer that arrives when the producers are about done pays one round
+// trip per poll, and data that is already there costs one round trip per INF words a thread.
+template <int INF>
 __device__ __forceinline__ bool stage_poll(const uint64_t* src, int rows, int width, size_t stride, uint32_t tag,
                                            uint16_t* hi, uint16_t* lo, int pitch, uint32_t* err) {
   const int q = kT / width, rm = kT % width;
   int row = (int)threadIdx.x / width, col = (int)threadIdx.x % width;
   bool ok = true;
-  for (int base = 0; base < rows * width; base += kT * kInflight) {
-    int rr[kInflight], cc[kInflight];
+  for (int base = 0; base < rows * width; base += kT * INF) {
+    int rc[INF];   // row << 16 | column (rows <= 16, columns < 2^16)
     uint32_t pend = 0;
 #pragma unroll
-    for (int m = 0; m < kInflight; ++m) {
-      rr[m] = row;
-      cc[m] = col;
+    for (int m = 0; m < INF; ++m) {
+      rc[m] = (row << 16) | col;
       if (row < rows) pend |= 1u << m;
       col += rm;
       row += q;
@@ -349,13 +306,14 @@ __device__ __forceinline__ bool stage_poll(const uint64_t* src, int rows, int wi
       }
     }
     for (long sp = 0; pend; ++sp) {
-      uint64_t v[kInflight];
+      uint64_t v[INF];
 #pragma unroll
-      for (int m = 0; m < kInflight; ++m) v[m] = (pend >> m) & 1u ? ld64(src + (size_t)rr[m] * stride + cc[m]) : 0ull;
+      for (int m = 0; m < INF; ++m)
+        v[m] = (pend >> m) & 1u ? ld64(src + (size_t)(rc[m] >> 16) * stride + (rc[m] & 0xffff)) : 0ull;
 #pragma unroll
-      for (int m = 0; m < kInflight; ++m) {
+      for (int m = 0; m < INF; ++m) {
         if (((pend >> m) & 1u) && (uint32_t)(v[m] >> 32) == tag) {
-          put_split(hi, lo, rr[m] * pitch + cc[m], (uint32_t)v[m]);
+          put_split(hi, lo, (rc[m] >> 16) * pitch + (rc[m] & 0xffff), (uint32_t)v[m]);
           pend &= ~(1u << m);
         }
       }
@@ -446,6 +404,7 @@ template <int KK, typename LT, bool PRIOR, bool NARROW, bool MARKOV, bool SAMPLE
 __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr int TPW = kOps / KK;   // AGPR tiles per wave
+  constexpr int kInf = kInflight;   // hand-off loads in flight per thread
   // At most 4 sequences use at most 4 of an MFMA's 16 A rows, so the hi and lo halves of rho
   // share one operand (rows 0..3 hi, 4..7 lo): one MFMA chain per tile instead of two.  The
   // two halves' products are summed when the tile is folded, in the same order as before.
@@ -544,14 +503,14 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     __syncthreads();
     bool ok = true;
     if (tid < G) {
-      for (int b0 = 0; b0 < batch; b0 += kInflight) {
-        uint64_t v[kInflight];
+      for (int b0 = 0; b0 < batch; b0 += kInf) {
+        uint64_t v[kInf];
 #pragma unroll
-        for (int m = 0; m < kInflight; ++m)
+        for (int m = 0; m < kInf; ++m)
           v[m] = b0 + m < batch ? ld64(kp + (size_t)(b0 + m) * G + tid) : 0ull;
         uint32_t bad = 0;
 #pragma unroll
-        for (int m = 0; m < kInflight; ++m) {
+        for (int m = 0; m < kInf; ++m) {
           if (b0 + m < batch) {
             if ((uint32_t)(v[m] & 0xffu) == tag8) atomicMax((unsigned long long*)&s_best[b0 + m], v[m]);
             else bad |= 1u << m;
@@ -681,10 +640,27 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         const uint64_t* hsrc = hnew + (size_t)mt * 16 * H;
         bool ok = true;
         f32x4_t racc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        // W_hh h_{j+1} accumulates here too: with several K chunks (wide batches) each staged
+        // chunk serves both products, instead of being staged again after rho is out
+        const bool chunked = HC < H;
+        const bool with_gh = j + 1 < Bk;
+        f32x4_t g0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, g1 = g0, g2 = g0;   // gates r, z, n
+        auto gh_chunk = [&](int k0) __attribute__((always_inline)) {
+          for (int kk = wave; kk < HC / 32; kk += 4) {
+            uint4 ahi, alo;
+            plane_operand(s_hi, s_lo, pitch, nb, n16, g4, 32 * kk, ahi, alo);
+            const uint4 b0 = s_whh[(0 * KKH + k0 / 32 + kk) * 64 + lane];
+            const uint4 b1 = s_whh[(1 * KKH + k0 / 32 + kk) * 64 + lane];
+            const uint4 b2 = s_whh[(2 * KKH + k0 / 32 + kk) * 64 + lane];
+            g0 = mfma_vv(alo, b0, mfma_vv(ahi, b0, g0));
+            g1 = mfma_vv(alo, b1, mfma_vv(ahi, b1, g1));
+            g2 = mfma_vv(alo, b2, mfma_vv(ahi, b2, g2));
+          }
+        };
         for (int k0 = 0; k0 < H; k0 += HC) {
           if (k0) __syncthreads();
           // the other GRU workgroups publish h at about the same time: poll the words directly
-          ok &= stage_poll(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
+          ok &= stage_poll<kInf>(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
           __syncthreads();
           for (int kk = wave; kk < HC / 32; kk += 4) {
             uint4 ahi, alo;
@@ -694,6 +670,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
             racc = mfma_vv(ahi, bw, racc);
             racc = mfma_vv(alo, bw, racc);
           }
+          if (chunked && with_gh) gh_chunk(k0);
         }
         if (n16 < rpg) s_rred[(wave * 4 + g4) * rpg + n16] = racc;
         if (fail_barrier(!ok, s_fail)) return;
@@ -710,28 +687,12 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
             }
           }
         }
-        if (j + 1 < Bk) {
-          f32x4_t gacc[3];
-          for (int q = 0; q < 3; ++q) gacc[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-          for (int k0 = 0; k0 < H; k0 += HC) {
-            if (HC < H) {   // several chunks: stage each again (all of h is there by now)
-              __syncthreads();
-              ok &= stage_split(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
-              __syncthreads();
-            }
-            for (int kk = wave; kk < HC / 32; kk += 4) {
-              uint4 ahi, alo;
-              plane_operand(s_hi, s_lo, pitch, nb, n16, g4, 32 * kk, ahi, alo);
-#pragma unroll
-              for (int q = 0; q < 3; ++q) {
-                const uint4 bh = s_whh[(q * KKH + k0 / 32 + kk) * 64 + lane];
-                gacc[q] = mfma_vv(ahi, bh, gacc[q]);
-                gacc[q] = mfma_vv(alo, bh, gacc[q]);
-              }
-            }
-          }
+        if (with_gh) {
+          if (!chunked) gh_chunk(0);   // one chunk: after rho is out, from the same staged h
           __syncthreads();   // planes read: their space takes the partial sums
-          for (int q = 0; q < 3; ++q) s_red[(wave * 3 + q) * 64 + lane] = gacc[q];
+          s_red[(wave * 3 + 0) * 64 + lane] = g0;
+          s_red[(wave * 3 + 1) * 64 + lane] = g1;
+          s_red[(wave * 3 + 2) * 64 + lane] = g2;
           __syncthreads();
           if (wave == 0) {
             float* gh = s_gh + mt * 16 * 48;
@@ -801,7 +762,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         // GRU workgroups come here after W_hh h, when rho is about complete: they poll the words
         // directly; the others wait (gently) for the first producer, then poll
         if (!gru) wait_any_producer(rsrc, (size_t)rpg, a.NG, tag, err);
-        const bool ok = stage_poll(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err);
+        const bool ok = stage_poll<kInf>(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err);
         if (fail_barrier(!ok, s_fail)) return;
         if (PACK) {
           // rows 0..3 of the A operand carry the hi halves of slots 0..3, rows 4..7 the lo
