@@ -724,21 +724,44 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     // ======================= vocabulary head + fused combine (all workgroups) =======================
     for (int mt = 0; mt < mtiles; ++mt) {
       const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
-      // long logits of the owned rows (independent of rho: in flight while rho is awaited)
-      for (int slot = 0; slot < nb; ++slot) {
-        const LT* src = L + ((size_t)(mt * 16 + slot) * Bk + j) * V + v_base;
-        LT* dst = s_ll + (size_t)slot * a.rows_max;
-        for (int r0 = 0; r0 < nrows; r0 += 4 * kT) {
-          LT x[4];
+      // long logits of the owned rows (independent of rho: in flight while rho is awaited).
+      // Wide batches: 16 values per thread in flight, over [slot][row] flattened (element
+      // 256 m + tid of a group), so that 16 slots cost a few round trips rather than one each
+      if (NARROW) {
+        for (int slot = 0; slot < nb; ++slot) {
+          const LT* src = L + ((size_t)(mt * 16 + slot) * Bk + j) * V + v_base;
+          LT* dst = s_ll + (size_t)slot * a.rows_max;
+          for (int r0 = 0; r0 < nrows; r0 += 4 * kT) {
+            LT x[4];
 #pragma unroll
-          for (int m = 0; m < 4; ++m) {
-            const int row = r0 + m * kT + tid;
-            x[m] = (row < nrows && v_base + row < V) ? src[row] : LT(0);
+            for (int m = 0; m < 4; ++m) {
+              const int row = r0 + m * kT + tid;
+              x[m] = (row < nrows && v_base + row < V) ? src[row] : LT(0);
+            }
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+              const int row = r0 + m * kT + tid;
+              if (row < nrows) dst[row] = x[m];
+            }
+          }
+        }
+      } else if (nrows > 0) {
+        int sl = 0, rw = tid;   // this thread's first element of the group
+        while (sl < nb && rw >= nrows) { rw -= nrows; ++sl; }
+        while (sl < nb) {
+          LT x[16];
+          int s2 = sl, r2 = rw;
+#pragma unroll
+          for (int m = 0; m < 16; ++m) {
+            x[m] = (s2 < nb && v_base + r2 < V) ? L[((size_t)(mt * 16 + s2) * Bk + j) * V + v_base + r2] : LT(0);
+            r2 += kT;
+            while (s2 < nb && r2 >= nrows) { r2 -= nrows; ++s2; }
           }
 #pragma unroll
-          for (int m = 0; m < 4; ++m) {
-            const int row = r0 + m * kT + tid;
-            if (row < nrows) dst[row] = x[m];
+          for (int m = 0; m < 16; ++m) {
+            if (sl < nb) s_ll[(size_t)sl * a.rows_max + rw] = x[m];
+            rw += kT;
+            while (sl < nb && rw >= nrows) { rw -= nrows; ++sl; }
           }
         }
       }
