@@ -157,6 +157,22 @@ def test_persistent_small(shape, literal):
     assert rep["fusion_active"] > 0.2
 
 
+EXTREME = [
+    dict(V=4099, d=64, H=128, r=128, Bk=64, batch=3),     # the longest block (64 positions)
+    dict(V=1031, d=64, H=128, r=128, Bk=64, batch=64),    # the largest batch with the longest block
+    dict(V=2053, d=64, H=128, r=128, Bk=1, batch=5),      # a single position
+]
+
+
+@pytest.mark.parametrize("shape", range(len(EXTREME)))
+def test_persistent_extreme_block_sizes(shape):
+    sh = EXTREME[shape]
+    p = _problem("qwen3-8b-b16", "stress", dtype="bf16", **sh)
+    seqs = sorted({0, sh["batch"] // 2, sh["batch"] - 1})
+    _check(p, 0.6, prepared=True, sequences=seqs)
+    _check(p, 0.6, 0.4, with_prior=True, literal=True, prepared=True, sequences=seqs[:1])
+
+
 @pytest.mark.parametrize("shape", [0, 3])
 def test_persistent_small_prior(shape):
     p = _problem("qwen3-8b-b16", "stress", dtype="bf16", **SMALL[shape])
