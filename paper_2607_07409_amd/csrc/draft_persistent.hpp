@@ -40,8 +40,7 @@ constexpr int kT = 256;          // threads per workgroup (one wave per SIMD)
 constexpr int kOps = 56;         // MFMA B operands of 16 bytes per lane held in AGPRs (224 of
                                  // the 256; the rest take the accumulators)
 constexpr long kMaxSpins = 1L << 22;
-constexpr int kInflight = 8;     // hand-off loads a thread issues before checking any of them
-                                 // (twice as many for batches of more than 4 sequences)
+constexpr int kInflight = 8;     // 16-byte hand-off loads a thread issues before checking any of them
 constexpr int kStageK = 256;     // K chunk of staged hand-off values (16 slots x 256 floats in LDS)
 constexpr int kStatWords = 9;    // tagged words of one published partial
 constexpr int kRhoCopies = 8;    // replicas of the published rank vector (spreads the readers)
@@ -63,6 +62,24 @@ __device__ __forceinline__ void stf(float* p, float v) {
 }
 __device__ __forceinline__ float ldf(const float* p) {
   return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Agent-coherent 16-byte loads (the cache policy of ld64: sc1) through a buffer resource over
+// `bytes` bytes from `base`; offsets past the end read as zeros.  A 16-byte aligned load lies
+// within one cache line: each of its two 64-bit words is read whole, as by ld64.  Polling loops
+// put a compiler barrier (poll_fence) before each round, so that every round loads again.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t coherent_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ u32x4 ld128(__amdgpu_buffer_rsrc_t rs, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 16);   // sc1
+}
+__device__ __forceinline__ void poll_fence() { asm volatile("" ::: "memory"); }
+// the thread index, recomputed where it is used: values derived from it are not hoisted out of
+// the drafting loop and kept live across it (the wide kernels have no registers to spare)
+__device__ __forceinline__ int local_tid() {
+  int t = (int)threadIdx.x;
+  asm volatile("" : "+v"(t));
+  return t;
 }
 // all earlier vector-memory operations of this wave have completed
 __device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
@@ -281,12 +298,14 @@ __device__ __forceinline__ void put_split(uint16_t* hi, uint16_t* lo, int idx, u
 }
 
 // Stage rows x width tagged words (row stride `stride` words) into the operand planes at
-// [row * pitch + c], INF words per thread at a time: every thread re-reads only its words whose
-// tag does not match yet, all of them in flight together, until none is left (or the spin
-// budget runs out).  A consumer that arrives when the producers are about done pays one round
-// trip per poll, and data that is already there costs one round trip per INF words a thread.
+// [row * pitch + c], one word per load and INF words per thread at a time: every thread
+// re-reads only its words whose tag does not match yet, all of them in flight together, until
+// none is left (or the spin budget runs out).  A consumer that arrives when the producers are
+// about done pays one round trip per poll, and data that is already there costs one round trip
+// per INF words a thread.  Used for narrow batches, where a round or two covers the hand-off
+// and 8-byte loads spread over all threads arrive sooner than half as many 16-byte loads.
 template <int INF>
-__device__ __forceinline__ bool stage_poll(const uint64_t* src, int rows, int width, size_t stride, uint32_t tag,
+__device__ __forceinline__ bool stage_poll_words(const uint64_t* src, int rows, int width, size_t stride, uint32_t tag,
                                            uint16_t* hi, uint16_t* lo, int pitch, uint32_t* err) {
   const int q = kT / width, rm = kT % width;
   int row = (int)threadIdx.x / width, col = (int)threadIdx.x % width;
@@ -314,6 +333,71 @@ __device__ __forceinline__ bool stage_poll(const uint64_t* src, int rows, int wi
       for (int m = 0; m < INF; ++m) {
         if (((pend >> m) & 1u) && (uint32_t)(v[m] >> 32) == tag) {
           put_split(hi, lo, (rc[m] >> 16) * pitch + (rc[m] & 0xffff), (uint32_t)v[m]);
+          pend &= ~(1u << m);
+        }
+      }
+      if (!pend) break;
+      __builtin_amdgcn_s_sleep(2);
+      if ((sp & 63) == 63 && ld32(err)) {
+        ok = false;
+        break;
+      }
+      if (sp > kMaxSpins) {
+        st32(err, 1u);
+        ok = false;
+        break;
+      }
+    }
+  }
+  return ok;
+}
+
+// two staged values (an even index): their bf16 hi and lo halves
+__device__ __forceinline__ void put_split2(uint16_t* hi, uint16_t* lo, int idx, uint32_t b0, uint32_t b1) {
+  uint32_t h, l;
+  split_pair(__uint_as_float(b0), __uint_as_float(b1), h, l);
+  *(uint32_t*)(hi + idx) = h;
+  *(uint32_t*)(lo + idx) = l;
+}
+
+// As stage_poll_words, two adjacent words per 16-byte load (width, stride and the word offset
+// of src even, src 16-byte aligned), INF loads per thread at a time: data that is already there
+// costs one round trip per 2 INF words a thread.  Used for wide batches, whose hand-offs are
+// 16 to 64 times larger.
+template <int INF>
+__device__ __forceinline__ bool stage_poll_pairs(const uint64_t* src, int rows, int width, int stride, uint32_t tag,
+                                           uint16_t* hi, uint16_t* lo, int pitch, uint32_t* err) {
+  const int wp = width >> 1;   // pairs per row
+  const __amdgpu_buffer_rsrc_t rs = coherent_rsrc(src, (uint32_t)(((size_t)(rows - 1) * stride + width) * 8));
+  const int q = kT / wp, rm = kT % wp;
+  const int t = local_tid();
+  int row = t / wp, col = t % wp;
+  bool ok = true;
+  for (int base = 0; base < rows * wp; base += kT * INF) {
+    int rc[INF];   // row << 16 | pair column (rows <= 16, columns < 2^16)
+    uint32_t pend = 0;
+#pragma unroll
+    for (int m = 0; m < INF; ++m) {
+      rc[m] = (row << 16) | col;
+      if (row < rows) pend |= 1u << m;
+      col += rm;
+      row += q;
+      if (col >= wp) {
+        col -= wp;
+        ++row;
+      }
+    }
+    for (long sp = 0; pend; ++sp) {
+      poll_fence();
+      u32x4 v[INF];
+#pragma unroll
+      for (int m = 0; m < INF; ++m)
+        v[m] = (pend >> m) & 1u ? ld128(rs, (uint32_t)(((rc[m] >> 16) * stride + 2 * (rc[m] & 0xffff)) * 8))
+                                : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int m = 0; m < INF; ++m) {
+        if (((pend >> m) & 1u) && v[m].y == tag && v[m].w == tag) {
+          put_split2(hi, lo, (rc[m] >> 16) * pitch + 2 * (rc[m] & 0xffff), v[m].x, v[m].z);
           pend &= ~(1u << m);
         }
       }
@@ -419,7 +503,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   const uint32_t epoch_full = ld32(a.hdr);
   const uint32_t epoch = epoch_full & 0xffffffu;
   const int set = (int)(epoch & 1u);
-  const size_t kstride = (size_t)kMaxBatch * G;       // one (set, parity) plane of keys
+  const int Gp = (G + 1) & ~1;                         // key row stride: even, for 16-byte loads of pairs
+  const size_t kstride = (size_t)kMaxBatch * Gp;      // one (set, parity) plane of keys
 
   int t0, nt;
   persist_tile_range(w, G, a.NG, a.NT, a.cap_a, &t0, &nt);
@@ -463,7 +548,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   // ---- clear this workgroup's key slots of the other set (read by the next call)
   for (int i = tid; i < 2 * kMaxBatch; i += kT) {
     const int par = i / kMaxBatch, b = i % kMaxBatch;
-    st64(a.keys + (size_t)(1 - set) * 2 * kstride + par * kstride + (size_t)b * G + w, 0ull);
+    st64(a.keys + (size_t)(1 - set) * 2 * kstride + par * kstride + (size_t)b * Gp + w, 0ull);
   }
 
   // ---- resident weights
@@ -494,34 +579,84 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   const LT* L = (const LT*)a.L;
   const float wl = a.wl;
 
-  // Tokens of position jm (the argmax keys of all workgroups, max-reduced through LDS atomics)
-  // into s_tok; workgroup 0 also writes the drafted tokens.  Workgroup-uniform result.
+  // Tokens of position jm (the argmax keys of all workgroups) into s_tok; workgroup 0 also
+  // writes the drafted tokens.  Narrow batches: thread t loads the keys of workgroup t and
+  // max-reduces them through LDS atomics.  Wide batches: wave v merges sequences v, v + 4, ...;
+  // each lane loads the key pairs (workgroups 2c, 2c + 1) c = lane and lane + 64 of a sequence
+  // with 16-byte loads, four sequences per round, and the wave reduces them with DPP (256
+  // atomics on one LDS word per sequence would serialise).  Workgroup-uniform result.
   auto merge_position = [&](int jm) -> bool {
     const uint32_t tag8 = (uint32_t)(jm + 1);
     const uint64_t* kp = a.keys + (size_t)set * 2 * kstride + (size_t)(jm & 1) * kstride;
-    for (int b = tid; b < batch; b += kT) s_best[b] = 0ull;
-    __syncthreads();
     bool ok = true;
-    if (tid < G) {
-      for (int b0 = 0; b0 < batch; b0 += kInf) {
-        uint64_t v[kInf];
+    if (NARROW) {
+      for (int b = tid; b < batch; b += kT) s_best[b] = 0ull;
+      __syncthreads();
+      if (tid < G) {
+        uint64_t v[4];
 #pragma unroll
-        for (int m = 0; m < kInf; ++m)
-          v[m] = b0 + m < batch ? ld64(kp + (size_t)(b0 + m) * G + tid) : 0ull;
-        uint32_t bad = 0;
+        for (int m = 0; m < 4; ++m) v[m] = m < batch ? ld64(kp + (size_t)m * Gp + tid) : 0ull;
 #pragma unroll
-        for (int m = 0; m < kInf; ++m) {
-          if (b0 + m < batch) {
-            if ((uint32_t)(v[m] & 0xffu) == tag8) atomicMax((unsigned long long*)&s_best[b0 + m], v[m]);
-            else bad |= 1u << m;
+        for (int m = 0; m < 4; ++m) {
+          if (m < batch) {
+            if ((uint32_t)(v[m] & 0xffu) != tag8) ok &= wait_key(kp + (size_t)m * Gp + tid, tag8, err, v[m]);
+            atomicMax((unsigned long long*)&s_best[m], v[m]);
           }
         }
-#pragma unroll 1
-        for (int m = 0; bad; ++m, bad >>= 1) {
-          if (bad & 1u) {
-            uint64_t k;
-            ok &= wait_key(kp + (size_t)(b0 + m) * G + tid, tag8, err, k);
-            atomicMax((unsigned long long*)&s_best[b0 + m], k);
+      }
+    } else {
+      const __amdgpu_buffer_rsrc_t rs = coherent_rsrc(kp, (uint32_t)((size_t)batch * Gp * 8));
+      constexpr int SPR = kInf / 2;   // sequences per round (two loads each)
+      const int lane = local_tid() & 63;
+      for (int b0 = wave; b0 < batch; b0 += 4 * SPR) {   // wave-uniform
+        uint32_t pend = 0;
+#pragma unroll
+        for (int m = 0; m < kInf; ++m) {
+          const int b = b0 + 4 * (m >> 1), c = lane + 64 * (m & 1);
+          if (b < batch && 2 * c < G) pend |= 1u << m;
+        }
+        uint64_t best[SPR];
+#pragma unroll
+        for (int k = 0; k < SPR; ++k) best[k] = 0ull;
+        for (long sp = 0; pend; ++sp) {
+          poll_fence();
+          u32x4 v[kInf];
+#pragma unroll
+          for (int m = 0; m < kInf; ++m) {
+            const int b = b0 + 4 * (m >> 1), c = lane + 64 * (m & 1);
+            v[m] = (pend >> m) & 1u ? ld128(rs, (uint32_t)(((size_t)b * Gp + 2 * c) * 8)) : u32x4{0u, 0u, 0u, 0u};
+          }
+#pragma unroll
+          for (int m = 0; m < kInf; ++m) {
+            if ((pend >> m) & 1u) {
+              const int c = lane + 64 * (m & 1);
+              const bool has1 = 2 * c + 1 < G;   // the pad column of an odd grid is never written
+              if ((v[m].x & 0xffu) == tag8 && (!has1 || (v[m].z & 0xffu) == tag8)) {
+                const uint64_t k0 = ((uint64_t)v[m].y << 32) | v[m].x;
+                const uint64_t k1 = has1 ? ((uint64_t)v[m].w << 32) | v[m].z : 0ull;
+                best[m >> 1] = key_max(best[m >> 1], key_max(k0, k1));
+                pend &= ~(1u << m);
+              }
+            }
+          }
+          if (!pend) break;
+          __builtin_amdgcn_s_sleep(2);
+          if ((sp & 63) == 63 && ld32(err)) {
+            ok = false;
+            break;
+          }
+          if (sp > kMaxSpins) {
+            st32(err, 1u);
+            ok = false;
+            break;
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < SPR; ++k) {
+          const int b = b0 + 4 * k;
+          if (b < batch) {   // wave-uniform
+            const uint64_t kb = wave_key_max(best[k]);
+            if (lane == 0) s_best[b] = kb;
           }
         }
       }
@@ -581,24 +716,36 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         }
         __syncthreads();
       }
-      // gates of the owned units: gi = T[u] (folded input projection), gh from the previous step
-      for (int mt = 0; mt < mtiles; ++mt) {
-        const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
+      // gates of the owned units: gi = T[u] (folded input projection) for all sequences at once,
+      // 16-byte loads; gh from the previous step.  Wave m computes the gates of M tile m.
+      {
+        const int mt = wave;
+        const int nb = mt < mtiles ? (batch - mt * 16 < 16 ? batch - mt * 16 : 16) : 0;
         uint64_t hv[4];   // the owned units' previous state, in flight together with the gather
-        if (wave == 0) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            hv[i] = (hs > 0 && 4 * g4 + i < nb) ? ld64(hprev + (size_t)(mt * 16 + 4 * g4 + i) * H + 16 * w + n16)
-                                                 : 0ull;
-        }
-        // with statistics of the previous position pending, wave 3 publishes them while the
-        // other waves gather (the gather is latency-bound; wave 3 loads nothing until the
-        // rank stage, so its stores delay no load of its own)
+        for (int i = 0; i < 4; ++i)
+          hv[i] = (hs > 0 && 4 * g4 + i < nb) ? ld64(hprev + (size_t)(mt * 16 + 4 * g4 + i) * H + 16 * w + n16)
+                                               : 0ull;
+        // with statistics of the previous position pending (one M tile), wave 3 publishes them
+        // while the other waves gather (the gather is latency-bound; wave 3 loads nothing until
+        // the rank stage, so its stores delay no load of its own)
         const int gthreads = pending_stats >= 0 ? 192 : kT;
+        const int ngi = batch * 12;   // (sequence, gate, 4 units) loads
         if (tid < gthreads) {
-          for (int i = tid; i < 16 * 48; i += gthreads) {
-            const int slot = i / 48, q = (i % 48) / 16, u = i % 16;
-            s_gi[i] = slot < nb ? a.T[(size_t)s_tok[mt * 16 + slot] * 3 * H + q * H + 16 * w + u] : 0.f;
+          for (int i0 = local_tid(); i0 < ngi; i0 += 4 * gthreads) {
+            f32x4_t x[4];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+              const int i = i0 + m * gthreads;
+              const int slot = i / 12, q = (i % 12) >> 2, u4 = i & 3;
+              x[m] = i < ngi ? *(const f32x4_t*)(a.T + (size_t)s_tok[slot] * 3 * H + q * H + 16 * w + 4 * u4)
+                             : f32x4_t{0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+              const int i = i0 + m * gthreads;
+              if (i < ngi) *(f32x4_t*)(s_gi + (i / 12) * 48 + ((i % 12) >> 2) * 16 + 4 * (i & 3)) = x[m];
+            }
           }
         } else {
           publish_stats(pending_stats, 0, batch, 3);
@@ -606,7 +753,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         pending_stats = -1;
         __syncthreads();
         bool ok = true;
-        if (wave == 0) {
+        if (nb > 0) {   // wave-uniform
           const float* gh = s_gh + mt * 16 * 48;
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
@@ -621,7 +768,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
                 ghz = gh[slot * 48 + 16 + n16];
                 ghn = gh[slot * 48 + 32 + n16];
               }
-              const float* gi = s_gi + slot * 48;
+              const float* gi = s_gi + bb * 48;
               const float rg = sigm(gi[n16] + ghr);
               const float zg = sigm(gi[16 + n16] + ghz);
               const float ng = tanhf_(gi[32 + n16] + rg * ghn);
@@ -660,7 +807,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         for (int k0 = 0; k0 < H; k0 += HC) {
           if (k0) __syncthreads();
           // the other GRU workgroups publish h at about the same time: poll the words directly
-          ok &= stage_poll<kInf>(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
+          ok &= NARROW ? stage_poll_words<kInf>(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err)
+                       : stage_poll_pairs<kInf>(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
           __syncthreads();
           for (int kk = wave; kk < HC / 32; kk += 4) {
             uint4 ahi, alo;
@@ -725,8 +873,9 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     for (int mt = 0; mt < mtiles; ++mt) {
       const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
       // long logits of the owned rows (independent of rho: in flight while rho is awaited).
-      // Wide batches: 16 values per thread in flight, over [slot][row] flattened (element
-      // 256 m + tid of a group), so that 16 slots cost a few round trips rather than one each
+      // Wide batches: 16-byte loads over [slot][row] flattened, eight per thread in flight, so
+      // that 16 slots cost a round trip or two rather than one each
+      constexpr int EPI = 16 / (int)sizeof(LT);   // long logits per 16-byte load
       if (NARROW) {
         for (int slot = 0; slot < nb; ++slot) {
           const LT* src = L + ((size_t)(mt * 16 + slot) * Bk + j) * V + v_base;
@@ -743,6 +892,29 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
               const int row = r0 + m * kT + tid;
               if (row < nrows) dst[row] = x[m];
             }
+          }
+        }
+      } else if (nrows > 0 && V % EPI == 0) {
+        // every 16-byte piece lies wholly inside or wholly past the vocabulary (V and v_base are
+        // multiples of EPI); rows past V are stored as zeros and never folded
+        const int ipr = nrows / EPI;                                   // pieces per slot
+        const int nvalid = (V - v_base < nrows ? V - v_base : nrows) / EPI;
+        const int n = nb * ipr;
+        for (int i0 = local_tid(); i0 < n; i0 += 8 * kT) {
+          uint4 x[8];
+#pragma unroll
+          for (int m = 0; m < 8; ++m) {
+            const int i = i0 + m * kT;
+            const int sl = i / ipr, c = i - sl * ipr;
+            x[m] = (i < n && c < nvalid)
+                       ? *(const uint4*)(L + ((size_t)(mt * 16 + sl) * Bk + j) * V + v_base + EPI * c)
+                       : make_uint4(0u, 0u, 0u, 0u);
+          }
+#pragma unroll
+          for (int m = 0; m < 8; ++m) {
+            const int i = i0 + m * kT;
+            const int sl = i / ipr, c = i - sl * ipr;
+            if (i < n) *(uint4*)(s_ll + (size_t)sl * a.rows_max + EPI * c) = x[m];
           }
         }
       } else if (nrows > 0) {
@@ -785,7 +957,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         // GRU workgroups come here after W_hh h, when rho is about complete: they poll the words
         // directly; the others wait (gently) for the first producer, then poll
         if (!gru) wait_any_producer(rsrc, (size_t)rpg, a.NG, tag, err);
-        const bool ok = stage_poll<kInf>(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err);
+        const bool ok = NARROW ? stage_poll_words<kInf>(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err)
+                               : stage_poll_pairs<kInf>(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err);
         if (fail_barrier(!ok, s_fail)) return;
         if (PACK) {
           // rows 0..3 of the A operand carry the hi halves of slots 0..3, rows 4..7 the lo
@@ -881,7 +1054,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       };
 
       auto fold_tile = [&](const f32x4_t& acc, int lt) {
-        const int row = 16 * lt + n16;
+        const int row = 16 * lt + (local_tid() & 15);
         const int v = v_base + row;
         const bool vin = v < V;
         float gz[4] = {0.f, 0.f, 0.f, 0.f};
@@ -1002,7 +1175,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       if (tid < nb) {
         uint64_t k = s_wkey[tid];
         for (int q = 1; q < 4; ++q) k = key_max(k, s_wkey[q * 16 + tid]);
-        st64(a.keys + (size_t)set * 2 * kstride + par * kstride + (size_t)(mt * 16 + tid) * G + w, k);
+        st64(a.keys + (size_t)set * 2 * kstride + par * kstride + (size_t)(mt * 16 + tid) * Gp + w, k);
       }
       // the full partials (LSEs, top-2) for the row statistics: off the critical path
       if (a.out_stats) {
