@@ -190,6 +190,19 @@ __device__ __forceinline__ void lse_push(Lse& a, float x) {
   a.m = up ? x : a.m;
 }
 
+// lse_push for a running maximum that starts finite (kFinMin instead of -inf): no test of the
+// value is needed, since x = -inf gives d = -inf, a zero term and no new maximum.  Such a
+// state is empty while s == 0 (a push sets s >= 1); fin_to_empty restores the -inf form.
+constexpr float kFinMin = -3.0e38f;
+__device__ __forceinline__ void lse_push_fin(Lse& a, float x) {
+  const float d = x - a.m;
+  const float e = fast_exp2(-fabsf(d) * kLog2e);
+  const bool up = d > 0.f;
+  a.s = up ? __builtin_fmaf(a.s, e, 1.0f) : a.s + e;
+  a.m = up ? x : a.m;
+}
+__device__ __forceinline__ void fin_to_empty(Lse& a) { a.m = a.s > 0.f ? a.m : -INFINITY; }
+
 // value of the lane N places further along in the same row of 16 lanes (DPP row rotate)
 template <int N>
 __device__ __forceinline__ float row_ror(float v) {
@@ -990,7 +1003,10 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
 
       Partial P[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) P[i] = partial_empty();
+      for (int i = 0; i < 4; ++i) {
+        P[i] = partial_empty();
+        if (!NARROW) P[i].L.m = P[i].S.m = P[i].F.m = kFinMin;   // the wide fold's finite start
+      }
 
       // the fused value f of an entry: greedy decoding ranks f; sampling folds f / T into the
       // log-sum-exp and ranks f / T + g (Gumbel-max), g the entry's noise
@@ -1053,30 +1069,32 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         }
       };
 
+      // wide batches: lane (row n16, group g4) folds slots 4 g4 + i of one row.  Entries past the
+      // batch or the vocabulary enter as -inf (no term, no maximum, no top-2 change) rather than
+      // behind per-lane branches.
       auto fold_tile = [&](const f32x4_t& acc, int lt) {
         const int row = 16 * lt + (local_tid() & 15);
         const int v = v_base + row;
         const bool vin = v < V;
+        // the long-only first row of the literal schedule: no head term, no prior, no short sum
+        const float alx = long_only ? 0.f : al, bex = long_only ? 0.f : be;
         float gz[4] = {0.f, 0.f, 0.f, 0.f};
         if (SAMPLE) gumbel_quad(a.smp, mt * 16 + 4 * g4, j, v, nb, gz);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int slot = 4 * g4 + i;
           if (i < nb) {   // uniform: skips slot sets no lane holds
-            if (slot < nb && vin) {
-              const float x = to_f32(s_ll[slot * a.rows_max + row]);
-              float f;
-              if (long_only) {
-                f = wl * x;
-              } else {
-                const float s = acc[i];
-                f = __builtin_fmaf(al, s, wl * x);
-                if (PRIOR) f = __builtin_fmaf(-be, s_prior[row], f);
-                lse_push(P[i].S, s);
-              }
-              lse_push(P[i].L, x);
-              fold_fused(P[i], f, gz[i], v);
-            }
+            const bool ok = slot < nb && vin;
+            const float xr = to_f32(s_ll[(ok ? slot : 0) * a.rows_max + row]);
+            const float x = ok ? xr : -INFINITY;
+            float f = __builtin_fmaf(alx, acc[i], wl * x);
+            if (PRIOR) f = __builtin_fmaf(-bex, s_prior[row], f);
+            f = ok ? f : -INFINITY;
+            lse_push_fin(P[i].S, ok && !long_only ? acc[i] : -INFINITY);
+            lse_push_fin(P[i].L, x);
+            if (SAMPLE) f *= a.smp.inv_temp;
+            lse_push_fin(P[i].F, f);
+            top2_push(P[i], SAMPLE ? f + gz[i] : f, v);
           }
         }
       };
@@ -1182,6 +1200,11 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           if (i < nb) {
+            if (!NARROW) {
+              fin_to_empty(P[i].L);
+              fin_to_empty(P[i].S);
+              fin_to_empty(P[i].F);
+            }
             P[i] = allred_partial(P[i], RowRor<NARROW>{});   // over the row (narrow: the wave)
             if (narrow) {
               if (lane == 0) s_part[wave * 16 + i] = P[i];
