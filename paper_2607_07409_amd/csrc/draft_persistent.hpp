@@ -1005,21 +1005,9 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         P[i] = partial_empty();
-        if (!NARROW) P[i].L.m = P[i].S.m = P[i].F.m = kFinMin;   // the wide fold's finite start
+        P[i].L.m = P[i].S.m = P[i].F.m = kFinMin;   // the fold's finite start
       }
 
-      // the fused value f of an entry: greedy decoding ranks f; sampling folds f / T into the
-      // log-sum-exp and ranks f / T + g (Gumbel-max), g the entry's noise
-      auto fold_fused = [&](Partial& Q, float f, float g, int v) {
-        if (SAMPLE) {
-          f *= a.smp.inv_temp;
-          lse_push(Q.F, f);
-          top2_push(Q, f + g, v);
-        } else {
-          lse_push(Q.F, f);
-          top2_push(Q, f, v);
-        }
-      };
       // keep the useful rows of a tile's result at stash position tq (narrow: slots < nb of
       // lane group 0; wide: all 16 slots)
       auto stash = [&](const f32x4_t& acc, int tq) {
@@ -1039,39 +1027,40 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
             if (i < nb) s_stash[(tq * 4 + i) * 16 + n16] = acc[i];
         }
       };
-      // narrow: fold stashed tiles base + stride * tq (tq < ntile), lane group tq taking tile tq
+      // The fused value f of an entry: greedy decoding ranks f; sampling folds f / T into the
+      // log-sum-exp and ranks f / T + g (Gumbel-max), g the entry's noise.
+      // narrow: fold stashed tiles base + stride * tq (tq < ntile), lane group tq taking tile tq;
+      // lanes without an entry (past the vocabulary, or a group past ntile) fold -inf
       auto fold_narrow = [&](int base, int stride, int ntile) {
         float gz[4] = {0.f, 0.f, 0.f, 0.f};
         if (SAMPLE) gumbel_quad(a.smp, mt * 16, j, v_base + 16 * (base + stride * g4) + n16, nb, gz);
-        if (g4 < ntile) {
-          const int row = 16 * (base + stride * g4) + n16;
-          const int v = v_base + row;
-          if (v < V) {
+        const int row = 16 * (base + stride * g4) + (local_tid() & 15);
+        const int v = v_base + row;
+        const bool ok = g4 < ntile && v < V;
+        const int rowc = ok ? row : 0;   // an in-range LDS row for lanes without an entry
+        const float alx = long_only ? 0.f : al, bex = long_only ? 0.f : be;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              if (i < nb) {
-                const float x = to_f32(s_ll[i * a.rows_max + row]);
-                float f;
-                if (long_only) {
-                  f = wl * x;
-                } else {
-                  const float sv = PACK ? s_stash[(g4 * 4 + i) * 16 + n16] + s_stash[((4 + g4) * 4 + i) * 16 + n16]
-                                        : s_stash[(g4 * 4 + i) * 16 + n16];
-                  f = __builtin_fmaf(al, sv, wl * x);
-                  if (PRIOR) f = __builtin_fmaf(-be, s_prior[row], f);
-                  lse_push(P[i].S, sv);
-                }
-                lse_push(P[i].L, x);
-                fold_fused(P[i], f, gz[i], v);
-              }
-            }
+        for (int i = 0; i < 4; ++i) {
+          if (i < nb) {   // uniform
+            const float xr = to_f32(s_ll[i * a.rows_max + rowc]);
+            const float x = ok ? xr : -INFINITY;
+            const float sv = PACK ? s_stash[(g4 * 4 + i) * 16 + n16] + s_stash[((4 + g4) * 4 + i) * 16 + n16]
+                                  : s_stash[(g4 * 4 + i) * 16 + n16];
+            float f = __builtin_fmaf(alx, sv, wl * x);
+            if (PRIOR) f = __builtin_fmaf(-bex, s_prior[rowc], f);
+            f = ok ? f : -INFINITY;
+            lse_push_fin(P[i].S, ok && !long_only ? sv : -INFINITY);
+            lse_push_fin(P[i].L, x);
+            if (SAMPLE) f *= a.smp.inv_temp;
+            lse_push_fin(P[i].F, f);
+            top2_push(P[i], SAMPLE ? f + gz[i] : f, v);
           }
         }
       };
 
-      // wide batches: lane (row n16, group g4) folds slots 4 g4 + i of one row.  Entries past the
-      // batch or the vocabulary enter as -inf (no term, no maximum, no top-2 change) rather than
-      // behind per-lane branches.
+      // wide batches: lane (row n16, group g4) folds slots 4 g4 + i of one row.  As in the narrow
+      // fold, entries past the batch or the vocabulary enter as -inf (no term, no maximum, no
+      // top-2 change) rather than behind per-lane branches.
       auto fold_tile = [&](const f32x4_t& acc, int lt) {
         const int row = 16 * lt + (local_tid() & 15);
         const int v = v_base + row;
@@ -1200,11 +1189,9 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           if (i < nb) {
-            if (!NARROW) {
-              fin_to_empty(P[i].L);
-              fin_to_empty(P[i].S);
-              fin_to_empty(P[i].F);
-            }
+            fin_to_empty(P[i].L);
+            fin_to_empty(P[i].S);
+            fin_to_empty(P[i].F);
             P[i] = allred_partial(P[i], RowRor<NARROW>{});   // over the row (narrow: the wave)
             if (narrow) {
               if (lane == 0) s_part[wave * 16 + i] = P[i];
