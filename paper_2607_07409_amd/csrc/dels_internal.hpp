@@ -88,6 +88,9 @@ hipError_t launch_unigram_prior(const int32_t* tokens, int64_t n, int32_t V, flo
 constexpr int kMaxBatch = 64;              // sequences per call on the persistent path
 constexpr int kMaxG = 256;                 // workgroups (one per CU of a gfx950)
 constexpr size_t kMaxLds = 160 * 1024;     // LDS per CU on gfx950
+constexpr int kNarrowBatch = 4;            // the persistent kernel's narrow form: at most 4 sequences
+constexpr int kMaxH = 16 * kMaxG;          // GRU hidden units on the persistent path (16 per GRU workgroup)
+constexpr size_t kH32Set = (size_t)2 * kMaxBatch * kMaxH;   // words of one set of the wide h hand-off
 constexpr uint64_t kPreparedMagic = 0x50455250534c4544ull;
 
 struct PreparedHeader {
@@ -123,7 +126,9 @@ struct PersistArgs {
   dls_row_stats* out_stats;
   uint32_t* hdr;             // [0] call epoch, [1] error word
   uint64_t* keys;            // [2 sets][2 parities][kMaxBatch][G]
-  uint64_t* hbuf;            // [2 parities][batch][H]
+  uint64_t* hbuf;            // [2 parities][batch][H] (narrow batches)
+  uint32_t* h32;             // wide batches: [2 sets][2 parities][kMaxBatch][H] in a set stride of
+                             // kH32Set words; 24-bit h | 8-bit position tag
   uint64_t* rbuf;            // [replicas][2 parities][batch][r]
   uint64_t* stats;           // [B][batch][G][8] tagged LSE partials
 };
@@ -134,7 +139,7 @@ struct PersistPlan {
   size_t lds_region_a, lds;
 };
 struct PersistWorkspace {
-  size_t off_keys, off_h, off_rho, off_stats, total;
+  size_t off_keys, off_h, off_h32, off_rho, off_stats, total;
 };
 __host__ __device__ inline void persist_tile_range(int w, int G, int NG, int NT, int cap_a, int* t0, int* n);
 PersistPlan persist_plan(const dls_local_head& h, int32_t batch, int32_t B, dls_dtype long_dtype, bool prior, int G);

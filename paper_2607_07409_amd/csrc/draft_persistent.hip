@@ -73,6 +73,8 @@ PersistWorkspace persist_workspace(const dls_local_head& h, int32_t batch, int32
   o += (size_t)2 * 2 * kMaxBatch * kMaxG * 8;
   L.off_h = o;
   o += (size_t)2 * batch * h.H * 8;
+  L.off_h32 = o;
+  if (batch > kNarrowBatch) o += 2 * kH32Set * 4;
   L.off_rho = o;
   o += (size_t)kRhoCopies * 2 * batch * h.r * 8;
   L.off_stats = o;

@@ -430,6 +430,79 @@ __device__ __forceinline__ bool stage_poll_pairs(const uint64_t* src, int rows, 
   return ok;
 }
 
+// Wide batches hand h over as 32-bit words: the value rounded to 24 bits (sign, exponent, 15
+// mantissa bits) over an 8-bit position tag, so a 16-byte load carries four values.  The bf16
+// hi + lo split of such a value is exact (hi its top 16 bits, lo the remaining 8 significant
+// bits), as precise as the split of a full fp32 value into two round-to-nearest bf16 halves.
+__device__ __forceinline__ uint32_t pack_h24(float v, uint32_t tag8) {
+  const uint32_t u = __float_as_uint(v);
+  return ((u + 0x7fu + ((u >> 8) & 1u)) & 0xffffff00u) | tag8;
+}
+__device__ __forceinline__ void split_h24(uint32_t wd, uint32_t& hi, uint32_t& lo) {
+  const uint32_t x = wd & 0xffffff00u, h = wd & 0xffff0000u;
+  hi = h >> 16;
+  lo = __float_as_uint(__uint_as_float(x) - __uint_as_float(h)) >> 16;
+}
+__device__ __forceinline__ bool quad_tagged(const u32x4& q, uint32_t tag8) {
+  return ((q.x & 0xffu) == tag8) & ((q.y & 0xffu) == tag8) & ((q.z & 0xffu) == tag8) & ((q.w & 0xffu) == tag8);
+}
+// Load the 32-bit h words of rows < nb, columns [k0, k0 + HC) (half 0) and, with two, [k0 + HC,
+// k0 + 2 HC) (half 1) of a row-major [rows][stride] source, four words per 16-byte load: quad m
+// of a thread is item tid + 256 (m & 3) of half m >> 2 (row = item / (HC / 4)); at most 4 items
+// per thread and half (nb * HC <= 4096).  Polls until every loaded quad carries tag8.
+__device__ __forceinline__ bool poll_quads(const uint32_t* src, int nb, int HC, int stride, int k0, bool two,
+                                           uint32_t tag8, u32x4 (&qv)[8], uint32_t* err) {
+  const int qpr = HC >> 2;
+  const __amdgpu_buffer_rsrc_t rs = coherent_rsrc(src, (uint32_t)(((size_t)(nb - 1) * stride + k0 + (two ? 2 : 1) * HC) * 4));
+  const int t = local_tid();
+  uint32_t pend = 0;
+  uint32_t off[8];
+#pragma unroll
+  for (int m = 0; m < 8; ++m) {
+    const int i = t + kT * (m & 3), row = i / qpr, qc = i - row * qpr;
+    off[m] = (uint32_t)((row * stride + k0 + (m >> 2) * HC + 4 * qc) * 4);
+    if (row < nb && (m < 4 || two)) pend |= 1u << m;
+    qv[m] = u32x4{0u, 0u, 0u, 0u};
+  }
+  for (long sp = 0; pend; ++sp) {
+    poll_fence();
+#pragma unroll
+    for (int m = 0; m < 8; ++m)
+      if ((pend >> m) & 1u) qv[m] = ld128(rs, off[m]);
+#pragma unroll
+    for (int m = 0; m < 8; ++m)
+      if (((pend >> m) & 1u) && quad_tagged(qv[m], tag8)) pend &= ~(1u << m);
+    if (!pend) break;
+    __builtin_amdgcn_s_sleep(2);
+    if ((sp & 63) == 63 && ld32(err)) return false;
+    if (sp > kMaxSpins) {
+      st32(err, 1u);
+      return false;
+    }
+  }
+  return true;
+}
+// Split the quads of one half (loaded by poll_quads) into the operand planes at [row * pitch + c].
+__device__ __forceinline__ void put_quads(const u32x4 (&qv)[8], int half, int nb, int HC, uint16_t* hi, uint16_t* lo,
+                                          int pitch) {
+  const int qpr = HC >> 2;
+  const int t = local_tid();
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const int i = t + kT * m, row = i / qpr, qc = i - row * qpr;
+    if (row < nb) {
+      const u32x4 q = qv[4 * half + m];
+      uint32_t h0, l0, h1, l1, h2, l2, h3, l3;
+      split_h24(q.x, h0, l0);
+      split_h24(q.y, h1, l1);
+      split_h24(q.z, h2, l2);
+      split_h24(q.w, h3, l3);
+      *(uint2*)(hi + row * pitch + 4 * qc) = make_uint2(h0 | (h1 << 16), h2 | (h3 << 16));
+      *(uint2*)(lo + row * pitch + 4 * qc) = make_uint2(l0 | (l1 << 16), l2 | (l3 << 16));
+    }
+  }
+}
+
 // Wait until at least one of np producers has published (one lane per producer); the bulk of
 // a hand-off then follows within a fraction of a microsecond.
 __device__ __forceinline__ void wait_any_producer(const uint64_t* src0, size_t pstride, int np, uint32_t tag,
@@ -562,6 +635,13 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   for (int i = tid; i < 2 * kMaxBatch; i += kT) {
     const int par = i / kMaxBatch, b = i % kMaxBatch;
     st64(a.keys + (size_t)(1 - set) * 2 * kstride + par * kstride + (size_t)b * Gp + w, 0ull);
+  }
+  // ---- wide batches: clear this workgroup's share of the other set of h words (the next call
+  // starts from zeros, whatever batch, B or H earlier calls used); 8-bit tags need it
+  if (!NARROW && !MARKOV) {
+    uint64_t* hz = (uint64_t*)(a.h32 + (size_t)(1 - set) * kH32Set);
+    const size_t n64 = kH32Set / 2, per = (n64 + G - 1) / G;
+    for (size_t i = (size_t)w * per + tid; i < (size_t)(w + 1) * per && i < n64; i += kT) st64(hz + i, 0ull);
   }
 
   // ---- resident weights
@@ -706,6 +786,9 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   // the gather of position j + 1: right after the argmax key they are on the critical path
   // to the next merge.  -1: nothing pending.
   int pending_stats = -1;
+  // wide batches: the state of the owned units of this lane's slots (wave m, M tile m), kept in
+  // registers across positions: the published 24-bit copy feeds only the matrix products
+  float hown[4] = {0.f, 0.f, 0.f, 0.f};
 
   for (int j = 0; j < Bk; ++j) {
     const uint32_t tag = (epoch << 8) | (uint32_t)(j + 1);
@@ -720,6 +803,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       const uint32_t tag_prev = (epoch << 8) | (uint32_t)j;   // h published at position j-1
       const uint64_t* hprev = a.hbuf + (size_t)((j - 1) & 1) * batch * H;
       uint64_t* hnew = a.hbuf + (size_t)par * batch * H;
+      uint32_t* h32new = NARROW ? nullptr : a.h32 + (size_t)set * kH32Set + (size_t)par * kMaxBatch * H;
       if (j > 0) {
         if (!merge_position(j - 1)) return;
       } else {
@@ -734,11 +818,12 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       {
         const int mt = wave;
         const int nb = mt < mtiles ? (batch - mt * 16 < 16 ? batch - mt * 16 : 16) : 0;
-        uint64_t hv[4];   // the owned units' previous state, in flight together with the gather
+        uint64_t hv[4];   // narrow: the owned units' previous state, in flight together with the gather
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          hv[i] = (hs > 0 && 4 * g4 + i < nb) ? ld64(hprev + (size_t)(mt * 16 + 4 * g4 + i) * H + 16 * w + n16)
-                                               : 0ull;
+          hv[i] = (NARROW && hs > 0 && 4 * g4 + i < nb)
+                      ? ld64(hprev + (size_t)(mt * 16 + 4 * g4 + i) * H + 16 * w + n16)
+                      : 0ull;
         // with statistics of the previous position pending (one M tile), wave 3 publishes them
         // while the other waves gather (the gather is latency-bound; wave 3 loads nothing until
         // the rank stage, so its stores delay no load of its own)
@@ -774,9 +859,13 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
             if (slot < nb) {
               float hp = 0.f, ghr = 0.f, ghz = 0.f, ghn = 0.f;
               if (hs > 0) {
-                if ((uint32_t)(hv[i] >> 32) != tag_prev)
-                  ok &= wait_tag(hprev + (size_t)bb * H + 16 * w + n16, tag_prev, err, hv[i]);
-                hp = __uint_as_float((uint32_t)hv[i]);
+                if (NARROW) {
+                  if ((uint32_t)(hv[i] >> 32) != tag_prev)
+                    ok &= wait_tag(hprev + (size_t)bb * H + 16 * w + n16, tag_prev, err, hv[i]);
+                  hp = __uint_as_float((uint32_t)hv[i]);
+                } else {
+                  hp = hown[i];
+                }
                 ghr = gh[slot * 48 + n16];
                 ghz = gh[slot * 48 + 16 + n16];
                 ghn = gh[slot * 48 + 32 + n16];
@@ -785,7 +874,13 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
               const float rg = sigm(gi[n16] + ghr);
               const float zg = sigm(gi[16 + n16] + ghz);
               const float ng = tanhf_(gi[32 + n16] + rg * ghn);
-              st64(hnew + (size_t)bb * H + 16 * w + n16, tagged((1.f - zg) * ng + zg * hp, tag));
+              const float hv1 = (1.f - zg) * ng + zg * hp;
+              if (NARROW) {
+                st64(hnew + (size_t)bb * H + 16 * w + n16, tagged(hv1, tag));
+              } else {
+                hown[i] = hv1;
+                st32(h32new + (size_t)bb * H + 16 * w + n16, pack_h24(hv1, tag8));
+              }
             }
           }
         }
@@ -817,12 +912,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
             g2 = mfma_vv(alo, b2, mfma_vv(ahi, b2, g2));
           }
         };
-        for (int k0 = 0; k0 < H; k0 += HC) {
-          if (k0) __syncthreads();
-          // the other GRU workgroups publish h at about the same time: poll the words directly
-          ok &= NARROW ? stage_poll_words<kInf>(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err)
-                       : stage_poll_pairs<kInf>(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
-          __syncthreads();
+        // the owned rank rows and, with several chunks, W_hh h of the chunk staged at column k0
+        auto chunk_products = [&](int k0) __attribute__((always_inline)) {
           for (int kk = wave; kk < HC / 32; kk += 4) {
             uint4 ahi, alo;
             plane_operand(s_hi, s_lo, pitch, nb, n16, g4, 32 * kk, ahi, alo);
@@ -832,6 +923,34 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
             racc = mfma_vv(alo, bw, racc);
           }
           if (chunked && with_gh) gh_chunk(k0);
+        };
+        // the other GRU workgroups publish h at about the same time: poll the words directly
+        if (NARROW) {
+          for (int k0 = 0; k0 < H; k0 += HC) {
+            if (k0) __syncthreads();
+            ok &= stage_poll_words<kInf>(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
+            __syncthreads();
+            chunk_products(k0);
+          }
+        } else {
+          // 32-bit words, two chunks per round of loads: the second chunk waits in registers
+          // while the first is multiplied
+          const uint32_t* h32src = h32new + (size_t)mt * 16 * H;
+          for (int k0 = 0; k0 < H; k0 += 2 * HC) {
+            const bool two = k0 + HC < H;
+            u32x4 qv[8];
+            ok &= poll_quads(h32src, nb, HC, H, k0, two, tag8, qv, err);
+            if (k0) __syncthreads();   // every wave is done with the planes' previous chunk
+            put_quads(qv, 0, nb, HC, s_hi, s_lo, pitch);
+            __syncthreads();
+            chunk_products(k0);
+            if (two) {
+              __syncthreads();
+              put_quads(qv, 1, nb, HC, s_hi, s_lo, pitch);
+              __syncthreads();
+              chunk_products(k0 + HC);
+            }
+          }
         }
         if (n16 < rpg) s_rred[(wave * 4 + g4) * rpg + n16] = racc;
         if (fail_barrier(!ok, s_fail)) return;
@@ -1288,7 +1407,7 @@ hipError_t launch_k(const PersistArgs& pa, int G, size_t lds, hipStream_t st) {
 // translation unit of its own.
 template <int KK, bool SAMPLE>
 hipError_t launch_persistent_kk(const PersistArgs& pa, int G, size_t lds, dls_dtype long_dtype, hipStream_t st) {
-  const bool narrow = pa.batch <= 4, prior = pa.prior != nullptr, markov = pa.e_m != nullptr;
+  const bool narrow = pa.batch <= kNarrowBatch, prior = pa.prior != nullptr, markov = pa.e_m != nullptr;
 #define DLS_PK(LT, P, N, M) \
   if (prior == P && narrow == N && markov == M) return launch_k<KK, LT, P, N, M, SAMPLE>(pa, G, lds, st);
 #define DLS_PK_LT(LT)                                                                              \

@@ -211,6 +211,28 @@ def test_persistent_repeat_and_paths_agree():
         assert np.all(ref.gap[near] < TOL)
 
 
+def test_persistent_workspace_shared_across_shapes():
+    """One workspace serves calls of different batch sizes and block lengths in turn, each with
+    other inputs than the call before (wide batches hand h over with 8-bit position tags, so a
+    call must not see words left by an earlier one): every call returns the bits of the same
+    call on a fresh workspace."""
+    p = _problem("qwen3-8b-b16", "stress", dtype="bf16", **SMALL[3])   # batch 37, 5 positions
+    head = _head(p, True)
+    ws = B.draft_workspace(head, 64, 16)
+    shapes = [(37, 5), (6, 3), (37, 5), (20, 4), (2, 5), (37, 5), (37, 5)]
+    for k, (b, bk) in enumerate(shapes):
+        lt = B.as_tensor(np.ascontiguousarray(p["long_h"][:b, :bk]))
+        last = torch.from_numpy(np.ascontiguousarray(np.roll(p["last"], k)[:b])).cuda()
+        alpha = 0.4 + 0.1 * (k % 3)
+        tok, st = B.draft_block(head, lt, last, None, 1.0, alpha, 0.0, workspace=ws)
+        fresh = B.draft_workspace(head, b, bk)
+        tok2, st2 = B.draft_block(head, lt, last, None, 1.0, alpha, 0.0, workspace=fresh)
+        torch.cuda.synchronize()
+        assert B.workspace_error(ws) == 0 and B.workspace_error(fresh) == 0
+        assert torch.equal(tok, tok2), (k, b, bk)
+        assert torch.equal(st.view(torch.int32), st2.view(torch.int32)), (k, b, bk)
+
+
 @pytest.mark.parametrize("shape", [0, 1, 3])
 def test_exclusive_device_launch_same_bits(shape):
     """DLS_EXCLUSIVE_DEVICE (an ordinary instead of a cooperative dispatch of the persistent
