@@ -525,7 +525,11 @@ __device__ __forceinline__ void wait_any_producer(const uint64_t* src0, size_t p
 
 // Workgroup barrier that also tells whether any thread failed.  A failure is final (all waves
 // leave), so the LDS flag is set once and never cleared.
-__device__ __forceinline__ bool fail_barrier(bool failed, volatile int* s_fail) {
+// The flag lives in LDS and is accessed through an LDS-qualified pointer: through a generic
+// pointer the volatile access becomes a flat load, whose wait also waits for every store the
+// wave still has in flight (the hand-off stores take a microsecond to complete).
+typedef __attribute__((address_space(3))) volatile int lds_flag_t;
+__device__ __forceinline__ bool fail_barrier(bool failed, lds_flag_t* s_fail) {
   if (failed) *s_fail = 1;
   __syncthreads();
   return *s_fail != 0;
@@ -628,7 +632,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   p += (size_t)kMaxBatch * 8;
   int* s_tok = (int*)p;                             // kMaxBatch
   p += (size_t)kMaxBatch * 4;
-  volatile int* s_fail = (volatile int*)p;          // sticky failure flag
+  lds_flag_t* s_fail = (lds_flag_t*)p;              // sticky failure flag
   if (tid == 0) *s_fail = 0;
 
   // ---- clear this workgroup's key slots of the other set (read by the next call)
@@ -853,6 +857,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         bool ok = true;
         if (nb > 0) {   // wave-uniform
           const float* gh = s_gh + mt * 16 * 48;
+          float hn[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int slot = 4 * g4 + i, bb = mt * 16 + slot;
@@ -874,12 +879,20 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
               const float rg = sigm(gi[n16] + ghr);
               const float zg = sigm(gi[16 + n16] + ghz);
               const float ng = tanhf_(gi[32 + n16] + rg * ghn);
-              const float hv1 = (1.f - zg) * ng + zg * hp;
+              hn[i] = (1.f - zg) * ng + zg * hp;
+            }
+          }
+          // the stores after all four values: a store ahead of the arithmetic of the next slot
+          // would make the wave wait for its completion
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int slot = 4 * g4 + i, bb = mt * 16 + slot;
+            if (slot < nb) {
               if (NARROW) {
-                st64(hnew + (size_t)bb * H + 16 * w + n16, tagged(hv1, tag));
+                st64(hnew + (size_t)bb * H + 16 * w + n16, tagged(hn[i], tag));
               } else {
-                hown[i] = hv1;
-                st32(h32new + (size_t)bb * H + 16 * w + n16, pack_h24(hv1, tag8));
+                hown[i] = hn[i];
+                st32(h32new + (size_t)bb * H + 16 * w + n16, pack_h24(hn[i], tag8));
               }
             }
           }
