@@ -22,7 +22,10 @@
 // Cross-workgroup data moves through device-coherent 64-bit words that carry a tag
 // (epoch of the call, position); a consumer spins on the word itself until the tag
 // matches, so each hand-off costs one propagation, with no counters and no cache
-// flushes.  Every wait is bounded; on expiry an error word is set and all waves leave.
+// flushes.  Batches of more than four sequences (the wide form) load two such words per
+// 16-byte load and hand h over as 32-bit words (24-bit value, 8-bit position tag) in two
+// sets that alternate between calls.  Every wait is bounded; on expiry an error word is
+// set and all waves leave.
 #pragma once
 #include <atomic>
 
