@@ -793,8 +793,9 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   // the gather of position j + 1: right after the argmax key they are on the critical path
   // to the next merge.  -1: nothing pending.
   int pending_stats = -1;
-  // wide batches: the state of the owned units of this lane's slots (wave m, M tile m), kept in
-  // registers across positions: the published 24-bit copy feeds only the matrix products
+  // wide batches: the state of the owned units of this lane's slots (the gate pairs of its
+  // wave), kept in registers across positions: the published 24-bit copy feeds only the
+  // matrix products
   float hown[4] = {0.f, 0.f, 0.f, 0.f};
 
   for (int j = 0; j < Bk; ++j) {
@@ -821,16 +822,19 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         __syncthreads();
       }
       // gates of the owned units: gi = T[u] (folded input projection) for all sequences at once,
-      // 16-byte loads; gh from the previous step.  Wave m computes the gates of M tile m.
+      // 16-byte loads; gh from the previous step.  The (M tile, slot group i) pairs are spread
+      // over the waves, mtiles pairs each: wave v takes pairs v * mtiles + k, pair p being M tile
+      // p / 4 and slots 4 g4 + p % 4 of it (one M tile: wave v computes slot group v).
       {
-        const int mt = wave;
-        const int nb = mt < mtiles ? (batch - mt * 16 < 16 ? batch - mt * 16 : 16) : 0;
+        const int npw = mtiles;   // pairs per wave (mtiles <= 4)
         uint64_t hv[4];   // narrow: the owned units' previous state, in flight together with the gather
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          hv[i] = (NARROW && hs > 0 && 4 * g4 + i < nb)
-                      ? ld64(hprev + (size_t)(mt * 16 + 4 * g4 + i) * H + 16 * w + n16)
+        for (int k = 0; k < 4; ++k) {
+          const int pp = wave * npw + k, mt = pp >> 2, slot = 4 * g4 + (pp & 3);
+          hv[k] = (NARROW && hs > 0 && k < npw && mt * 16 + slot < batch && slot < 16)
+                      ? ld64(hprev + (size_t)(mt * 16 + slot) * H + 16 * w + n16)
                       : 0ull;
+        }
         // with statistics of the previous position pending (one M tile), wave 3 publishes them
         // while the other waves gather (the gather is latency-bound; wave 3 loads nothing until
         // the rank stage, so its stores delay no load of its own)
@@ -858,45 +862,43 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         pending_stats = -1;
         __syncthreads();
         bool ok = true;
-        if (nb > 0) {   // wave-uniform
-          const float* gh = s_gh + mt * 16 * 48;
-          float hn[4] = {0.f, 0.f, 0.f, 0.f};
+        float hn[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int slot = 4 * g4 + i, bb = mt * 16 + slot;
-            if (slot < nb) {
-              float hp = 0.f, ghr = 0.f, ghz = 0.f, ghn = 0.f;
-              if (hs > 0) {
-                if (NARROW) {
-                  if ((uint32_t)(hv[i] >> 32) != tag_prev)
-                    ok &= wait_tag(hprev + (size_t)bb * H + 16 * w + n16, tag_prev, err, hv[i]);
-                  hp = __uint_as_float((uint32_t)hv[i]);
-                } else {
-                  hp = hown[i];
-                }
-                ghr = gh[slot * 48 + n16];
-                ghz = gh[slot * 48 + 16 + n16];
-                ghn = gh[slot * 48 + 32 + n16];
-              }
-              const float* gi = s_gi + bb * 48;
-              const float rg = sigm(gi[n16] + ghr);
-              const float zg = sigm(gi[16 + n16] + ghz);
-              const float ng = tanhf_(gi[32 + n16] + rg * ghn);
-              hn[i] = (1.f - zg) * ng + zg * hp;
-            }
-          }
-          // the stores after all four values: a store ahead of the arithmetic of the next slot
-          // would make the wave wait for its completion
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int slot = 4 * g4 + i, bb = mt * 16 + slot;
-            if (slot < nb) {
+        for (int k = 0; k < 4; ++k) {
+          const int pp = wave * npw + k, mt = pp >> 2, slot = 4 * g4 + (pp & 3), bb = mt * 16 + slot;
+          if (k < npw && bb < batch && slot < 16) {
+            float hp = 0.f, ghr = 0.f, ghz = 0.f, ghn = 0.f;
+            if (hs > 0) {
               if (NARROW) {
-                st64(hnew + (size_t)bb * H + 16 * w + n16, tagged(hn[i], tag));
+                if ((uint32_t)(hv[k] >> 32) != tag_prev)
+                  ok &= wait_tag(hprev + (size_t)bb * H + 16 * w + n16, tag_prev, err, hv[k]);
+                hp = __uint_as_float((uint32_t)hv[k]);
               } else {
-                hown[i] = hn[i];
-                st32(h32new + (size_t)bb * H + 16 * w + n16, pack_h24(hn[i], tag8));
+                hp = hown[k];
               }
+              const float* gh = s_gh + mt * 16 * 48;
+              ghr = gh[slot * 48 + n16];
+              ghz = gh[slot * 48 + 16 + n16];
+              ghn = gh[slot * 48 + 32 + n16];
+            }
+            const float* gi = s_gi + bb * 48;
+            const float rg = sigm(gi[n16] + ghr);
+            const float zg = sigm(gi[16 + n16] + ghz);
+            const float ng = tanhf_(gi[32 + n16] + rg * ghn);
+            hn[k] = (1.f - zg) * ng + zg * hp;
+          }
+        }
+        // the stores after all the values: a store ahead of the arithmetic of the next slot
+        // would make the wave wait for its completion
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int pp = wave * npw + k, mt = pp >> 2, slot = 4 * g4 + (pp & 3), bb = mt * 16 + slot;
+          if (k < npw && bb < batch && slot < 16) {
+            if (NARROW) {
+              st64(hnew + (size_t)bb * H + 16 * w + n16, tagged(hn[k], tag));
+            } else {
+              hown[k] = hn[k];
+              st32(h32new + (size_t)bb * H + 16 * w + n16, pack_h24(hn[k], tag8));
             }
           }
         }
