@@ -308,7 +308,7 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_d
       pa.hdr = (uint32_t*)ws;
       pa.keys = (uint64_t*)(ws + pw.off_keys);
       pa.hbuf = (uint64_t*)(ws + pw.off_h);
-      pa.h32 = batch > dls::kNarrowBatch ? (uint32_t*)(ws + pw.off_h32) : nullptr;
+      pa.h32 = (uint32_t*)(ws + pw.off_h32);
       pa.rbuf = (uint64_t*)(ws + pw.off_rho);
       pa.stats = (uint64_t*)(ws + pw.off_stats);
       hipError_t e = dls::launch_persistent(pa, pl, long_dtype, (hipStream_t)stream);

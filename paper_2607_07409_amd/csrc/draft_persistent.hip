@@ -71,10 +71,12 @@ PersistWorkspace persist_workspace(const dls_local_head& h, int32_t batch, int32
   size_t o = 256;                                     // header: epoch, error word
   L.off_keys = o;
   o += (size_t)2 * 2 * kMaxBatch * kMaxG * 8;
+  // the two sets of 32-bit h words sit at a fixed offset with a fixed size, whatever the
+  // batch, B or H of a call: their 8-bit tags must never meet words another layout left there
+  L.off_h32 = o;
+  o += 2 * kH32Set * 4;
   L.off_h = o;
   o += (size_t)2 * batch * h.H * 8;
-  L.off_h32 = o;
-  if (batch > kNarrowBatch) o += 2 * kH32Set * 4;
   L.off_rho = o;
   o += (size_t)kRhoCopies * 2 * batch * h.r * 8;
   L.off_stats = o;

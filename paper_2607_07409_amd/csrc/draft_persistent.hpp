@@ -643,9 +643,10 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     const int par = i / kMaxBatch, b = i % kMaxBatch;
     st64(a.keys + (size_t)(1 - set) * 2 * kstride + par * kstride + (size_t)b * Gp + w, 0ull);
   }
-  // ---- wide batches: clear this workgroup's share of the other set of h words (the next call
-  // starts from zeros, whatever batch, B or H earlier calls used); 8-bit tags need it
-  if (!NARROW && !MARKOV) {
+  // ---- clear this workgroup's share of the other set of the wide h words, in every call (a
+  // narrow or Markov call too): the next call then starts from zeros, whatever earlier calls
+  // wrote, which the 8-bit tags of those words need
+  {
     uint64_t* hz = (uint64_t*)(a.h32 + (size_t)(1 - set) * kH32Set);
     const size_t n64 = kH32Set / 2, per = (n64 + G - 1) / G;
     for (size_t i = (size_t)w * per + tid; i < (size_t)(w + 1) * per && i < n64; i += kT) st64(hz + i, 0ull);

@@ -231,6 +231,13 @@ def test_persistent_workspace_shared_across_shapes():
         assert B.workspace_error(ws) == 0 and B.workspace_error(fresh) == 0
         assert torch.equal(tok, tok2), (k, b, bk)
         assert torch.equal(st.view(torch.int32), st2.view(torch.int32)), (k, b, bk)
+        # white-box: the set of 32-bit h words the next call will read is all zeros, whatever
+        # this call was (narrow calls clear it too).  Layout: 256-byte header, 2 x 2 x 64 x 256
+        # argmax keys of 8 bytes, then two sets of 2 x 64 x 4096 words of 4 bytes; the set is
+        # the parity of the call epoch (the first uint32 of the header, advanced by each call)
+        nxt = int(ws[0:4].view(torch.int32).item()) & 1
+        off, size = 256 + 2 * 2 * 64 * 256 * 8, 2 * 64 * 4096 * 4
+        assert int(ws[off + nxt * size: off + (nxt + 1) * size].count_nonzero().item()) == 0, (k, b, bk)
 
 
 @pytest.mark.parametrize("shape", [0, 1, 3])

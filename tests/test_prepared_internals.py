@@ -87,7 +87,9 @@ def test_first_position_handoffs(prob):
                             workspace=ws)
     torch.cuda.synchronize()
     assert B.workspace_error(ws) == 0
-    off_h = 256 + 2 * 2 * 64 * 256 * 8
+    # workspace layout: 256-byte header, argmax keys, the two sets of wide-batch h words
+    # (2 x 2 x 64 x 4096 words of 4 bytes), then the 64-bit h and rho hand-off words
+    off_h = 256 + 2 * 2 * 64 * 256 * 8 + 2 * 2 * 64 * 4096 * 4
     off_r = off_h + 2 * batch * H * 8
     words_h = ws[off_h:off_h + batch * H * 8].view(torch.int64).cpu().numpy()
     words_r = ws[off_r:off_r + batch * R * 8].view(torch.int64).cpu().numpy()
