@@ -506,15 +506,21 @@ __device__ __forceinline__ void put_quads(const u32x4 (&qv)[8], int half, int nb
   }
 }
 
-// Wait until at least one of np producers has published (one lane per producer); the bulk of
-// a hand-off then follows within a fraction of a microsecond.
-__device__ __forceinline__ void wait_any_producer(const uint64_t* src0, size_t pstride, int np, uint32_t tag,
-                                                  uint32_t* err) {
+// Wait until one (ALL = false) or every (ALL = true) of np producers has published (one lane
+// per producer, polling one word of each).  Narrow batches stage after the first producer: the
+// rest of their small hand-off follows within a fraction of a microsecond.  A wide batch of one
+// M tile waits for the last one, so that the 16-byte loads of its larger hand-off find every
+// word there in one round instead of polling again for the late producers.
+template <bool ALL>
+__device__ __forceinline__ void wait_producers(const uint64_t* src0, size_t pstride, int np, uint32_t tag,
+                                               uint32_t* err) {
   if (threadIdx.x < 64) {
     const int l = (int)threadIdx.x;
+    bool done = l >= np;   // a published word keeps its tag until this workgroup moves on
     for (long sp = 0;; ++sp) {
-      const bool seen = l < np && (uint32_t)(ld64(src0 + (size_t)l * pstride) >> 32) == tag;
-      if (__any(seen)) break;
+      const bool seen = !done && (uint32_t)(ld64(src0 + (size_t)l * pstride) >> 32) == tag;
+      done |= seen;
+      if (ALL ? __all(done) : __any(seen)) break;
       __builtin_amdgcn_s_sleep(4);
       if ((sp & 63) == 63 && ld32(err)) break;
       if (sp > kMaxSpins) {
@@ -1106,8 +1112,12 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       } else if (!long_only) {
         const uint64_t* rsrc = a.rbuf + ((size_t)(w % kRhoCopies) * 2 + par) * batch * r + (size_t)mt * 16 * r;
         // GRU workgroups come here after W_hh h, when rho is about complete: they poll the words
-        // directly; the others wait (gently) for the first producer, then poll
-        if (!gru) wait_any_producer(rsrc, (size_t)rpg, a.NG, tag, err);
+        // directly; the others wait (gently) for the first producer, or with one wide M tile for
+        // all of them (several M tiles: the rho of the later tiles is out long before), then poll
+        if (!gru) {
+          if (!NARROW && mtiles == 1) wait_producers<true>(rsrc, (size_t)rpg, a.NG, tag, err);
+          else wait_producers<false>(rsrc, (size_t)rpg, a.NG, tag, err);
+        }
         const bool ok = NARROW ? stage_poll_words<kInf>(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err)
                                : stage_poll_pairs<kInf>(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err);
         if (fail_barrier(!ok, s_fail)) return;
