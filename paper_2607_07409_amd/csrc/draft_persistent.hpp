@@ -43,7 +43,8 @@ constexpr int kT = 256;          // threads per workgroup (one wave per SIMD)
 constexpr int kOps = 56;         // MFMA B operands of 16 bytes per lane held in AGPRs (224 of
                                  // the 256; the rest take the accumulators)
 constexpr long kMaxSpins = 1L << 22;
-constexpr int kInflight = 8;     // 16-byte hand-off loads a thread issues before checking any of them
+constexpr int kInflight = 8;     // hand-off loads a thread issues before checking any of them (one
+                                 // 64-bit word each for narrow batches, 16 bytes for wide ones)
 constexpr int kStageK = 256;     // K chunk of staged hand-off values (16 slots x 256 floats in LDS)
 constexpr int kStatWords = 9;    // tagged words of one published partial
 constexpr int kRhoCopies = 8;    // replicas of the published rank vector (spreads the readers)
