@@ -144,6 +144,7 @@ SMALL = [
     dict(V=7001, d=64, H=256, r=256, Bk=9, batch=2),
     dict(V=1024, d=64, H=128, r=128, Bk=4, batch=1),
     dict(V=4099, d=128, H=128, r=128, Bk=5, batch=37),
+    dict(V=2053, d=64, H=512, r=128, Bk=5, batch=9),      # wide, h staged in two K chunks
 ]
 
 
