@@ -288,6 +288,7 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_d
       pa.NG = pl.NG;
       pa.rpg = pl.rpg;
       pa.cap_a = pl.cap_a;
+      pa.gcap = pl.gcap;
       pa.rows_max = pl.rows_max;
       pa.lds_region_a = pl.lds_region_a;
       pa.L = long_logits;

@@ -111,7 +111,7 @@ struct PersistArgs {
   const uint4* whh;          // W_hh in MFMA operand order, per 16-unit group
   const bf16_t* w_rank;      // [r][H]
   const bf16_t* e_m;         // Markov head: E_M [V][r] (the GRU fields are unused then)
-  int V, H, r, NT, NG, rpg, cap_a, rows_max;
+  int V, H, r, NT, NG, rpg, cap_a, gcap, rows_max;
   size_t lds_region_a;
   const void* L;             // long logits [batch][B][V]
   const int32_t* last;
@@ -135,13 +135,14 @@ struct PersistArgs {
 struct PersistPlan {
   bool ok;
   const char* why;
-  int G, NG, rpg, NT, cap_a, rows_max;
+  int G, NG, rpg, NT, cap_a, gcap, rows_max;
   size_t lds_region_a, lds;
 };
 struct PersistWorkspace {
   size_t off_keys, off_h, off_h32, off_rho, off_stats, total;
 };
-__host__ __device__ inline void persist_tile_range(int w, int G, int NG, int NT, int cap_a, int* t0, int* n);
+__host__ __device__ inline void persist_tile_range(int w, int G, int NG, int NT, int cap_a, int gcap, int* t0,
+                                                   int* n);
 PersistPlan persist_plan(const dls_local_head& h, int32_t batch, int32_t B, dls_dtype long_dtype, bool prior, int G);
 PersistWorkspace persist_workspace(const dls_local_head& h, int32_t batch, int32_t B);
 hipError_t launch_persistent(const PersistArgs& pa, const PersistPlan& pl, dls_dtype long_dtype, hipStream_t st);

@@ -36,27 +36,45 @@ PersistPlan persist_plan(const dls_local_head& h, int32_t batch, int32_t B, dls_
   pl.rpg = markov ? 0 : h.r / NG;
   pl.NT = (h.V + 15) / 16;
   pl.cap_a = 4 * (kOps / KK);
-  int rows_max = 0, nl_max = 0;
-  for (int w = 0; w < G; ++w) {
-    int t0, n;
-    persist_tile_range(w, G, NG, pl.NT, pl.cap_a, &t0, &n);
-    rows_max = std::max(rows_max, 16 * n);
-    if (w >= NG) nl_max = std::max(nl_max, n - std::min(n, pl.cap_a));
-    else if (n > pl.cap_a) {
-      pl.why = "vocabulary tiles exceed the GRU workgroups' AGPRs";
-      return pl;
-    }
-  }
-  const size_t region_gru = markov ? 0 : (size_t)3 * (h.H / 32) * 1024 + (size_t)pl.rpg * h.H * 2;
-  const size_t region_tiles = (size_t)nl_max * KK * 1024;
-  pl.lds_region_a = (std::max(region_gru, region_tiles) + 15) & ~(size_t)15;
-  pl.rows_max = rows_max;
   const size_t esz = long_dtype == DLS_BF16 ? 2 : 4;
   const int ll_slots = batch < 16 ? batch : 16;
-  size_t lds = pl.lds_region_a + (((size_t)ll_slots * rows_max * esz + 15) & ~(size_t)15);
-  if (prior) lds += (size_t)rows_max * 4;
-  lds += (size_t)2 * kPlane * 2 + (size_t)16 * pl.rpg * 16 + (size_t)((batch + 15) / 16) * 16 * 48 * 4 +
-         (size_t)4 * 16 * sizeof(Partial) + (size_t)kMaxBatch * 8 + (size_t)kMaxBatch * 4 + 16;
+  // LDS need of the tile split with gcap tiles per GRU workgroup (0: a GRU workgroup's tiles
+  // exceed its AGPRs)
+  auto lds_need = [&](int gcap, int* rows_out, size_t* region_out) -> size_t {
+    int rows_max = 0, nl_max = 0;
+    for (int w = 0; w < G; ++w) {
+      int t0, n;
+      persist_tile_range(w, G, NG, pl.NT, pl.cap_a, gcap, &t0, &n);
+      rows_max = std::max(rows_max, 16 * n);
+      if (w >= NG) nl_max = std::max(nl_max, n - std::min(n, pl.cap_a));
+      else if (n > pl.cap_a) return 0;
+    }
+    const size_t region_gru = markov ? 0 : (size_t)3 * (h.H / 32) * 1024 + (size_t)pl.rpg * h.H * 2;
+    const size_t region_tiles = (size_t)nl_max * KK * 1024;
+    const size_t region_a = (std::max(region_gru, region_tiles) + 15) & ~(size_t)15;
+    size_t lds = region_a + (((size_t)ll_slots * rows_max * esz + 15) & ~(size_t)15);
+    if (prior) lds += (size_t)rows_max * 4;
+    lds += (size_t)2 * kPlane * 2 + (size_t)16 * pl.rpg * 16 + (size_t)((batch + 15) / 16) * 16 * 48 * 4 +
+           (size_t)4 * 16 * sizeof(Partial) + (size_t)kMaxBatch * 8 + (size_t)kMaxBatch * 4 + 16;
+    *rows_out = rows_max;
+    *region_out = region_a;
+    return lds;
+  };
+  // Narrow batches: the GRU workgroups reach their vocabulary tiles about 2 us after the others
+  // (they compute W_hh h and stage rho first), so they take three quarters of a full AGPR load
+  // and the others hold the surplus in LDS, which narrow batches leave free; the share grows
+  // back toward a full load while the others' LDS would overflow.  Wide batches: a full load.
+  int gcap = (batch <= kNarrowBatch && !markov) ? (3 * pl.cap_a + 3) / 4 : pl.cap_a;
+  int rows_max = 0;
+  size_t region_a = 0, lds = lds_need(gcap, &rows_max, &region_a);
+  while ((lds == 0 || lds > kMaxLds) && gcap < pl.cap_a) lds = lds_need(++gcap, &rows_max, &region_a);
+  if (lds == 0) {
+    pl.why = "vocabulary tiles exceed the GRU workgroups' AGPRs";
+    return pl;
+  }
+  pl.gcap = gcap;
+  pl.lds_region_a = region_a;
+  pl.rows_max = rows_max;
   pl.lds = lds;
   if (lds > kMaxLds) {
     pl.why = "per-workgroup LDS need exceeds 160 KiB";

@@ -263,17 +263,21 @@ struct RowRor {
 // ------------------------------------------------------------------------------------------
 // tile ownership (shared with the host)
 // ------------------------------------------------------------------------------------------
-__host__ __device__ inline void persist_tile_range(int w, int G, int NG, int NT, int cap_a, int* t0, int* n) {
+// cap_a: vocabulary tiles a workgroup holds in AGPRs; gcap (<= cap_a): tiles of a GRU workgroup
+// when the tiles do not fit in the AGPRs of all workgroups (the rest go to the others, which
+// hold the surplus in LDS)
+__host__ __device__ inline void persist_tile_range(int w, int G, int NG, int NT, int cap_a, int gcap, int* t0,
+                                                   int* n) {
   if (NT <= G * cap_a) {
     const int q = NT / G, rm = NT % G;
     *t0 = w * q + (w < rm ? w : rm);
     *n = q + (w < rm ? 1 : 0);
     return;
   }
-  const int ga = NG * cap_a;
+  const int ga = NG * gcap;
   if (w < NG) {
-    *t0 = w * cap_a;
-    *n = cap_a;
+    *t0 = w * gcap;
+    *n = gcap;
     return;
   }
   const int rest = NT - ga, m = G - NG, i = w - NG;
@@ -607,7 +611,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   const size_t kstride = (size_t)kMaxBatch * Gp;      // one (set, parity) plane of keys
 
   int t0, nt;
-  persist_tile_range(w, G, a.NG, a.NT, a.cap_a, &t0, &nt);
+  persist_tile_range(w, G, a.NG, a.NT, a.cap_a, a.gcap, &t0, &nt);
   const int na = nt < a.cap_a ? nt : a.cap_a;
   const int nl = nt - na;
   const int v_base = 16 * t0;
