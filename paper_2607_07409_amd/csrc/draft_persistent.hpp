@@ -695,8 +695,9 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   // writes the drafted tokens.  Narrow batches: thread t loads the keys of workgroup t and
   // max-reduces them through LDS atomics.  Wide batches: wave v merges sequences v, v + 4, ...;
   // each lane loads the key pairs (workgroups 2c, 2c + 1) c = lane and lane + 64 of a sequence
-  // with 16-byte loads, four sequences per round, and the wave reduces them with DPP (256
-  // atomics on one LDS word per sequence would serialise).  Workgroup-uniform result.
+  // with 16-byte loads, four sequences per round; each row of 16 lanes reduces them with DPP and
+  // its first lane max-reduces the result into LDS (four atomics per sequence, where 256 would
+  // serialise and cross-row shuffles cost LDS round trips).  Workgroup-uniform result.
   auto merge_position = [&](int jm) -> bool {
     const uint32_t tag8 = (uint32_t)(jm + 1);
     const uint64_t* kp = a.keys + (size_t)set * 2 * kstride + (size_t)(jm & 1) * kstride;
@@ -717,6 +718,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         }
       }
     } else {
+      for (int b = tid; b < batch; b += kT) s_best[b] = 0ull;
+      __syncthreads();
       const __amdgpu_buffer_rsrc_t rs = coherent_rsrc(kp, (uint32_t)((size_t)batch * Gp * 8));
       constexpr int SPR = kInf / 2;   // sequences per round (two loads each)
       const int lane = local_tid() & 63;
@@ -767,8 +770,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         for (int k = 0; k < SPR; ++k) {
           const int b = b0 + 4 * k;
           if (b < batch) {   // wave-uniform
-            const uint64_t kb = wave_key_max(best[k]);
-            if (lane == 0) s_best[b] = kb;
+            const uint64_t kb = row_key_max(best[k]);
+            if ((lane & 15) == 0) atomicMax((unsigned long long*)&s_best[b], kb);
           }
         }
       }
