@@ -229,11 +229,31 @@ __device__ __forceinline__ uint64_t row_key_max(uint64_t k) {
   k = key_max(k, row_ror_u64<1>(k));
   return k;
 }
+// The value of lane l ^ 16 (or l ^ 32) through the permlane swaps of gfx950: VALU operations,
+// where a shuffle across rows would take an LDS round trip (ds_bpermute).  With both operands
+// equal, each swap returns this lane's value and its partner's, in an order that depends on
+// the lane; a symmetric operation can take the pair as it is.
+__device__ __forceinline__ uint32_t lane_xor16(uint32_t v) {
+  const auto q = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return (threadIdx.x & 16) ? q[0] : q[1];
+}
+__device__ __forceinline__ uint32_t lane_xor32(uint32_t v) {
+  const auto q = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return (threadIdx.x & 32) ? q[0] : q[1];
+}
 // largest key over the wave (every lane gets it)
 __device__ __forceinline__ uint64_t wave_key_max(uint64_t k) {
   k = row_key_max(k);
-  k = key_max(k, __shfl_xor(k, 16));
-  k = key_max(k, __shfl_xor(k, 32));
+  {
+    const auto lo = __builtin_amdgcn_permlane16_swap((uint32_t)k, (uint32_t)k, false, false);
+    const auto hi = __builtin_amdgcn_permlane16_swap((uint32_t)(k >> 32), (uint32_t)(k >> 32), false, false);
+    k = key_max(((uint64_t)hi[0] << 32) | lo[0], ((uint64_t)hi[1] << 32) | lo[1]);
+  }
+  {
+    const auto lo = __builtin_amdgcn_permlane32_swap((uint32_t)k, (uint32_t)k, false, false);
+    const auto hi = __builtin_amdgcn_permlane32_swap((uint32_t)(k >> 32), (uint32_t)(k >> 32), false, false);
+    k = key_max(((uint64_t)hi[0] << 32) | lo[0], ((uint64_t)hi[1] << 32) | lo[1]);
+  }
   return k;
 }
 
@@ -252,7 +272,8 @@ struct RowRor {
       case 4: return row_ror_i<4>(v);
       case 2: return row_ror_i<2>(v);
       case 1: return row_ror_i<1>(v);
-      default: return __shfl_xor(v, m);
+      case 16: return (int)lane_xor16((uint32_t)v);
+      default: return (int)lane_xor32((uint32_t)v);
     }
   }
   __device__ __forceinline__ float operator()(float v, int m) const { return __int_as_float(i(__float_as_int(v), m)); }
@@ -562,6 +583,14 @@ __device__ __forceinline__ void plane_operand(const uint16_t* hi, const uint16_t
 // NARROW: at most 4 sequences (one M tile whose useful rows all sit in lanes 0..15)
 // MARKOV: the Markov head of App. A, rho_j = E_M[u_j]: no GRU workgroups and no hand-off
 //         but the argmax keys; every workgroup merges the keys and reads the E_M row itself
+// the value of lane l ^ k within its quad (k = 1, 2, 3): a DPP quad permutation
+__device__ __forceinline__ uint32_t quad_xor(uint32_t v, int k) {
+  switch (k) {
+    case 1: return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xf, 0xf, false);   // [1, 0, 3, 2]
+    case 2: return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xf, 0xf, false);   // [2, 3, 0, 1]
+    default: return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x1B, 0xf, 0xf, false);  // [3, 2, 1, 0]
+  }
+}
 // Gumbel noise g[i] of sequences bq0 + i (i < n <= 4) at this lane's vocabulary entry v, for
 // temperature sampling.  The four lanes of a quad hold v = 4k .. 4k + 3 (one Philox block
 // counter): each runs the block of one sequence, bq0 + (lane & 3), and the quad exchanges
@@ -575,7 +604,7 @@ __device__ __forceinline__ void gumbel_quad(const Sampler& sm, int bq0, int j, i
     // round k: lane q ^ k of the quad needs word q ^ k of this lane's block
     const int want = q ^ k;
     const uint32_t send = want == 0 ? x4.x : (want == 1 ? x4.y : (want == 2 ? x4.z : x4.w));
-    r[k] = k == 0 ? send : (uint32_t)__shfl_xor((int)send, k);
+    r[k] = k == 0 ? send : quad_xor(send, k);
   }
   // r[k] is word q (entry v) of the block of sequence bq0 + (q ^ k)
 #pragma unroll
