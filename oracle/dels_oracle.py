@@ -23,6 +23,10 @@ Readings where the paper is silent (each is also listed in the design notes):
   GPU path decides in); every reported value is float64.
 * The short-logit weight is the paper's alpha; a long-logit weight w_long
   (1 in the paper) is kept so that w_long = 0 gives the local head alone.
+* A term whose weight is zero is absent, also where its logit is -inf (a
+  masked token): 0 * (-inf) reads as 0, the exponent form p^0 = 1 of the
+  fusion.  So w_long = 0 ignores a mask in the long logits, and beta = 0 an
+  unsmoothed prior's -inf.
 * Row j of the long logits is draft position j.  By default the head is seeded
   with the last accepted token and every row is fused.  With
   first_row_long_only=True row 0 is decoded from the long logits alone and the
@@ -94,13 +98,23 @@ class RowResult:
     scores: Optional[np.ndarray] = None   # c_v for every v, when requested
 
 
+def weighted(w: float, x) -> np.ndarray:
+    """w * x, except that a zero weight gives 0 even where x = -inf: a term weighted by 0 is
+    absent from the fusion (p^0 = 1 for every p, a masked p = 0 included), so w_long = 0
+    ignores the long logits and beta = 0 the prior, masked entries and all."""
+    x = np.asarray(x, dtype=F64)
+    if w == 0:
+        return np.zeros_like(x)
+    return F64(w) * x
+
+
 def fuse(long_row, short_row, prior, w_long: float, alpha: float, beta: float) -> np.ndarray:
     """l = w_long * l_L + alpha * l_S - beta * l_P  (Sec. 4.3; w_long = 1 in the paper)."""
-    f = F64(w_long) * np.asarray(long_row, dtype=F64)
+    f = weighted(w_long, long_row)
     if short_row is not None:
-        f = f + F64(alpha) * np.asarray(short_row, dtype=F64)
+        f = f + weighted(alpha, short_row)
     if prior is not None:
-        f = f - F64(beta) * np.asarray(prior, dtype=F64)
+        f = f - weighted(beta, prior)
     return f
 
 
@@ -132,7 +146,7 @@ def combine_row(long_row, short_row, prior, w_long: float, alpha: float, beta: f
     """
     long_row = np.asarray(long_row, dtype=F64)
     if short_row is None:
-        fused = F64(w_long) * long_row
+        fused = weighted(w_long, long_row)
         lse_s = float("nan")
         a_eff = 0.0
     else:
@@ -149,7 +163,7 @@ def combine_row(long_row, short_row, prior, w_long: float, alpha: float, beta: f
     lse_f = logsumexp(scaled)
     best = greedy_token(decide)
     tok = best if force_token is None else int(force_token)
-    norm = F64(w_long) * lse_l + (F64(a_eff) * lse_s if short_row is not None else 0.0)
+    norm = float(weighted(w_long, lse_l)) + (float(weighted(a_eff, lse_s)) if short_row is not None else 0.0)
     res = RowResult(token=tok, score=float(fused[tok] - norm), logprob=float(scaled[tok] - lse_f),
                     gap=top2_gap(decide), lse_long=lse_l, lse_short=lse_s, lse_fused=lse_f,
                     argmax=best, margin=float(decide[best] - decide[tok]))

@@ -274,3 +274,69 @@ def test_per_position_weights():
                 fused = (L[b, j] - be[j] * P).astype(np.float32)
                 assert res.tokens[b, j] == int(np.argmax(fused))
             u = r.token
+
+
+def _exact_masked(qL, qS, w, a):
+    """Exact fused quantities when some long probabilities are 0 (a -inf long logit, a masked
+    token).  With integer exponents the fused weight is p_L^w p_S^a, and 0^0 = 1: a zero long
+    weight leaves a masked token in play, a positive one removes it."""
+    sL, sS = sum(qL), sum(qS)
+    F = [Fraction(qL[v], sL) ** w * Fraction(qS[v], sS) ** a for v in range(len(qL))]
+    best = max(F)
+    tok = F.index(best)
+    rest = sorted(F, reverse=True)
+    if len(F) < 2:
+        gap = math.inf
+    elif rest[1] == 0:
+        gap = math.inf
+    else:
+        gap = math.log(rest[0] / rest[1])
+    G = [Fraction(qL[v]) ** w * Fraction(qS[v]) ** a for v in range(len(qL))]
+    return dict(token=tok, gap=gap, score=math.log(F[tok]), logprob=math.log(F[tok] / sum(F)),
+                lse_long=math.log(sL), lse_short=math.log(sS), lse_fused=math.log(sum(G)),
+                scores=[math.log(f) if f > 0 else -math.inf for f in F])
+
+
+@pytest.mark.parametrize("w,a", [(0, 1), (1, 0), (1, 1)])
+def test_brute_force_masked_long(w, a):
+    """Masked long logits (-inf): with w_long = 1 a masked token can never be drafted unless
+    every token is masked; with w_long = 0 the mask is absent with the rest of the long term
+    (the fusion's exponent form, p^0 = 1)."""
+    g = np.random.default_rng(4242 + 2 * w + a)
+    for _ in range(400):
+        V = int(g.integers(1, 7))
+        qL = [int(x) for x in g.integers(0, 6, size=V)]
+        if sum(qL) == 0:
+            qL[int(g.integers(0, V))] = 1          # at least one unmasked token
+        qS = [int(x) for x in g.integers(1, 10, size=V)]
+        with np.errstate(divide="ignore"):
+            long_row = np.log(np.array(qL, dtype=np.float64))
+        short_row = np.log(np.array(qS, dtype=np.float64))
+        ex = _exact_masked(qL, qS, w, a)
+        res = O.combine_row(long_row, short_row, None, float(w), float(a), 0.0, want_scores=True)
+        assert res.token == ex["token"], (qL, qS, w, a)
+        if w == 1:
+            assert qL[res.token] > 0
+        if math.isinf(ex["gap"]):
+            assert math.isinf(res.gap) and res.gap > 0, (qL, qS, w, a, res.gap)
+        else:
+            assert abs(res.gap - ex["gap"]) < 1e-12
+        for k in ("score", "logprob", "lse_long", "lse_short", "lse_fused"):
+            assert abs(getattr(res, k) - ex[k]) < 1e-12, (k, qL, qS, w, a)
+        np.testing.assert_allclose(res.scores, ex["scores"], atol=1e-12)
+
+
+def test_zero_prior_weight_ignores_unseen_tokens():
+    """beta = 0 removes the prior term even where an unsmoothed prior is -inf (an unseen
+    token): the fused row equals the row without a prior."""
+    g = np.random.default_rng(11)
+    for _ in range(50):
+        V = int(g.integers(2, 40))
+        L = g.normal(0, 3, V)
+        S = g.normal(0, 2, V)
+        P = np.log(g.dirichlet(np.ones(V)))
+        P[g.integers(0, V, size=3)] = -np.inf
+        a = O.combine_row(L, S, P, 1.0, 0.5, 0.0, want_scores=True)
+        b = O.combine_row(L, S, None, 1.0, 0.5, 0.0, want_scores=True)
+        assert a.token == b.token and a.gap == b.gap and a.logprob == b.logprob
+        np.testing.assert_array_equal(a.scores, b.scores)

@@ -16,8 +16,10 @@ PIN_TESTS = [os.path.join(ROOT, "tests", f) for f in
               "test_oracle_sampling.py")]
 
 MUTATIONS = {
-    "prior_sign": ("f = f - F64(beta) * np.asarray(prior", "f = f + F64(beta) * np.asarray(prior"),
-    "drop_short": ("f = f + F64(alpha) * np.asarray(short_row", "f = f + 0.0 * np.asarray(short_row"),
+    "prior_sign": ("f = f - weighted(beta, prior)", "f = f + weighted(beta, prior)"),
+    "drop_short": ("f = f + weighted(alpha, short_row)", "f = f + 0.0 * np.asarray(short_row, dtype=F64)"),
+    "zero_weight_as_product": ("    if w == 0:\n        return np.zeros_like(x)\n", ""),
+    "zero_weight_masks_all": ("        return np.zeros_like(x)\n", "        return np.where(np.isneginf(x), x, 0.0)\n"),
     "tie_highest_index": ("return int(np.argmax(np.asarray(fused, dtype=np.float32)))",
                           "a = np.asarray(fused, dtype=np.float32); return int(len(a) - 1 - np.argmax(a[::-1]))"),
     "gate_swap_rz": ("r = sigmoid(gi[:H] + gh[:H])", "r = sigmoid(gi[H:2 * H] + gh[H:2 * H])"),
@@ -28,7 +30,7 @@ MUTATIONS = {
     "no_feedback": ("            u = res.token\n", "            u = int(last_token[b])\n"),
     "lse_no_shift": ("return float(m + np.log(np.sum(np.exp(x - m))))",
                      "return float(m + np.log(np.sum(np.exp(x))))"),
-    "score_norm_drop_wlong": ("norm = F64(w_long) * lse_l", "norm = lse_l"),
+    "score_norm_drop_wlong": ("norm = float(weighted(w_long, lse_l))", "norm = float(lse_l)"),
     "logprob_wrong_lse": ("logprob=float(scaled[tok] - lse_f)", "logprob=float(scaled[tok] - lse_l)"),
     "gap_top1_only": ("return float(top[1] - top[0])", "return float(top[1])"),
     "accept_off_by_one": ("while a < B and draft[b, a] == target[b, a]",
