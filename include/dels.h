@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define DLS_ABI_VERSION 2
+#define DLS_ABI_VERSION 3
 
 typedef enum dls_status {
   DLS_OK = 0,
@@ -123,6 +123,11 @@ typedef enum dls_head_kind {
  *   w_vocab [V, r]   W_M, the low-rank vocabulary head
  * prepared  NULL, or a device buffer filled by dls_prepare_head from these same tensors;
  *           it enables the persistent drafting kernel (see below)
+ * prepared_bytes  the size of that buffer in bytes (0 when prepared is NULL).  A drafting
+ *           call checks on the host that it is at least dls_prepare_head_size(head)
+ *           (DLS_ERR_WORKSPACE otherwise); the persistent kernel checks the buffer's header,
+ *           written by dls_prepare_head, against the head's shapes and tensor pointers and
+ *           fails with DLS_DRAFT_ERR_PREPARED (see dls_draft_block_error) if they differ
  * Limits: 1 <= V <= 2^24; d, H, r multiples of 8 with 8 <= d <= 16384,
  * 8 <= H <= 4096, 8 <= r <= 512 (RNN); 8 <= r <= 512, r a multiple of 8 (Markov). */
 typedef struct dls_local_head {
@@ -136,6 +141,7 @@ typedef struct dls_local_head {
   const void *prepared;
   int32_t kind;        /* dls_head_kind */
   int32_t reserved;    /* 0 */
+  size_t prepared_bytes;
 } dls_local_head;
 
 /* ---------------------------------------------------------------------------------
@@ -181,9 +187,13 @@ dls_status dls_combine_logits(const void *long_logits, const void *short_logits,
  * persistent kernel keeps the head weights on chip for the whole block; otherwise each
  * position is a sequence of kernel launches.  dls_draft_block_path tells which is used.
  * The workspace must be zero-filled before its first use; the library keeps it
- * consistent afterwards.  If a persistent call ever sets the error word (the second
- * uint32 of the workspace, nonzero after a stalled hand-off between workgroups), later
- * persistent calls on that workspace do nothing until it is zero-filled again.
+ * consistent afterwards.  A persistent call that fails sets the workspace's error word
+ * (read it with dls_draft_block_error; the call itself has returned DLS_OK long before,
+ * since it only enqueues work).  A failed call writes token -1 at every position it did
+ * not finish drafting (all positions unless only the statistics failed) and NaN into
+ * every statistics row it could not merge, so that no stale output passes for a draft.
+ * Later persistent calls on a workspace whose error word is set do nothing but write
+ * the same sentinels, until the workspace is zero-filled again.
  *   head         RNN or Markov local head (see dls_local_head); device pointers
  *   long_logits  [batch, B, V] of `long_dtype`; row j is the long logits of draft
  *                position j
@@ -206,6 +216,19 @@ dls_status dls_draft_block(const dls_local_head *head, const void *long_logits,
                            int32_t batch, int32_t B, dls_fusion fusion, int32_t *out_tokens,
                            dls_row_stats *out_stats, void *workspace, size_t ws_bytes,
                            void *stream);
+
+/* Error word of a drafting workspace (0 when every persistent call on it succeeded). */
+#define DLS_DRAFT_ERR_STALLED 1   /* a hand-off between workgroups did not arrive within the spin
+                                     budget (about a second): typically other kernels held compute
+                                     units during a DLS_EXCLUSIVE_DEVICE call */
+#define DLS_DRAFT_ERR_PREPARED 2  /* head->prepared holds the prepared form of another head (its
+                                     header's shapes or tensor pointers differ from head's) */
+/* Copy the error word of `workspace` (a drafting workspace of ws_bytes >= 256 bytes, as
+ * passed to dls_draft_block) into *out_error, asynchronously on `stream` after the work
+ * already queued there: one int32 in memory the device can write (device memory, or host
+ * memory from hipHostMalloc).  Nothing is synchronised. */
+dls_status dls_draft_block_error(const void *workspace, size_t ws_bytes, int32_t *out_error,
+                                 void *stream);
 
 /* Per-position fusion weights (Sec. 5.6 learns one alpha_j and one beta_j for each
  * draft position; App. C lists them): host arrays of B values that replace fusion.alpha

@@ -52,7 +52,7 @@ class LocalHeadC(ctypes.Structure):
                 ("r", ctypes.c_int32), ("dtype", ctypes.c_int),
                 ("emb", ctypes.c_void_p), ("w_ih", ctypes.c_void_p), ("w_hh", ctypes.c_void_p),
                 ("w_rank", ctypes.c_void_p), ("w_vocab", ctypes.c_void_p), ("prepared", ctypes.c_void_p),
-                ("kind", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("kind", ctypes.c_int32), ("reserved", ctypes.c_int32), ("prepared_bytes", ctypes.c_size_t)]
 
 
 _lib = None
@@ -86,6 +86,8 @@ def lib() -> ctypes.CDLL:
         L.dls_prepare_head_size.argtypes = [ctypes.POINTER(LocalHeadC)]
         L.dls_prepare_head.restype = ctypes.c_int
         L.dls_prepare_head.argtypes = [ctypes.POINTER(LocalHeadC), _vp, _sz, _vp]
+        L.dls_draft_block_error.restype = ctypes.c_int
+        L.dls_draft_block_error.argtypes = [_vp, _sz, _vp, _vp]
         L.dls_draft_block_path.restype = ctypes.c_int
         L.dls_draft_block_path.argtypes = [ctypes.POINTER(LocalHeadC), _i32, _i32, ctypes.c_int, ctypes.c_int]
         L.dls_unigram_log_prior.restype = ctypes.c_int
@@ -185,11 +187,13 @@ class LocalHead:
         _check(L.dls_prepare_head(ctypes.byref(self.c), _ptr(buf), n, _stream(stream)))
         self.prepared = buf
         self.c.prepared = buf.data_ptr()
+        self.c.prepared_bytes = n
         return self
 
     def unprepare(self) -> "LocalHead":
         self.prepared = None
         self.c.prepared = None
+        self.c.prepared_bytes = 0
         return self
 
     def twin(self) -> "LocalHead":
@@ -255,9 +259,15 @@ def draft_workspace(head: LocalHead, batch: int, B: int, device=None) -> torch.T
     return torch.zeros(n, dtype=torch.uint8, device=device or head.emb.device)
 
 
-def workspace_error(workspace: torch.Tensor) -> int:
-    """The persistent kernel's error word (nonzero after a stalled hand-off); synchronises."""
-    return int(workspace[4:8].view(torch.int32).item())
+DLS_DRAFT_ERR_STALLED, DLS_DRAFT_ERR_PREPARED = 1, 2
+
+
+def workspace_error(workspace: torch.Tensor, stream=None) -> int:
+    """The error word of a drafting workspace, read through dls_draft_block_error after the work
+    queued on the stream; synchronises.  0, DLS_DRAFT_ERR_STALLED or DLS_DRAFT_ERR_PREPARED."""
+    out = torch.full((1,), -7, dtype=torch.int32, device=workspace.device)
+    _check(lib().dls_draft_block_error(_ptr(workspace), workspace.numel(), _ptr(out), _stream(stream)))
+    return int(out.item())
 
 
 def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional[torch.Tensor], prior=None,

@@ -7,22 +7,24 @@
 #include <cstdio>
 #include <cstring>
 #include <mutex>
-#include <string>
+#include <type_traits>
 
 #include "dels_internal.hpp"
 
 namespace {
 
-thread_local std::string g_last_error;
+// Process-lifetime state of the library is trivially destructible (plain arrays and flags):
+// the library registers no destructor that would run at process exit.
+thread_local char g_last_error[512];
+
+void clear_error() { g_last_error[0] = 0; }
 
 dls_status fail(dls_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 dls_status fail(dls_status s, const char* fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
+  vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
   va_end(ap);
-  g_last_error = buf;
   return s;
 }
 
@@ -32,10 +34,11 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 // id is computed once; it never changes during the life of the process.
 struct DevInfo {
   std::once_flag once;
-  bool ok = false;
-  int cus = 0;
-  std::string why;
+  bool ok;
+  int cus;
+  char why[160];
 };
+static_assert(std::is_trivially_destructible<DevInfo>::value, "no exit-time destructor");
 DevInfo g_dev[64];
 
 dls_status check_device(int* cus = nullptr) {
@@ -51,11 +54,11 @@ dls_status check_device(int* cus = nullptr) {
     hipDeviceProp_t p;
     hipError_t pe = hipGetDeviceProperties(&p, dev);
     if (pe != hipSuccess) {
-      di.why = std::string("hipGetDeviceProperties failed: ") + hipGetErrorString(pe);
+      snprintf(di.why, sizeof di.why, "hipGetDeviceProperties failed: %s", hipGetErrorString(pe));
       return;
     }
     if (std::strncmp(p.gcnArchName, "gfx950", 6) != 0) {
-      di.why = std::string("device is ") + p.gcnArchName + ", the library is built for gfx950 only";
+      snprintf(di.why, sizeof di.why, "device is %s, the library is built for gfx950 only", p.gcnArchName);
       return;
     }
     int coop = 0;
@@ -63,7 +66,7 @@ dls_status check_device(int* cus = nullptr) {
     di.cus = coop ? p.multiProcessorCount : 0;
     di.ok = true;
   });
-  if (!di.ok) return fail(DLS_ERR_DEVICE, "%s", di.why.c_str());
+  if (!di.ok) return fail(DLS_ERR_DEVICE, "%s", di.why);
   if (cus) *cus = di.cus;
   return DLS_OK;
 }
@@ -136,7 +139,7 @@ const char* dls_status_string(dls_status s) {
   return "DLS_UNKNOWN_STATUS";
 }
 
-const char* dls_last_error(void) { return g_last_error.c_str(); }
+const char* dls_last_error(void) { return g_last_error; }
 
 int dls_abi_version(void) { return DLS_ABI_VERSION; }
 
@@ -153,7 +156,7 @@ dls_status dls_combine_logits(const void* long_logits, const void* short_logits,
                               const float* prior, int64_t rows, int32_t V, dls_fusion fusion,
                               int32_t* out_token, dls_row_stats* out_stats, float* out_scores,
                               void* workspace, size_t ws_bytes, void* stream) {
-  g_last_error.clear();
+  clear_error();
   if (!valid_dtype(dtype)) return fail(DLS_ERR_DTYPE, "unknown dtype %d", (int)dtype);
   if (rows < 0 || rows > (1 << 20)) return fail(DLS_ERR_SHAPE, "rows=%lld outside [0, 2^20]", (long long)rows);
   if (V < 1 || V > (1 << 24)) return fail(DLS_ERR_SHAPE, "V=%d outside [1, 2^24]", V);
@@ -195,12 +198,12 @@ dls_status dls_combine_logits(const void* long_logits, const void* short_logits,
 
 size_t dls_prepare_head_size(const dls_local_head* head) {
   if (!head || check_head(head) != DLS_OK) return 0;
-  g_last_error.clear();
+  clear_error();
   return dls::prepared_layout(canon(*head)).total;
 }
 
 dls_status dls_prepare_head(const dls_local_head* head, void* prepared, size_t bytes, void* stream) {
-  g_last_error.clear();
+  clear_error();
   dls_status s = check_head(head);
   if (s != DLS_OK) return s;
   if (head->dtype != DLS_BF16) return fail(DLS_ERR_DTYPE, "only bf16 heads can be prepared");
@@ -220,7 +223,7 @@ dls_status dls_prepare_head(const dls_local_head* head, void* prepared, size_t b
 
 size_t dls_draft_block_workspace_size(const dls_local_head* head, int32_t batch, int32_t B) {
   if (!head || batch <= 0 || B <= 0 || check_head(head) != DLS_OK) return 0;
-  g_last_error.clear();
+  clear_error();
   const dls_local_head ch = canon(*head);
   // persistent region first (its header must start zero-filled), per-launch region after it
   return dls::persist_workspace(ch, batch, B).total + dls::draft_layout(ch, batch, B).total;
@@ -230,12 +233,25 @@ size_t dls_draft_block_workspace_size(const dls_local_head* head, int32_t batch,
 
 namespace {
 
+// Checks of a prepared buffer that need no device access: its stated size.
+dls_status check_prepared_size(const dls_local_head* head) {
+  if (!head->prepared) return DLS_OK;
+  const size_t need = dls::prepared_layout(canon(*head)).total;
+  if (head->prepared_bytes < need)
+    return fail(DLS_ERR_WORKSPACE, "head.prepared_bytes = %zu, but this head's prepared form needs %zu bytes",
+                head->prepared_bytes, need);
+  if (!aligned(head->prepared, 256)) return fail(DLS_ERR_ARG, "head.prepared is not 256-byte aligned");
+  return DLS_OK;
+}
+
+// The drafting entry points.
 dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,
                       const int32_t* last_token, const float* prior, int32_t batch, int32_t B, dls_fusion fusion,
                       const float* alphas, const float* betas, dls_sampling sampling, int32_t* out_tokens,
                       dls_row_stats* out_stats, void* workspace, size_t ws_bytes, void* stream) {
   dls_status s = check_head(head);
   if (s != DLS_OK) return s;
+  if ((s = check_prepared_size(head)) != DLS_OK) return s;
   if (!valid_dtype(long_dtype)) return fail(DLS_ERR_DTYPE, "unknown long-logit dtype %d", (int)long_dtype);
   if (batch < 0 || batch > 256) return fail(DLS_ERR_SHAPE, "batch=%d outside [0, 256]", batch);
   if (B < 0 || B > 64) return fail(DLS_ERR_SHAPE, "B=%d outside [0, 64]", B);
@@ -276,6 +292,16 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_d
       const char* pp = (const char*)head->prepared;
       char* ws = (char*)workspace;
       dls::PersistArgs pa;
+      pa.prep = (const dls::PreparedHeader*)pp;
+      pa.expect.magic = dls::kPreparedMagic;
+      pa.expect.V = ch.V;
+      pa.expect.d = ch.d;
+      pa.expect.H = ch.H;
+      pa.expect.r = ch.r;
+      pa.expect.emb = ch.emb;
+      pa.expect.w_ih = ch.w_ih;
+      pa.expect.w_hh = ch.w_hh;
+      pa.expect.w_vocab = ch.w_vocab;
       pa.T = (const float*)(pp + PL.off_T);
       pa.wv = (const uint4*)(pp + PL.off_wv);
       pa.whh = (const uint4*)(pp + PL.off_whh);
@@ -348,7 +374,7 @@ dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, 
                            const int32_t* last_token, const float* prior, int32_t batch, int32_t B,
                            dls_fusion fusion, int32_t* out_tokens, dls_row_stats* out_stats, void* workspace,
                            size_t ws_bytes, void* stream) {
-  g_last_error.clear();
+  clear_error();
   return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, nullptr, nullptr,
                     dls_sampling{0.f, 0u, 0ull}, out_tokens, out_stats, workspace, ws_bytes, stream);
 }
@@ -357,7 +383,7 @@ dls_status dls_draft_block_scheduled(const dls_local_head* head, const void* lon
                                      const int32_t* last_token, const float* prior, int32_t batch, int32_t B,
                                      dls_fusion fusion, dls_fusion_schedule schedule, int32_t* out_tokens,
                                      dls_row_stats* out_stats, void* workspace, size_t ws_bytes, void* stream) {
-  g_last_error.clear();
+  clear_error();
   return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, schedule.alpha,
                     schedule.beta, dls_sampling{0.f, 0u, 0ull}, out_tokens, out_stats, workspace, ws_bytes, stream);
 }
@@ -367,15 +393,28 @@ dls_status dls_draft_block_sampled(const dls_local_head* head, const void* long_
                                    dls_fusion fusion, dls_fusion_schedule schedule, dls_sampling sampling,
                                    int32_t* out_tokens, dls_row_stats* out_stats, void* workspace, size_t ws_bytes,
                                    void* stream) {
-  g_last_error.clear();
+  clear_error();
   return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, schedule.alpha,
                     schedule.beta, sampling, out_tokens, out_stats, workspace, ws_bytes, stream);
 }
 
+dls_status dls_draft_block_error(const void* workspace, size_t ws_bytes, int32_t* out_error, void* stream) {
+  clear_error();
+  if (!out_error || !aligned(out_error, 4)) return fail(DLS_ERR_ARG, "out_error is NULL or misaligned");
+  if (!workspace || ws_bytes < 256 || !aligned(workspace, 256))
+    return fail(DLS_ERR_WORKSPACE, "a drafting workspace has at least 256 bytes and is 256-byte aligned");
+  dls_status s = check_device();
+  if (s != DLS_OK) return s;
+  hipError_t e = dls::launch_copy_word((const uint32_t*)workspace + 1, out_error, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "draft_block_error launch");
+  return DLS_OK;
+}
+
 int dls_draft_block_path(const dls_local_head* head, int32_t batch, int32_t B, dls_dtype long_dtype,
                          int has_prior) {
-  g_last_error.clear();
-  if (check_head(head) != DLS_OK || !valid_dtype(long_dtype) || batch < 1 || batch > 256 || B < 1 || B > 64)
+  clear_error();
+  if (check_head(head) != DLS_OK || check_prepared_size(head) != DLS_OK || !valid_dtype(long_dtype) || batch < 1 ||
+      batch > 256 || B < 1 || B > 64)
     return -1;
   if (!head->prepared) return 0;
   int cus = 0;
@@ -387,7 +426,7 @@ int dls_draft_block_path(const dls_local_head* head, int32_t batch, int32_t B, d
 
 dls_status dls_unigram_log_prior(const int32_t* tokens, int64_t n, int32_t V, float smoothing, uint64_t* out_counts,
                                  float* out_log_prior, void* stream) {
-  g_last_error.clear();
+  clear_error();
   if (n < 0 || n > ((int64_t)1 << 40)) return fail(DLS_ERR_SHAPE, "n=%lld outside [0, 2^40]", (long long)n);
   if (V < 1 || V > (1 << 24)) return fail(DLS_ERR_SHAPE, "V=%d outside [1, 2^24]", V);
   if (!(smoothing >= 0.f) || !std::isfinite(smoothing)) return fail(DLS_ERR_ARG, "smoothing must be finite and >= 0");
@@ -403,7 +442,7 @@ dls_status dls_unigram_log_prior(const int32_t* tokens, int64_t n, int32_t V, fl
 
 dls_status dls_accept_len(const int32_t* draft, const int32_t* target, int32_t batch, int32_t B, int32_t* out_len,
                           void* stream) {
-  g_last_error.clear();
+  clear_error();
   if (batch < 0 || batch > (1 << 24)) return fail(DLS_ERR_SHAPE, "batch=%d outside [0, 2^24]", batch);
   if (B < 0 || B > 4096) return fail(DLS_ERR_SHAPE, "B=%d outside [0, 4096]", B);
   if (batch == 0) return DLS_OK;

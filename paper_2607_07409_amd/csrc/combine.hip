@@ -21,8 +21,8 @@ constexpr int kUnroll = 2;
 // l_v for one element (the GPU's float32 reading of the fusion equation)
 template <bool PRIOR>
 __device__ __forceinline__ float fuse1(float a, float b, float p, float wl, float al, float be) {
-  float f = __builtin_fmaf(al, b, wl * a);
-  if (PRIOR) f = __builtin_fmaf(-be, p, f);
+  float f = __builtin_fmaf(al, b, weighted(wl, a));
+  if (PRIOR) f = minus_weighted(f, be, p);
   return f;
 }
 

@@ -51,6 +51,14 @@ template <> struct Chunk<float> {
   }
 };
 
+// w * x, except that a zero weight gives 0 even for x = -inf: a fusion term weighted by 0 is
+// absent (p^0 = 1), masked entries (-inf long logits, an unsmoothed prior's -inf) included
+__device__ __forceinline__ float weighted(float w, float x) { return w == 0.f ? 0.f : w * x; }
+// f - b * p with the same reading of a zero weight
+__device__ __forceinline__ float minus_weighted(float f, float b, float p) {
+  return b == 0.f ? f : __builtin_fmaf(-b, p, f);
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 

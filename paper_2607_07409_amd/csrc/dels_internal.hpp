@@ -21,7 +21,7 @@ __device__ __forceinline__ void finalize_row(const Partial& P, float wl, float a
   *tok = t;
   const float lse_l = lse_value(P.L);
   const float lse_s = long_only ? __builtin_nanf("") : lse_value(P.S);
-  const float nr = long_only ? wl * lse_l : __builtin_fmaf(al, lse_s, wl * lse_l);
+  const float nr = long_only ? weighted(wl, lse_l) : __builtin_fmaf(al, lse_s, weighted(wl, lse_l));
   if (st) {
     const float ft = P.t1 - g_tok;   // l_tok / T
     st->score = ft * temp - nr;
@@ -105,7 +105,14 @@ struct PreparedLayout {
 PreparedLayout prepared_layout(const dls_local_head& h);
 hipError_t launch_prepare(const dls_local_head& h, void* buf, hipStream_t st);
 
+// error word of a persistent drafting workspace (the second uint32 of its header)
+constexpr uint32_t kErrStalled = DLS_DRAFT_ERR_STALLED;
+constexpr uint32_t kErrPrepared = DLS_DRAFT_ERR_PREPARED;
+hipError_t launch_copy_word(const uint32_t* src, int32_t* dst, hipStream_t st);
+
 struct PersistArgs {
+  const PreparedHeader* prep;   // header of the prepared buffer, and what it must hold
+  PreparedHeader expect;
   const float* T;            // folded input projection [V][3H]
   const uint4* wv;           // W_vocab tiles in MFMA operand order
   const uint4* whh;          // W_hh in MFMA operand order, per 16-unit group

@@ -226,11 +226,11 @@ __global__ __launch_bounds__(kThreads) void k_lmhead(const WT* __restrict__ w_vo
         float a = to_f32(lrow[v]);
         float f;
         if (long_only) {
-          f = wl * a;
+          f = weighted(wl, a);
         } else {
           float s = s_S[b * slice + i];
-          f = __builtin_fmaf(al, s, wl * a);
-          if (PRIOR) f = __builtin_fmaf(-be, prior[v], f);
+          f = __builtin_fmaf(al, s, weighted(wl, a));
+          if (PRIOR) f = minus_weighted(f, be, prior[v]);
           lse_fold<1>(P.S, &s, s);
         }
         lse_fold<1>(P.L, &a, a);

@@ -103,6 +103,17 @@ PersistWorkspace persist_workspace(const dls_local_head& h, int32_t batch, int32
   return L;
 }
 
+namespace {
+__global__ void k_copy_word(const uint32_t* src, int32_t* dst) {
+  *dst = (int32_t)__hip_atomic_load(src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+}  // namespace
+
+hipError_t launch_copy_word(const uint32_t* src, int32_t* dst, hipStream_t st) {
+  k_copy_word<<<1, 1, 0, st>>>(src, dst);
+  return hipGetLastError();
+}
+
 hipError_t launch_persistent(const PersistArgs& pa, const PersistPlan& pl, dls_dtype long_dtype, hipStream_t st) {
   const bool sample = pa.smp.inv_temp != 0.f;
   switch (pa.r / 32) {

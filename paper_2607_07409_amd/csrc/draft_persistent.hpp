@@ -102,7 +102,7 @@ __device__ __forceinline__ bool wait_tag(const uint64_t* p, uint32_t tag, uint32
     if ((uint32_t)(v >> 32) == tag) return true;
     if ((s & 63) == 0 && ld32(err)) return false;
     if (s > kMaxSpins) {
-      st32(err, 1u);
+      st32(err, kErrStalled);
       return false;
     }
   }
@@ -117,7 +117,7 @@ __device__ __forceinline__ bool wait_key(const uint64_t* p, uint32_t tag8, uint3
     if ((uint32_t)(v & 0xffu) == tag8) return true;
     if ((s & 63) == 0 && ld32(err)) return false;
     if (s > kMaxSpins) {
-      st32(err, 1u);
+      st32(err, kErrStalled);
       return false;
     }
   }
@@ -385,7 +385,7 @@ __device__ __forceinline__ bool stage_poll_words(const uint64_t* src, int rows, 
         break;
       }
       if (sp > kMaxSpins) {
-        st32(err, 1u);
+        st32(err, kErrStalled);
         ok = false;
         break;
       }
@@ -450,7 +450,7 @@ __device__ __forceinline__ bool stage_poll_pairs(const uint64_t* src, int rows, 
         break;
       }
       if (sp > kMaxSpins) {
-        st32(err, 1u);
+        st32(err, kErrStalled);
         ok = false;
         break;
       }
@@ -505,7 +505,7 @@ __device__ __forceinline__ bool poll_quads(const uint32_t* src, int nb, int HC, 
     __builtin_amdgcn_s_sleep(2);
     if ((sp & 63) == 63 && ld32(err)) return false;
     if (sp > kMaxSpins) {
-      st32(err, 1u);
+      st32(err, kErrStalled);
       return false;
     }
   }
@@ -550,7 +550,7 @@ __device__ __forceinline__ void wait_producers(const uint64_t* src0, size_t pstr
       __builtin_amdgcn_s_sleep(4);
       if ((sp & 63) == 63 && ld32(err)) break;
       if (sp > kMaxSpins) {
-        st32(err, 1u);
+        st32(err, kErrStalled);
         break;
       }
     }
@@ -632,7 +632,6 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   const bool gru = w < a.NG;
   const int KKH = H / 32;
   uint32_t* err = a.hdr + 1;
-  if (ld32(err)) return;
   const uint32_t epoch_full = ld32(a.hdr);
   const uint32_t epoch = epoch_full & 0xffffffu;
   const int set = (int)(epoch & 1u);
@@ -676,7 +675,33 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   int* s_tok = (int*)p;                             // kMaxBatch
   p += (size_t)kMaxBatch * 4;
   lds_flag_t* s_fail = (lds_flag_t*)p;              // sticky failure flag
-  if (tid == 0) *s_fail = 0;
+
+  // A failed call leaves outputs that cannot pass for a draft: token -1 at every position
+  // (workgroup 0 is the only writer of tokens) and NaN in every statistics row (row q is
+  // merged, and on failure overwritten, by workgroup q mod G alone).
+  auto bail = [&]() {
+    if (w == 0)
+      for (int i = tid; i < batch * Bk; i += kT) a.out_tokens[i] = -1;
+    if (a.out_stats && tid < 6)
+      for (int q = w; q < batch * Bk; q += G) ((float*)(a.out_stats + q))[tid] = __builtin_nanf("");
+  };
+  // Entry: an earlier failure on this workspace (the error word is sticky until the workspace
+  // is zero-filled), or a prepared buffer that does not belong to this head (its header holds
+  // the shapes and tensor pointers dls_prepare_head was given), ends the call at once.
+  if (tid == 0) {
+    const PreparedHeader* ph = a.prep;
+    const PreparedHeader& ex = a.expect;
+    const bool mismatch = ph->magic != ex.magic || ph->V != ex.V || ph->d != ex.d || ph->H != ex.H ||
+                          ph->r != ex.r || ph->emb != ex.emb || ph->w_ih != ex.w_ih || ph->w_hh != ex.w_hh ||
+                          ph->w_vocab != ex.w_vocab;
+    if (mismatch) st32(err, kErrPrepared);
+    *s_fail = (mismatch || ld32(err) != 0u) ? 1 : 0;
+  }
+  __syncthreads();
+  if (*s_fail) {
+    bail();
+    return;
+  }
 
   // ---- clear this workgroup's key slots of the other set (read by the next call)
   for (int i = tid; i < 2 * kMaxBatch; i += kT) {
@@ -790,7 +815,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
             break;
           }
           if (sp > kMaxSpins) {
-            st32(err, 1u);
+            st32(err, kErrStalled);
             ok = false;
             break;
           }
@@ -857,7 +882,10 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       uint64_t* hnew = a.hbuf + (size_t)par * batch * H;
       uint32_t* h32new = NARROW ? nullptr : a.h32 + (size_t)set * kH32Set + (size_t)par * kMaxBatch * H;
       if (j > 0) {
-        if (!merge_position(j - 1)) return;
+        if (!merge_position(j - 1)) {
+          bail();
+          return;
+        }
       } else {
         for (int b = tid; b < batch; b += kT) {
           const int u = a.last[b];
@@ -946,7 +974,10 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
             }
           }
         }
-        if (fail_barrier(!ok, s_fail)) return;
+        if (fail_barrier(!ok, s_fail)) {
+          bail();
+          return;
+        }
       }
       // rho_i = SiLU(W_rank h_{j+1}) for the owned rank rows (MFMA over the staged h, K split
       // over the waves), then W_hh h_{j+1} for the next position from the same staged h
@@ -1015,7 +1046,10 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
           }
         }
         if (n16 < rpg) s_rred[(wave * 4 + g4) * rpg + n16] = racc;
-        if (fail_barrier(!ok, s_fail)) return;
+        if (fail_barrier(!ok, s_fail)) {
+          bail();
+          return;
+        }
         if (wave == 0 && n16 < rpg) {
           f32x4_t sm = s_rred[g4 * rpg + n16];
           for (int q = 1; q < 4; ++q) sm += s_rred[(q * 4 + g4) * rpg + n16];
@@ -1046,14 +1080,20 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
             }
           }
         }
-        if (fail_barrier(!ok, s_fail)) return;
+        if (fail_barrier(!ok, s_fail)) {
+          bail();
+          return;
+        }
       }
     }
 
     // ======================= Markov head: the previous token (all workgroups) =======================
     if (MARKOV && !long_only) {
       if (j > 0) {
-        if (!merge_position(j - 1)) return;
+        if (!merge_position(j - 1)) {
+          bail();
+          return;
+        }
       } else {
         for (int b = tid; b < batch; b += kT) {
           const int u = a.last[b];
@@ -1157,7 +1197,10 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         }
         const bool ok = NARROW ? stage_poll_words<kInf>(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err)
                                : stage_poll_pairs<kInf>(rsrc, nb, r, r, tag, s_hi, s_lo, r + 8, err);
-        if (fail_barrier(!ok, s_fail)) return;
+        if (fail_barrier(!ok, s_fail)) {
+          bail();
+          return;
+        }
         if (PACK) {
           // rows 0..3 of the A operand carry the hi halves of slots 0..3, rows 4..7 the lo
           // halves (rows past the batch repeat slot 0, rows 8..15 are unused)
@@ -1231,8 +1274,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
             const float x = ok ? xr : -INFINITY;
             const float sv = PACK ? s_stash[(g4 * 4 + i) * 16 + n16] + s_stash[((4 + g4) * 4 + i) * 16 + n16]
                                   : s_stash[(g4 * 4 + i) * 16 + n16];
-            float f = __builtin_fmaf(alx, sv, wl * x);
-            if (PRIOR) f = __builtin_fmaf(-bex, s_prior[rowc], f);
+            float f = __builtin_fmaf(alx, sv, weighted(wl, x));
+            if (PRIOR) f = minus_weighted(f, bex, s_prior[rowc]);
             f = ok ? f : -INFINITY;
             lse_push_fin(P[i].S, ok && !long_only ? sv : -INFINITY);
             lse_push_fin(P[i].L, x);
@@ -1261,8 +1304,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
             const bool ok = slot < nb && vin;
             const float xr = to_f32(s_ll[(ok ? slot : 0) * a.rows_max + row]);
             const float x = ok ? xr : -INFINITY;
-            float f = __builtin_fmaf(alx, acc[i], wl * x);
-            if (PRIOR) f = __builtin_fmaf(-bex, s_prior[row], f);
+            float f = __builtin_fmaf(alx, acc[i], weighted(wl, x));
+            if (PRIOR) f = minus_weighted(f, bex, s_prior[row]);
             f = ok ? f : -INFINITY;
             lse_push_fin(P[i].S, ok && !long_only ? acc[i] : -INFINITY);
             lse_push_fin(P[i].L, x);
@@ -1398,7 +1441,10 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
 
   // ---- the last position's tokens (workgroup 0)
   if (w == 0) {
-    if (!merge_position(Bk - 1)) return;
+    if (!merge_position(Bk - 1)) {
+      bail();
+      return;
+    }
   }
   // ---- row statistics: row (b, j) is merged by workgroup (b * B + j) % G from the tagged partials
   if (a.out_stats) {
@@ -1424,7 +1470,10 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         P.t1 = q9[6]; P.t2 = q9[7];
         P.i1 = __float_as_int(q9[8]);
       }
-      if (fail_barrier(!ok, s_fail)) return;
+      if (fail_barrier(!ok, s_fail)) {
+        bail();
+        return;
+      }
       P = block_merge(P, s_part, 4);
       if (tid == 0) {
         int t;

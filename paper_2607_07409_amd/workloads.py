@@ -268,6 +268,29 @@ def make_long_logits(wl: Workload, seed: Optional[int] = None):
     return Bf16Array(out) if wl.dtype == "bf16" else out
 
 
+def mask_long_logits(long, frac: float, seed: int, single=()):
+    """A copy of stored long logits [batch, B, V] with a seeded fraction of the entries set to -inf
+    (masked tokens); each (b, j) in `single` keeps one finite entry only, at a seeded token.
+    Returns (masked copy, {(b, j): the kept token})."""
+    g = _rng(seed, 40)
+    bf = isinstance(long, Bf16Array)
+    arr = long.bits.copy() if bf else np.array(long, dtype=np.float32, copy=True)
+    neg_inf = np.uint16(0xFF80) if bf else np.float32(-np.inf)
+    arr[g.random(arr.shape) < frac] = neg_inf
+    kept = {}
+    for (b, j) in single:
+        t = int(g.integers(0, arr.shape[2]))
+        keep = arr[b, j, t]
+        if bf and keep == neg_inf:
+            keep = np.uint16(0x3F80)          # 1.0
+        elif not bf and not np.isfinite(keep):
+            keep = np.float32(1.0)
+        arr[b, j, :] = neg_inf
+        arr[b, j, t] = keep
+        kept[(b, j)] = t
+    return (Bf16Array(arr) if bf else arr), kept
+
+
 def make_zipf_log_prior(V: int, seed: int, s: float = 1.1) -> np.ndarray:
     """[V] fp32 log unigram prior of a Zipf(s) law over seeded ranks (a normalised log-distribution)."""
     ranks = zipf_ranks(V, seed).astype(np.float64)

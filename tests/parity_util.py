@@ -72,7 +72,7 @@ def check_draft(gpu_tok, gpu_stats, head, long_logits, last_token, prior, w_long
     active = 0
     for b in seqs:
         rows = np.asarray(long_logits[b], dtype=np.float32)
-        long_arg = np.argmax(rows * np.float32(w_long) if w_long != 1.0 else rows, axis=1)
+        long_arg = np.argmax(rows, axis=1)
         for j in range(B):
             if ref.argmax[b, j] != gt[b, j]:
                 assert ref.gap[b, j] < TOL and ref.margin[b, j] < TOL, (

@@ -44,10 +44,10 @@ def test_struct_layout_matches_c(tmp_path):
 #include <stddef.h>
 #include "{HEADER}"
 int main(void) {{
-  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(dls_local_head), sizeof(dls_row_stats),
+  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(dls_local_head), sizeof(dls_row_stats),
          sizeof(dls_fusion), offsetof(dls_local_head, dtype), offsetof(dls_local_head, emb),
          offsetof(dls_local_head, w_vocab), offsetof(dls_fusion, flags), offsetof(dls_local_head, kind),
-         sizeof(dls_sampling), offsetof(dls_sampling, seed));
+         sizeof(dls_sampling), offsetof(dls_sampling, seed), offsetof(dls_local_head, prepared_bytes));
   return 0;
 }}''')
     exe = tmp_path / "lay"
@@ -55,13 +55,14 @@ int main(void) {{
     got = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True).stdout.split()]
     want = [ctypes.sizeof(b.LocalHeadC), ctypes.sizeof(b.RowStats), ctypes.sizeof(b.Fusion),
             b.LocalHeadC.dtype.offset, b.LocalHeadC.emb.offset, b.LocalHeadC.w_vocab.offset,
-            b.Fusion.flags.offset, b.LocalHeadC.kind.offset, ctypes.sizeof(b.Sampling), b.Sampling.seed.offset]
+            b.Fusion.flags.offset, b.LocalHeadC.kind.offset, ctypes.sizeof(b.Sampling), b.Sampling.seed.offset,
+            b.LocalHeadC.prepared_bytes.offset]
     assert got == want
 
 
 def test_header_compiles_as_cpp(tmp_path):
     src = tmp_path / "h.cpp"
-    src.write_text(f'#include "{HEADER}"\nint main() {{ return dls_abi_version() == 2 ? 0 : 1; }}\n')
+    src.write_text(f'#include "{HEADER}"\nint main() {{ return dls_abi_version() == 3 ? 0 : 1; }}\n')
     subprocess.run(["g++", "-std=c++17", "-Wall", "-Werror", "-c", str(src), "-o", str(tmp_path / "h.o")],
                    check=True)
 
@@ -71,7 +72,7 @@ def test_status_strings():
     for code, name in b.STATUS.items():
         assert L.dls_status_string(code).decode() == name
     assert L.dls_status_string(99).decode() == "DLS_UNKNOWN_STATUS"
-    assert L.dls_abi_version() == 2
+    assert L.dls_abi_version() == 3
 
 
 def _head(**kw):
@@ -252,3 +253,34 @@ def test_unigram_prior_rejects_bad_arguments():
     if not HAS_GPU:
         assert call() == "DLS_ERR_DEVICE"
         assert call(tokens=None, n=0) == "DLS_ERR_DEVICE"
+
+
+def test_prepared_buffer_size_is_checked():
+    """A prepared buffer smaller than the head's prepared form, or misaligned, is refused on the
+    host (the kernel would read past its end)."""
+    L = b.lib()
+    h = _head(V=4096, d=64, H=64, r=128)
+    need = L.dls_prepare_head_size(ctypes.byref(h))
+    assert need > 0
+    small = _head(V=4096, d=64, H=64, r=128, prepared=FAKE[10].value, prepared_bytes=need - 1)
+    rc, msg = _draft(small)
+    assert b.STATUS[rc] == "DLS_ERR_WORKSPACE" and "prepared" in msg, msg
+    assert L.dls_draft_block_path(ctypes.byref(small), 2, 4, b.DLS_BF16, 0) == -1
+    skew = _head(V=4096, d=64, H=64, r=128, prepared=FAKE[10].value + 16, prepared_bytes=need)
+    assert b.STATUS[_draft(skew)[0]] == "DLS_ERR_ARG"
+    ok = _head(V=4096, d=64, H=64, r=128, prepared=FAKE[10].value, prepared_bytes=need)
+    if not HAS_GPU:
+        assert b.STATUS[_draft(ok)[0]] == "DLS_ERR_DEVICE"
+
+
+def test_error_query_rejects_bad_arguments():
+    L = b.lib()
+    assert b.STATUS[L.dls_draft_block_error(FAKE[0], 1 << 20, None, None)] == "DLS_ERR_ARG"
+    assert b.STATUS[L.dls_draft_block_error(FAKE[0], 1 << 20, ctypes.c_void_p(FAKE[1].value + 2), None)] == \
+        "DLS_ERR_ARG"
+    assert b.STATUS[L.dls_draft_block_error(FAKE[0], 64, FAKE[1], None)] == "DLS_ERR_WORKSPACE"
+    assert b.STATUS[L.dls_draft_block_error(None, 0, FAKE[1], None)] == "DLS_ERR_WORKSPACE"
+    assert b.STATUS[L.dls_draft_block_error(ctypes.c_void_p(FAKE[0].value + 16), 1 << 20, FAKE[1], None)] == \
+        "DLS_ERR_WORKSPACE"
+    if not HAS_GPU:
+        assert b.STATUS[L.dls_draft_block_error(FAKE[0], 1 << 20, FAKE[1], None)] == "DLS_ERR_DEVICE"

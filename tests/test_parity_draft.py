@@ -118,21 +118,56 @@ def test_qwen3_8b_b1_alpha_zero_is_dflash(prepared):
 @pytest.mark.parametrize("prepared", [False, True])
 @pytest.mark.parametrize("init", ["baseline", "stress"])
 def test_serving_b16(init, prepared):
+    """Every sequence of the batch-16 workload, element by element against the oracle."""
     p = _problem("qwen3-8b-b16", init)
-    _check(p, 0.5, sequences=[0, 5, 10, 15], prepared=prepared)
+    _check(p, 0.5, prepared=prepared)
 
 
 @pytest.mark.parametrize("prepared", [False, True])
 def test_serving_b64(prepared):
+    """Every sequence of the batch-64 workload (four 16-sequence M tiles of the wide kernel)."""
     p = _problem("b64-d5120", "stress")
-    _check(p, 0.5, sequences=[0, 21, 42, 63], prepared=prepared)
+    _check(p, 0.5, prepared=prepared)
 
 
 @pytest.mark.parametrize("prepared", [False, True])
 def test_serving_b64_prior(prepared):
-    """beta = alpha with the Zipf log-prior (the paper's alpha = beta diagonal)."""
+    """beta = alpha with the Zipf log-prior (the paper's alpha = beta diagonal), every sequence."""
     p = _problem("b64-d5120", "stress")
-    _check(p, 0.5, 0.5, with_prior=True, sequences=[1, 62], prepared=prepared)
+    _check(p, 0.5, 0.5, with_prior=True, prepared=prepared)
+
+
+@pytest.mark.parametrize("prepared", [False, True])
+@pytest.mark.parametrize("w_long", [1.0, 0.0])
+@pytest.mark.parametrize("name", ["qwen3-4b-b1", "qwen3-8b-b16", "b64-d5120"])
+def test_masked_long_logits(name, w_long, prepared):
+    """-inf long logits (masked tokens, allowed by the ABI) through dls_draft_block, every sequence:
+    narrow (batch 1) and wide (batch 16: one M tile; batch 64: four) persistent kernels and the
+    per-position launches.  With w_long = 1 a masked token is never drafted, and a row that keeps a
+    single finite entry drafts that entry; with w_long = 0 the long term, masks included, is absent
+    (the head alone decides).  Statistics against the oracle within the tolerance."""
+    p = _problem(name, "stress")
+    wl = p["wl"]
+    single = [(0, 2), (wl.batch - 1, wl.B - 1)]
+    masked, kept = W.mask_long_logits(p["long_h"], 0.3, 17, single)
+    lt = B.as_tensor(masked)
+    last = torch.from_numpy(p["last"]).cuda()
+    head = _head(p, prepared)
+    assert head.path(wl.batch, wl.B, lt.dtype, False) == (1 if prepared else 0)
+    ws = B.draft_workspace(head, wl.batch, wl.B)
+    tok, st = B.draft_block(head, lt, last, None, w_long, 0.5, 0.0, workspace=ws)
+    torch.cuda.synchronize()
+    assert B.workspace_error(ws) == 0
+    tok, st = tok.cpu().numpy(), st.cpu().numpy()
+    if w_long > 0:
+        bits = masked.bits
+        for b in range(wl.batch):
+            for j in range(wl.B):
+                assert bits[b, j, tok[b, j]] != 0xFF80, (b, j)
+        for (b, j), t in kept.items():
+            assert tok[b, j] == t, (b, j)
+    rep = check_draft(tok, st, p["oracle"], masked, p["last"], None, w_long, 0.5, 0.0)
+    print(f"{name} masked w_long={w_long}: near_ties={rep['near_ties']} errs={rep['errs']}")
 
 
 # ---------------------------------------------------------------------------------------------
