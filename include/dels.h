@@ -26,9 +26,10 @@
  *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).  Every
  *    call only enqueues work; nothing is synchronised.  Outputs are valid once the
  *    caller has synchronised the stream.
- *  - The library never allocates device memory in a call and holds no mutable
- *    global state.  Scratch memory is the caller's `workspace`; one workspace must
- *    not be used by two calls that may run concurrently.
+ *  - The library never allocates device memory in a call.  Scratch memory is the
+ *    caller's `workspace`; one workspace must not be used by two calls that may run
+ *    concurrently.  The only mutable global state is the per-GPU scratch array of
+ *    dls_draft_block_noalloc.
  *  - Arguments are checked on the host before any HIP call.  A failed check returns
  *    DLS_ERR_ARG / DLS_ERR_SHAPE / DLS_ERR_DTYPE / DLS_ERR_WORKSPACE and enqueues
  *    nothing.  No usable GPU gives DLS_ERR_DEVICE; a HIP failure gives DLS_ERR_HIP.
@@ -226,7 +227,8 @@ dls_status dls_draft_block(const dls_local_head *head, const void *long_logits,
 /* Copy the error word of `workspace` (a drafting workspace of ws_bytes >= 256 bytes, as
  * passed to dls_draft_block) into *out_error, asynchronously on `stream` after the work
  * already queued there: one int32 in memory the device can write (device memory, or host
- * memory from hipHostMalloc).  Nothing is synchronised. */
+ * memory from hipHostMalloc).  With workspace == NULL it reads the error word of the
+ * current device's scratch used by dls_draft_block_noalloc.  Nothing is synchronised. */
 dls_status dls_draft_block_error(const void *workspace, size_t ws_bytes, int32_t *out_error,
                                  void *stream);
 
@@ -267,6 +269,27 @@ dls_status dls_draft_block_sampled(const dls_local_head *head, const void *long_
                                    dls_fusion_schedule schedule, dls_sampling sampling,
                                    int32_t *out_tokens, dls_row_stats *out_stats, void *workspace,
                                    size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------------
+ * Allocation-free drafting.  For callers that cannot allocate device memory or own a
+ * workspace: code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation.  dls_draft_block without the workspace arguments: the call runs in a scratch
+ * array that the library holds in device memory, one per GPU, of
+ * DLS_NOALLOC_SCRATCH_BYTES (32 MiB, reserved on every GPU the library runs on until the
+ * process ends).  Calls whose dls_draft_block_workspace_size(head, batch, B) exceeds it
+ * return DLS_ERR_WORKSPACE; the Qwen3-shaped heads (H = 1024, r = 256) fit up to batch 64
+ * at B = 16.  The call allocates nothing and calls no allocating routine.  Every call on a
+ * GPU uses that GPU's one scratch array, which keeps the state of the previous call:
+ * calls that may overlap on one GPU (two streams, two threads) race and must be ordered
+ * by the caller.  Each call first enqueues a one-workgroup check that zero-fills the
+ * scratch when the previous call left its error word set, so a failed call (read its
+ * error with dls_draft_block_error(NULL, 0, ...)) does not affect the next one.
+ * Otherwise identical to dls_draft_block. */
+#define DLS_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+dls_status dls_draft_block_noalloc(const dls_local_head *head, const void *long_logits,
+                                   dls_dtype long_dtype, const int32_t *last_token,
+                                   const float *prior, int32_t batch, int32_t B, dls_fusion fusion,
+                                   int32_t *out_tokens, dls_row_stats *out_stats, void *stream);
 
 /* ---------------------------------------------------------------------------------
  * Prefix-acceptance length (verification step of Algorithm 1): out_len[b] is the

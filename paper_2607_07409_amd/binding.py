@@ -86,6 +86,9 @@ def lib() -> ctypes.CDLL:
         L.dls_prepare_head_size.argtypes = [ctypes.POINTER(LocalHeadC)]
         L.dls_prepare_head.restype = ctypes.c_int
         L.dls_prepare_head.argtypes = [ctypes.POINTER(LocalHeadC), _vp, _sz, _vp]
+        L.dls_draft_block_noalloc.restype = ctypes.c_int
+        L.dls_draft_block_noalloc.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
+                                              Fusion, _vp, _vp, _vp]
         L.dls_draft_block_error.restype = ctypes.c_int
         L.dls_draft_block_error.argtypes = [_vp, _sz, _vp, _vp]
         L.dls_draft_block_path.restype = ctypes.c_int
@@ -262,11 +265,14 @@ def draft_workspace(head: LocalHead, batch: int, B: int, device=None) -> torch.T
 DLS_DRAFT_ERR_STALLED, DLS_DRAFT_ERR_PREPARED = 1, 2
 
 
-def workspace_error(workspace: torch.Tensor, stream=None) -> int:
-    """The error word of a drafting workspace, read through dls_draft_block_error after the work
-    queued on the stream; synchronises.  0, DLS_DRAFT_ERR_STALLED or DLS_DRAFT_ERR_PREPARED."""
-    out = torch.full((1,), -7, dtype=torch.int32, device=workspace.device)
-    _check(lib().dls_draft_block_error(_ptr(workspace), workspace.numel(), _ptr(out), _stream(stream)))
+def workspace_error(workspace: Optional[torch.Tensor], stream=None) -> int:
+    """The error word of a drafting workspace (None: the scratch of draft_block_noalloc on the
+    current device), read through dls_draft_block_error after the work queued on the stream;
+    synchronises.  0, DLS_DRAFT_ERR_STALLED or DLS_DRAFT_ERR_PREPARED."""
+    dev = workspace.device if workspace is not None else torch.device("cuda", torch.cuda.current_device())
+    out = torch.full((1,), -7, dtype=torch.int32, device=dev)
+    _check(lib().dls_draft_block_error(_ptr(workspace), 0 if workspace is None else workspace.numel(), _ptr(out),
+                                       _stream(stream)))
     return int(out.item())
 
 
@@ -313,6 +319,25 @@ def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional
         _check(L.dls_draft_block(ctypes.byref(head.c), _ptr(long_logits), _dtype_code(long_logits),
                                  _ptr(last_token), _ptr(prior), batch, B, f, _ptr(tok), _ptr(st), _ptr(workspace),
                                  workspace.numel(), _stream(stream)))
+    return tok, st
+
+
+def draft_block_noalloc(head: LocalHead, long_logits: torch.Tensor, last_token: Optional[torch.Tensor], prior=None,
+                        w_long=1.0, alpha=0.3, beta=0.3, first_row_long_only=False, want_stats=True, out=None,
+                        stream=None, exclusive_device=False):
+    """draft_block through dls_draft_block_noalloc: no workspace, the library's per-GPU scratch."""
+    L = lib()
+    batch, B, V = long_logits.shape
+    dev = long_logits.device
+    if out is None:
+        tok = torch.empty((batch, B), dtype=torch.int32, device=dev)
+        st = torch.empty((batch, B, 6), dtype=torch.float32, device=dev) if want_stats else None
+    else:
+        tok, st = out
+    f = fusion(w_long, alpha, beta, first_row_long_only, exclusive_device)
+    _check(L.dls_draft_block_noalloc(ctypes.byref(head.c), _ptr(long_logits), _dtype_code(long_logits),
+                                     _ptr(last_token), _ptr(prior), batch, B, f, _ptr(tok), _ptr(st),
+                                     _stream(stream)))
     return tok, st
 
 

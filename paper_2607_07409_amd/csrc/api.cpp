@@ -244,11 +244,13 @@ dls_status check_prepared_size(const dls_local_head* head) {
   return DLS_OK;
 }
 
-// The drafting entry points.
+// The drafting entry points.  noalloc: run in the current device's scratch array instead of
+// the caller's workspace (workspace and ws_bytes are then ignored).
 dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,
                       const int32_t* last_token, const float* prior, int32_t batch, int32_t B, dls_fusion fusion,
                       const float* alphas, const float* betas, dls_sampling sampling, int32_t* out_tokens,
-                      dls_row_stats* out_stats, void* workspace, size_t ws_bytes, void* stream) {
+                      dls_row_stats* out_stats, void* workspace, size_t ws_bytes, void* stream,
+                      bool noalloc = false) {
   dls_status s = check_head(head);
   if (s != DLS_OK) return s;
   if ((s = check_prepared_size(head)) != DLS_OK) return s;
@@ -278,10 +280,28 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_d
       (out_stats && !aligned(out_stats, 4)))
     return fail(DLS_ERR_ARG, "misaligned vector argument");
   const size_t need = dls_draft_block_workspace_size(head, batch, B);
-  if (ws_bytes < need) return fail(DLS_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, need);
-  if (!workspace || !aligned(workspace, 256)) return fail(DLS_ERR_ARG, "workspace is NULL or not 256-byte aligned");
+  if (noalloc) {
+    if (need > dls::kNoallocScratchBytes)
+      return fail(DLS_ERR_WORKSPACE,
+                  "dls_draft_block_noalloc: batch %d, B %d of this head need %zu bytes of scratch, more than the "
+                  "library's %zu-byte array", batch, B, need, dls::kNoallocScratchBytes);
+  } else {
+    if (ws_bytes < need) return fail(DLS_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, need);
+    if (!workspace || !aligned(workspace, 256))
+      return fail(DLS_ERR_ARG, "workspace is NULL or not 256-byte aligned");
+  }
   int cus = 0;
   if ((s = check_device(&cus)) != DLS_OK) return s;
+  if (noalloc) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) workspace = dls::noalloc_scratch(dev, &e);
+    if (e != hipSuccess) return hip_fail(e, "draft_block_noalloc scratch address");
+    ws_bytes = dls::kNoallocScratchBytes;
+    // a failed previous call on this scratch: restore it before this call uses it
+    if ((e = dls::launch_scratch_guard(workspace, (hipStream_t)stream)) != hipSuccess)
+      return hip_fail(e, "draft_block_noalloc scratch check");
+  }
 
   const dls_local_head ch = canon(*head);
   const dls::PersistWorkspace pw = dls::persist_workspace(ch, batch, B);
@@ -398,14 +418,29 @@ dls_status dls_draft_block_sampled(const dls_local_head* head, const void* long_
                     schedule.beta, sampling, out_tokens, out_stats, workspace, ws_bytes, stream);
 }
 
+dls_status dls_draft_block_noalloc(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,
+                                   const int32_t* last_token, const float* prior, int32_t batch, int32_t B,
+                                   dls_fusion fusion, int32_t* out_tokens, dls_row_stats* out_stats, void* stream) {
+  clear_error();
+  return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, nullptr, nullptr,
+                    dls_sampling{0.f, 0u, 0ull}, out_tokens, out_stats, nullptr, 0, stream, true);
+}
+
 dls_status dls_draft_block_error(const void* workspace, size_t ws_bytes, int32_t* out_error, void* stream) {
   clear_error();
   if (!out_error || !aligned(out_error, 4)) return fail(DLS_ERR_ARG, "out_error is NULL or misaligned");
-  if (!workspace || ws_bytes < 256 || !aligned(workspace, 256))
+  if (workspace && (ws_bytes < 256 || !aligned(workspace, 256)))
     return fail(DLS_ERR_WORKSPACE, "a drafting workspace has at least 256 bytes and is 256-byte aligned");
   dls_status s = check_device();
   if (s != DLS_OK) return s;
-  hipError_t e = dls::launch_copy_word((const uint32_t*)workspace + 1, out_error, (hipStream_t)stream);
+  hipError_t e = hipSuccess;
+  if (!workspace) {
+    int dev = 0;
+    e = hipGetDevice(&dev);
+    if (e == hipSuccess) workspace = dls::noalloc_scratch(dev, &e);
+    if (e != hipSuccess) return hip_fail(e, "draft_block_error scratch address");
+  }
+  e = dls::launch_copy_word((const uint32_t*)workspace + 1, out_error, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "draft_block_error launch");
   return DLS_OK;
 }

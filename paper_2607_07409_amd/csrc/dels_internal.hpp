@@ -110,6 +110,12 @@ constexpr uint32_t kErrStalled = DLS_DRAFT_ERR_STALLED;
 constexpr uint32_t kErrPrepared = DLS_DRAFT_ERR_PREPARED;
 hipError_t launch_copy_word(const uint32_t* src, int32_t* dst, hipStream_t st);
 
+// the scratch of dls_draft_block_noalloc (noalloc.hip): the device address of the current
+// device's copy, and the check that restores it after a failed call
+constexpr size_t kNoallocScratchBytes = DLS_NOALLOC_SCRATCH_BYTES;
+void* noalloc_scratch(int dev, hipError_t* err);
+hipError_t launch_scratch_guard(void* dev_scratch, hipStream_t st);
+
 struct PersistArgs {
   const PreparedHeader* prep;   // header of the prepared buffer, and what it must hold
   PreparedHeader expect;

@@ -255,6 +255,40 @@ def test_unigram_prior_rejects_bad_arguments():
         assert call(tokens=None, n=0) == "DLS_ERR_DEVICE"
 
 
+def _noalloc(head, **kw):
+    a = dict(long=FAKE[5], ldt=b.DLS_BF16, last=FAKE[6], prior=None, batch=2, B=4, f=b.fusion(),
+             tok=FAKE[7], st=FAKE[8])
+    a.update(kw)
+    L = b.lib()
+    rc = L.dls_draft_block_noalloc(ctypes.byref(head), a["long"], a["ldt"], a["last"], a["prior"], a["batch"], a["B"],
+                                   a["f"], a["tok"], a["st"], None)
+    return rc, L.dls_last_error().decode()
+
+
+def test_noalloc_rejects_bad_arguments_and_oversized_calls():
+    """The allocation-free entry point applies the checks of dls_draft_block and refuses calls whose
+    workspace would exceed its fixed scratch array (32 MiB), before any device call."""
+    assert b.STATUS[_noalloc(_head(V=0))[0]] == "DLS_ERR_SHAPE"
+    assert b.STATUS[_noalloc(_head(), tok=None)[0]] == "DLS_ERR_ARG"
+    assert b.STATUS[_noalloc(_head(), batch=257)[0]] == "DLS_ERR_SHAPE"
+    assert _noalloc(_head(), batch=0, long=None, tok=None)[0] == 0
+    L = b.lib()
+    big = _head(V=151936, d=4096, H=4096, r=256)
+    need = L.dls_draft_block_workspace_size(ctypes.byref(big), 256, 64)
+    assert need > 32 << 20
+    rc, msg = _noalloc(big, batch=256, B=64)
+    assert b.STATUS[rc] == "DLS_ERR_WORKSPACE" and "scratch" in msg, msg
+    # the Qwen3-shaped heads fit up to batch 64 at B = 16
+    q = _head(V=151936, d=5120, H=1024, r=256)
+    assert L.dls_draft_block_workspace_size(ctypes.byref(q), 64, 16) <= 32 << 20
+
+
+@pytest.mark.skipif(HAS_GPU, reason="would launch on fake pointers when a GPU is present")
+def test_noalloc_valid_arguments_stop_at_device_check():
+    rc, msg = _noalloc(_head())
+    assert b.STATUS[rc] == "DLS_ERR_DEVICE", msg
+
+
 def test_prepared_buffer_size_is_checked():
     """A prepared buffer smaller than the head's prepared form, or misaligned, is refused on the
     host (the kernel would read past its end)."""
@@ -266,6 +300,7 @@ def test_prepared_buffer_size_is_checked():
     rc, msg = _draft(small)
     assert b.STATUS[rc] == "DLS_ERR_WORKSPACE" and "prepared" in msg, msg
     assert L.dls_draft_block_path(ctypes.byref(small), 2, 4, b.DLS_BF16, 0) == -1
+    assert b.STATUS[_noalloc(small)[0]] == "DLS_ERR_WORKSPACE"
     skew = _head(V=4096, d=64, H=64, r=128, prepared=FAKE[10].value + 16, prepared_bytes=need)
     assert b.STATUS[_draft(skew)[0]] == "DLS_ERR_ARG"
     ok = _head(V=4096, d=64, H=64, r=128, prepared=FAKE[10].value, prepared_bytes=need)
@@ -279,8 +314,8 @@ def test_error_query_rejects_bad_arguments():
     assert b.STATUS[L.dls_draft_block_error(FAKE[0], 1 << 20, ctypes.c_void_p(FAKE[1].value + 2), None)] == \
         "DLS_ERR_ARG"
     assert b.STATUS[L.dls_draft_block_error(FAKE[0], 64, FAKE[1], None)] == "DLS_ERR_WORKSPACE"
-    assert b.STATUS[L.dls_draft_block_error(None, 0, FAKE[1], None)] == "DLS_ERR_WORKSPACE"
     assert b.STATUS[L.dls_draft_block_error(ctypes.c_void_p(FAKE[0].value + 16), 1 << 20, FAKE[1], None)] == \
         "DLS_ERR_WORKSPACE"
     if not HAS_GPU:
         assert b.STATUS[L.dls_draft_block_error(FAKE[0], 1 << 20, FAKE[1], None)] == "DLS_ERR_DEVICE"
+        assert b.STATUS[L.dls_draft_block_error(None, 0, FAKE[1], None)] == "DLS_ERR_DEVICE"
