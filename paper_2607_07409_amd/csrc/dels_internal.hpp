@@ -140,8 +140,9 @@ struct PersistArgs {
   uint32_t* hdr;             // [0] call epoch, [1] error word
   uint64_t* keys;            // [2 sets][2 parities][kMaxBatch][G]
   uint64_t* hbuf;            // [2 parities][batch][H] (narrow batches)
-  uint32_t* h32;             // wide batches' h: [2 sets][2 parities][kMaxBatch][H] in a set stride of
+  uint32_t* h32;             // wide batches' h: [2 sets][2 parities][hrep][batch][H] in a set stride of
                              // kH32Set words; 24-bit h | 8-bit position tag; cleared by every call
+  int hrep;                  // replicas of the wide h words (a power of two, 2 hrep batch H <= kH32Set)
   uint64_t* rbuf;            // [replicas][2 parities][batch][r]
   uint64_t* stats;           // [B][batch][G][8] tagged LSE partials
 };

@@ -71,8 +71,14 @@ __device__ __forceinline__ float ldf(const float* p) {
 // `bytes` bytes from `base`; offsets past the end read as zeros.  A 16-byte aligned load lies
 // within one cache line: each of its two 64-bit words is read whole, as by ld64.  Polling loops
 // put a compiler barrier (poll_fence) before each round, so that every round loads again.
+// The base and size are wave-uniform wherever this is used; readfirstlane tells the compiler so,
+// which keeps the descriptor in scalar registers (a descriptor it takes for per-lane would turn
+// every load into a loop over the lanes' distinct descriptors).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t coherent_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+  const uint64_t b = (uint64_t)(uintptr_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b), hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+  void* ub = (void*)(uintptr_t)(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(ub, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
 }
 __device__ __forceinline__ u32x4 ld128(__amdgpu_buffer_rsrc_t rs, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 16);   // sc1
@@ -175,6 +181,12 @@ __device__ __forceinline__ f32x4_t mfma_va(uint4 a, u32x4 b_agpr, f32x4_t c) {
   bb.u = b_agpr;
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(a), bb.b, c, 0, 0, 0);
 }
+// A operand resident in AGPRs (a W_vocab tile as the rows of the product)
+__device__ __forceinline__ f32x4_t mfma_av(u32x4 a_agpr, uint4 b, f32x4_t c) {
+  union { u32x4 u; bf16x8_t b; } aa;
+  aa.u = a_agpr;
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(aa.b, as_bf(b), c, 0, 0, 0);
+}
 __device__ __forceinline__ u32x4 to_agpr(uint4 v) {
   u32x4 r = {v.x, v.y, v.z, v.w};
   asm volatile("; weights -> agpr" : "=a"(r) : "0"(r));
@@ -197,7 +209,7 @@ __device__ __forceinline__ void lse_push(Lse& a, float x) {
 // lse_push for a running maximum that starts finite (kFinMin instead of -inf): no test of the
 // value is needed, since x = -inf gives d = -inf, a zero term and no new maximum.  Such a
 // state is empty while s == 0 (a push sets s >= 1); fin_to_empty restores the -inf form.
-constexpr float kFinMin = -3.0e38f;
+constexpr float kFinMin = -2.0e38f;   // kFinMin * log2(e) is still finite
 __device__ __forceinline__ void lse_push_fin(Lse& a, float x) {
   const float d = x - a.m;
   const float e = fast_exp2(-fabsf(d) * kLog2e);
@@ -206,6 +218,17 @@ __device__ __forceinline__ void lse_push_fin(Lse& a, float x) {
   a.m = up ? x : a.m;
 }
 __device__ __forceinline__ void fin_to_empty(Lse& a) { a.m = a.s > 0.f ? a.m : -INFINITY; }
+// four values at once into a finite-start state: one new maximum, one rescale of the sum and
+// one exponential per value (values of -inf add nothing)
+__device__ __forceinline__ void lse_push4_fin(Lse& a, const float (&x)[4]) {
+  const float mn = fmaxf(a.m, fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
+  const float ml = mn * kLog2e;
+  float s = a.s * fast_exp2((a.m - mn) * kLog2e);   // exactly 1 while the maximum stays
+#pragma unroll
+  for (int i = 0; i < 4; ++i) s += fast_exp2(__builtin_fmaf(x[i], kLog2e, -ml));
+  a.m = mn;
+  a.s = s;
+}
 
 // value of the lane N places further along in the same row of 16 lanes (DPP row rotate)
 template <int N>
@@ -256,6 +279,25 @@ __device__ __forceinline__ uint64_t wave_key_max(uint64_t k) {
   }
   return k;
 }
+
+// largest key over the lanes l, l ^ 16, l ^ 32 and l ^ 48 (every one of them gets it)
+__device__ __forceinline__ uint64_t groups_key_max(uint64_t k) {
+  k = key_max(k, ((uint64_t)lane_xor16((uint32_t)(k >> 32)) << 32) | lane_xor16((uint32_t)k));
+  k = key_max(k, ((uint64_t)lane_xor32((uint32_t)(k >> 32)) << 32) | lane_xor32((uint32_t)k));
+  return k;
+}
+// lane permutation for allred_partial over the lanes l, l ^ 16, l ^ 32 and l ^ 48
+struct GroupXor {
+  template <typename F>
+  __device__ __forceinline__ void each(F f) const {
+    f(16);
+    f(32);
+  }
+  __device__ __forceinline__ int i(int v, int m) const {
+    return (int)(m == 16 ? lane_xor16((uint32_t)v) : lane_xor32((uint32_t)v));
+  }
+  __device__ __forceinline__ float operator()(float v, int m) const { return __int_as_float(i(__float_as_int(v), m)); }
+};
 
 // lane permutations for allred_partial: DPP rotations within each row of 16 lanes, then
 // (FULL) xor shuffles across the four rows
@@ -472,66 +514,23 @@ __device__ __forceinline__ void split_h24(uint32_t wd, uint32_t& hi, uint32_t& l
   hi = h >> 16;
   lo = __float_as_uint(__uint_as_float(x) - __uint_as_float(h)) >> 16;
 }
+// Eight consecutive 24-bit words (two loaded quads) as an MFMA operand: their bf16 hi and lo halves
+__device__ __forceinline__ void split_h24x8(const u32x4& q0, const u32x4& q1, uint4& hi, uint4& lo) {
+  uint32_t h[8], l[8];
+  split_h24(q0.x, h[0], l[0]);
+  split_h24(q0.y, h[1], l[1]);
+  split_h24(q0.z, h[2], l[2]);
+  split_h24(q0.w, h[3], l[3]);
+  split_h24(q1.x, h[4], l[4]);
+  split_h24(q1.y, h[5], l[5]);
+  split_h24(q1.z, h[6], l[6]);
+  split_h24(q1.w, h[7], l[7]);
+  hi = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16));
+  lo = make_uint4(l[0] | (l[1] << 16), l[2] | (l[3] << 16), l[4] | (l[5] << 16), l[6] | (l[7] << 16));
+}
 __device__ __forceinline__ bool quad_tagged(const u32x4& q, uint32_t tag8) {
   return ((q.x & 0xffu) == tag8) & ((q.y & 0xffu) == tag8) & ((q.z & 0xffu) == tag8) & ((q.w & 0xffu) == tag8);
 }
-// Load the 32-bit h words of rows < nb, columns [k0, k0 + HC) (half 0) and, with two, [k0 + HC,
-// k0 + 2 HC) (half 1) of a row-major [rows][stride] source, four words per 16-byte load: quad m
-// of a thread is item tid + 256 (m & 3) of half m >> 2 (row = item / (HC / 4)); at most 4 items
-// per thread and half (nb * HC <= 4096).  Polls until every loaded quad carries tag8.
-__device__ __forceinline__ bool poll_quads(const uint32_t* src, int nb, int HC, int stride, int k0, bool two,
-                                           uint32_t tag8, u32x4 (&qv)[8], uint32_t* err) {
-  const int qpr = HC >> 2;
-  const __amdgpu_buffer_rsrc_t rs = coherent_rsrc(src, (uint32_t)(((size_t)(nb - 1) * stride + k0 + (two ? 2 : 1) * HC) * 4));
-  const int t = local_tid();
-  uint32_t pend = 0;
-  uint32_t off[8];
-#pragma unroll
-  for (int m = 0; m < 8; ++m) {
-    const int i = t + kT * (m & 3), row = i / qpr, qc = i - row * qpr;
-    off[m] = (uint32_t)((row * stride + k0 + (m >> 2) * HC + 4 * qc) * 4);
-    if (row < nb && (m < 4 || two)) pend |= 1u << m;
-    qv[m] = u32x4{0u, 0u, 0u, 0u};
-  }
-  for (long sp = 0; pend; ++sp) {
-    poll_fence();
-#pragma unroll
-    for (int m = 0; m < 8; ++m)
-      if ((pend >> m) & 1u) qv[m] = ld128(rs, off[m]);
-#pragma unroll
-    for (int m = 0; m < 8; ++m)
-      if (((pend >> m) & 1u) && quad_tagged(qv[m], tag8)) pend &= ~(1u << m);
-    if (!pend) break;
-    __builtin_amdgcn_s_sleep(2);
-    if ((sp & 63) == 63 && ld32(err)) return false;
-    if (sp > kMaxSpins) {
-      st32(err, kErrStalled);
-      return false;
-    }
-  }
-  return true;
-}
-// Split the quads of one half (loaded by poll_quads) into the operand planes at [row * pitch + c].
-__device__ __forceinline__ void put_quads(const u32x4 (&qv)[8], int half, int nb, int HC, uint16_t* hi, uint16_t* lo,
-                                          int pitch) {
-  const int qpr = HC >> 2;
-  const int t = local_tid();
-#pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    const int i = t + kT * m, row = i / qpr, qc = i - row * qpr;
-    if (row < nb) {
-      const u32x4 q = qv[4 * half + m];
-      uint32_t h0, l0, h1, l1, h2, l2, h3, l3;
-      split_h24(q.x, h0, l0);
-      split_h24(q.y, h1, l1);
-      split_h24(q.z, h2, l2);
-      split_h24(q.w, h3, l3);
-      *(uint2*)(hi + row * pitch + 4 * qc) = make_uint2(h0 | (h1 << 16), h2 | (h3 << 16));
-      *(uint2*)(lo + row * pitch + 4 * qc) = make_uint2(l0 | (l1 << 16), l2 | (l3 << 16));
-    }
-  }
-}
-
 // Wait until one (ALL = false) or every (ALL = true) of np producers has published (one lane
 // per producer, polling one word of each).  Narrow batches stage after the first producer: the
 // rest of their small hand-off follows within a fraction of a microsecond.  A wide batch of one
@@ -677,30 +676,26 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   lds_flag_t* s_fail = (lds_flag_t*)p;              // sticky failure flag
 
   // A failed call leaves outputs that cannot pass for a draft: token -1 at every position
-  // (workgroup 0 is the only writer of tokens) and NaN in every statistics row (row q is
-  // merged, and on failure overwritten, by workgroup q mod G alone).
+  // unless the drafting itself had finished (workgroup 0 is the only writer of tokens), and
+  // NaN in every statistics row (row q is merged, and on failure overwritten, by workgroup
+  // q mod G alone).
+  bool tokens_done = false;
   auto bail = [&]() {
-    if (w == 0)
+    if (w == 0 && !tokens_done)
       for (int i = tid; i < batch * Bk; i += kT) a.out_tokens[i] = -1;
     if (a.out_stats && tid < 6)
       for (int q = w; q < batch * Bk; q += G) ((float*)(a.out_stats + q))[tid] = __builtin_nanf("");
   };
-  // Entry: an earlier failure on this workspace (the error word is sticky until the workspace
-  // is zero-filled), or a prepared buffer that does not belong to this head (its header holds
-  // the shapes and tensor pointers dls_prepare_head was given), ends the call at once.
+  // Entry check, evaluated once the resident weights are in flight: an earlier failure on this
+  // workspace (the error word is sticky until the workspace is zero-filled), or a prepared
+  // buffer that does not belong to this head (its header holds the shapes and tensor pointers
+  // dls_prepare_head was given; the host has checked its size, so the loads below stay inside
+  // it either way), ends the call.
+  PreparedHeader ph;
+  uint32_t err_at_entry = 0u;
   if (tid == 0) {
-    const PreparedHeader* ph = a.prep;
-    const PreparedHeader& ex = a.expect;
-    const bool mismatch = ph->magic != ex.magic || ph->V != ex.V || ph->d != ex.d || ph->H != ex.H ||
-                          ph->r != ex.r || ph->emb != ex.emb || ph->w_ih != ex.w_ih || ph->w_hh != ex.w_hh ||
-                          ph->w_vocab != ex.w_vocab;
-    if (mismatch) st32(err, kErrPrepared);
-    *s_fail = (mismatch || ld32(err) != 0u) ? 1 : 0;
-  }
-  __syncthreads();
-  if (*s_fail) {
-    bail();
-    return;
+    ph = *a.prep;
+    err_at_entry = ld32(err);
   }
 
   // ---- clear this workgroup's key slots of the other set (read by the next call)
@@ -740,7 +735,18 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   }
   if (PRIOR)
     for (int i = tid; i < nrows; i += kT) s_prior[i] = v_base + i < V ? a.prior[v_base + i] : 0.f;
+  if (tid == 0) {
+    const PreparedHeader& ex = a.expect;
+    const bool mismatch = ph.magic != ex.magic || ph.V != ex.V || ph.d != ex.d || ph.H != ex.H || ph.r != ex.r ||
+                          ph.emb != ex.emb || ph.w_ih != ex.w_ih || ph.w_hh != ex.w_hh || ph.w_vocab != ex.w_vocab;
+    if (mismatch) st32(err, kErrPrepared);
+    *s_fail = (mismatch || err_at_entry != 0u) ? 1 : 0;
+  }
   __syncthreads();
+  if (*s_fail) {
+    bail();
+    return;
+  }
 
   const LT* L = (const LT*)a.L;
   const float wl = a.wl;
@@ -876,11 +882,14 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     const int hs = a.literal ? j - 1 : j;          // head step index (the first one starts from h = 0)
 
     // ======================= GRU and rank (GRU workgroups) =======================
-    if (gru && !long_only) {
+    if (!MARKOV && gru && !long_only) {
       const uint32_t tag_prev = (epoch << 8) | (uint32_t)j;   // h published at position j-1
       const uint64_t* hprev = a.hbuf + (size_t)((j - 1) & 1) * batch * H;
       uint64_t* hnew = a.hbuf + (size_t)par * batch * H;
-      uint32_t* h32new = NARROW ? nullptr : a.h32 + (size_t)set * kH32Set + (size_t)par * kMaxBatch * H;
+      // wide batches: the h words of this position, in a.hrep replicas (every GRU workgroup reads
+      // all of h; the replicas spread the readers over the memory channels)
+      const size_t hrep_stride = (size_t)batch * H;
+      uint32_t* h32new = NARROW ? nullptr : a.h32 + (size_t)set * kH32Set + (size_t)par * a.hrep * hrep_stride;
       if (j > 0) {
         if (!merge_position(j - 1)) {
           bail();
@@ -970,7 +979,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
               st64(hnew + (size_t)bb * H + 16 * w + n16, tagged(hn[k], tag));
             } else {
               hown[k] = hn[k];
-              st32(h32new + (size_t)bb * H + 16 * w + n16, pack_h24(hn[k], tag8));
+              const uint32_t word = pack_h24(hn[k], tag8);
+              for (int rep = 0; rep < a.hrep; ++rep) st32(h32new + rep * hrep_stride + (size_t)bb * H + 16 * w + n16, word);
             }
           }
         }
@@ -979,9 +989,121 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
           return;
         }
       }
-      // rho_i = SiLU(W_rank h_{j+1}) for the owned rank rows (MFMA over the staged h, K split
-      // over the waves), then W_hh h_{j+1} for the next position from the same staged h
-      for (int mt = 0; mt < mtiles; ++mt) {
+      // rho_i = SiLU(W_rank h_{j+1}) for the owned rank rows and W_hh h_{j+1} for the next
+      // position, from h_{j+1} of all GRU workgroups.
+      //
+      // Wide batches: the A operands come straight from the 32-bit hand-off words, with no LDS
+      // staging: lane (slot n16, group g4) loads columns 32 kk + 8 g4 .. +7 of its slot (two
+      // 16-byte loads, split into bf16 hi and lo halves in registers).  The M tiles are taken in
+      // order and the four waves split K (wave v: kk = v mod 4), so the rho of M tile m is out
+      // (and the other workgroups fold it) while M tile m + 1 is still being multiplied; the
+      // partial sums of the four waves are added in LDS in wave order.
+      if (!NARROW) {
+        const bool with_gh = j + 1 < Bk;
+        constexpr int NB = 8;   // K steps per round of loads and wave (two 16-byte loads each)
+        bool ok = true;
+        for (int mt = 0; mt < mtiles; ++mt) {
+          const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
+          f32x4_t racc = f32x4_t{0.f, 0.f, 0.f, 0.f}, g0 = racc, g1 = racc, g2 = racc;
+          const __amdgpu_buffer_rsrc_t rs =
+              coherent_rsrc(h32new + (size_t)(w % a.hrep) * hrep_stride + (size_t)mt * 16 * H, (uint32_t)(nb * H * 4));
+          const bool have = n16 < nb;   // lanes of slots past the batch multiply zeros
+          const uint32_t rowoff = (uint32_t)((have ? n16 : 0) * H + 8 * g4);
+          for (int c0 = 0; ok && wave + c0 * 4 < KKH; c0 += NB) {
+            u32x4 q[2 * NB];
+            uint32_t pend = 0;
+#pragma unroll
+            for (int t = 0; t < NB; ++t) {
+              q[2 * t] = q[2 * t + 1] = u32x4{0u, 0u, 0u, 0u};
+              if (have && wave + (c0 + t) * 4 < KKH) pend |= 3u << (2 * t);
+            }
+            for (long sp = 0; pend; ++sp) {
+              poll_fence();
+#pragma unroll
+              for (int m = 0; m < 2 * NB; ++m)
+                if ((pend >> m) & 1u)
+                  q[m] = ld128(rs, (rowoff + 32u * (uint32_t)(wave + (c0 + m / 2) * 4) + 4u * (m & 1)) * 4u);
+#pragma unroll
+              for (int m = 0; m < 2 * NB; ++m)
+                if (((pend >> m) & 1u) && quad_tagged(q[m], tag8)) pend &= ~(1u << m);
+              if (!pend) break;
+              __builtin_amdgcn_s_sleep(2);
+              if ((sp & 63) == 63 && ld32(err)) {
+                ok = false;
+                break;
+              }
+              if (sp > kMaxSpins) {
+                st32(err, kErrStalled);
+                ok = false;
+                break;
+              }
+            }
+            if (!ok) break;
+#pragma unroll
+            for (int t = 0; t < NB; ++t) {
+              const int kk = wave + (c0 + t) * 4;
+              if (kk < KKH) {   // wave-uniform
+                uint4 ahi, alo;
+                split_h24x8(q[2 * t], q[2 * t + 1], ahi, alo);
+                const uint4 bw = n16 < rpg ? *(const uint4*)(s_wrank + (size_t)n16 * H + 32 * kk + 8 * g4)
+                                           : make_uint4(0, 0, 0, 0);
+                racc = mfma_vv(alo, bw, mfma_vv(ahi, bw, racc));
+                if (with_gh) {
+                  const uint4 b0 = s_whh[(0 * KKH + kk) * 64 + lane];
+                  const uint4 b1 = s_whh[(1 * KKH + kk) * 64 + lane];
+                  const uint4 b2 = s_whh[(2 * KKH + kk) * 64 + lane];
+                  g0 = mfma_vv(alo, b0, mfma_vv(ahi, b0, g0));
+                  g1 = mfma_vv(alo, b1, mfma_vv(ahi, b1, g1));
+                  g2 = mfma_vv(alo, b2, mfma_vv(ahi, b2, g2));
+                }
+              }
+            }
+          }
+          // the four waves' partial sums, added in wave order by wave 0 (the planes are free
+          // here: the vocabulary phase stages rho into them only after the barrier that ends
+          // this M tile loop)
+          if (mt) __syncthreads();   // wave 0 is done reading the previous M tile's partials
+          s_red[(wave * 4 + 0) * 64 + lane] = racc;
+          s_red[(wave * 4 + 1) * 64 + lane] = g0;
+          s_red[(wave * 4 + 2) * 64 + lane] = g1;
+          s_red[(wave * 4 + 3) * 64 + lane] = g2;
+          if (fail_barrier(!ok, s_fail)) {
+            bail();
+            return;
+          }
+          if (wave == 0) {
+            for (int k = 1; k < 4; ++k) {
+              racc += s_red[(k * 4 + 0) * 64 + lane];
+              g0 += s_red[(k * 4 + 1) * 64 + lane];
+              g1 += s_red[(k * 4 + 2) * 64 + lane];
+              g2 += s_red[(k * 4 + 3) * 64 + lane];
+            }
+            if (n16 < rpg) {
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const int slot = 4 * g4 + i;
+                if (slot < nb) {
+                  const uint64_t word = tagged(siluf_(racc[i]), tag);
+                  for (int c = 0; c < kRhoCopies; ++c)
+                    st64(a.rbuf + ((size_t)c * 2 + par) * batch * r + (size_t)(mt * 16 + slot) * r + w * rpg + n16,
+                         word);
+                }
+              }
+            }
+            if (with_gh) {
+              float* gh = s_gh + mt * 16 * 48;
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                gh[(4 * g4 + i) * 48 + 0 * 16 + n16] = g0[i];
+                gh[(4 * g4 + i) * 48 + 1 * 16 + n16] = g1[i];
+                gh[(4 * g4 + i) * 48 + 2 * 16 + n16] = g2[i];
+              }
+            }
+          }
+        }
+        __syncthreads();   // s_red read, gh written: the planes and s_gh are free for what follows
+      }
+      for (int mt = 0; NARROW && mt < mtiles; ++mt) {
         const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
         const int HC = nb * (H + 8) <= kPlane ? H : kStageK;
         const int pitch = HC + 8;
@@ -1018,32 +1140,11 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
           if (chunked && with_gh) gh_chunk(k0);
         };
         // the other GRU workgroups publish h at about the same time: poll the words directly
-        if (NARROW) {
-          for (int k0 = 0; k0 < H; k0 += HC) {
-            if (k0) __syncthreads();
-            ok &= stage_poll_words<kInf>(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
-            __syncthreads();
-            chunk_products(k0);
-          }
-        } else {
-          // 32-bit words, two chunks per round of loads: the second chunk waits in registers
-          // while the first is multiplied
-          const uint32_t* h32src = h32new + (size_t)mt * 16 * H;
-          for (int k0 = 0; k0 < H; k0 += 2 * HC) {
-            const bool two = k0 + HC < H;
-            u32x4 qv[8];
-            ok &= poll_quads(h32src, nb, HC, H, k0, two, tag8, qv, err);
-            if (k0) __syncthreads();   // every wave is done with the planes' previous chunk
-            put_quads(qv, 0, nb, HC, s_hi, s_lo, pitch);
-            __syncthreads();
-            chunk_products(k0);
-            if (two) {
-              __syncthreads();
-              put_quads(qv, 1, nb, HC, s_hi, s_lo, pitch);
-              __syncthreads();
-              chunk_products(k0 + HC);
-            }
-          }
+        for (int k0 = 0; k0 < H; k0 += HC) {
+          if (k0) __syncthreads();
+          ok &= stage_poll_words<kInf>(hsrc + k0, nb, HC, H, tag, s_hi, s_lo, pitch, err);
+          __syncthreads();
+          chunk_products(k0);
         }
         if (n16 < rpg) s_rred[(wave * 4 + g4) * rpg + n16] = racc;
         if (fail_barrier(!ok, s_fail)) {
@@ -1221,13 +1322,16 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       // With at most 4 sequences every useful MFMA output sits in lanes 0..15 (rows = slots).
       // Such "narrow" tiles are stashed in LDS (the planes, free once the A operands are in
       // registers) and folded four tiles at a time, one tile per 16-lane group.
+      //
+      // Wider batches multiply the other way round: the resident W_vocab tile is the A operand
+      // and rho the B operand (the two operands take the same per-lane layout), so a product
+      // tile is vocabulary rows x slots and lane (slot n16, group g4) holds rows 4 g4 .. 4 g4 + 3
+      // of its one slot.  Its running statistics are then those of a single slot, its four long
+      // logits are one LDS read, its four entries share one Philox block, and the statistics
+      // reduce over the slot's four lanes instead of over sixteen lanes for each of four slots.
       constexpr bool narrow = NARROW;
-      // Sampling folds wide tiles from an LDS stash too (4 tiles of 16 slots x 16 rows per
-      // wave, 16 KiB in all), so that the Gumbel noise is generated in one loop body rather
-      // than in every unrolled tile.
-      constexpr bool stash_wide = SAMPLE && !NARROW;
-      float* s_stash = (float*)s_hi + wave * (stash_wide ? 1024 : (PACK ? 512 : 256));   // [halves][4 tiles][slots][16 rows]
-      if (narrow || stash_wide) __syncthreads();
+      float* s_stash = (float*)s_hi + wave * (PACK ? 512 : 256);   // narrow: [halves][4 tiles][slots][16 rows]
+      if (narrow) __syncthreads();
 
       Partial P[4];
 #pragma unroll
@@ -1237,13 +1341,9 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       }
 
       // keep the useful rows of a tile's result at stash position tq (narrow: slots < nb of
-      // lane group 0; wide: all 16 slots)
+      // lane group 0)
       auto stash = [&](const f32x4_t& acc, int tq) {
-        if (stash_wide) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (i < nb) s_stash[(tq * 16 + 4 * g4 + i) * 16 + n16] = acc[i];
-        } else if (PACK) {   // lane group 0 holds the hi products, group 1 the lo products
+        if (PACK) {   // lane group 0 holds the hi products, group 1 the lo products
           if (g4 < 2) {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
@@ -1286,45 +1386,60 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         }
       };
 
-      // wide batches: lane (row n16, group g4) folds slots 4 g4 + i of one row.  As in the narrow
-      // fold, entries past the batch or the vocabulary enter as -inf (no term, no maximum, no
-      // top-2 change) rather than behind per-lane branches.
-      auto fold_tile = [&](const f32x4_t& acc, int lt) {
-        const int row = 16 * lt + (local_tid() & 15);
-        const int v = v_base + row;
-        const bool vin = v < V;
+      // wide: fold a product tile (rows x slots) of tile lt.  Entries past the batch or the
+      // vocabulary enter as -inf (no term, no maximum, no top-2 change) rather than behind
+      // per-lane branches.
+      auto fold4 = [&](const f32x4_t& acc, int lt) {
+        const int lt16 = local_tid() & 63;
+        const int sl_own = lt16 & 15;                      // the lane's slot
+        const int row0 = 16 * lt + 4 * (lt16 >> 4);        // its first row in the owned range
+        const int v0 = v_base + row0;
+        const bool sok = sl_own < nb;
+        const int sl = sok ? sl_own : 0;
         // the long-only first row of the literal schedule: no head term, no prior, no short sum
         const float alx = long_only ? 0.f : al, bex = long_only ? 0.f : be;
+        float x[4];
+        if constexpr (sizeof(LT) == 2) {
+          const uint2 raw = *(const uint2*)(s_ll + (size_t)sl * a.rows_max + row0);
+          x[0] = bf16_lo(raw.x);
+          x[1] = bf16_hi(raw.x);
+          x[2] = bf16_lo(raw.y);
+          x[3] = bf16_hi(raw.y);
+        } else {
+          const float4 raw = *(const float4*)(s_ll + (size_t)sl * a.rows_max + row0);
+          x[0] = raw.x;
+          x[1] = raw.y;
+          x[2] = raw.z;
+          x[3] = raw.w;
+        }
+        float4 pr = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (PRIOR) pr = *(const float4*)(s_prior + row0);
         float gz[4] = {0.f, 0.f, 0.f, 0.f};
-        if (SAMPLE) gumbel_quad(a.smp, mt * 16 + 4 * g4, j, v, nb, gz);
+        if (SAMPLE) {   // entries v0 .. v0 + 3 are the four words of one Philox block (v0 % 4 == 0)
+          const uint4 x4 = philox_row(a.smp, mt * 16 + sl, j, v0);
+          gz[0] = gumbel_from_word(x4.x);
+          gz[1] = gumbel_from_word(x4.y);
+          gz[2] = gumbel_from_word(x4.z);
+          gz[3] = gumbel_from_word(x4.w);
+        }
+        const float prv[4] = {pr.x, pr.y, pr.z, pr.w};
+        float xl[4], xs[4], f[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int slot = 4 * g4 + i;
-          if (i < nb) {   // uniform: skips slot sets no lane holds
-            const bool ok = slot < nb && vin;
-            const float xr = to_f32(s_ll[(ok ? slot : 0) * a.rows_max + row]);
-            const float x = ok ? xr : -INFINITY;
-            float f = __builtin_fmaf(alx, acc[i], weighted(wl, x));
-            if (PRIOR) f = minus_weighted(f, bex, s_prior[row]);
-            f = ok ? f : -INFINITY;
-            lse_push_fin(P[i].S, ok && !long_only ? acc[i] : -INFINITY);
-            lse_push_fin(P[i].L, x);
-            if (SAMPLE) f *= a.smp.inv_temp;
-            lse_push_fin(P[i].F, f);
-            top2_push(P[i], SAMPLE ? f + gz[i] : f, v);
-          }
+          const bool ok = sok && v0 + i < V;
+          xl[i] = ok ? x[i] : -INFINITY;
+          xs[i] = (ok && !long_only) ? acc[i] : -INFINITY;
+          float fi = __builtin_fmaf(alx, acc[i], weighted(wl, x[i]));
+          if (PRIOR) fi = minus_weighted(fi, bex, prv[i]);
+          fi = ok ? fi : -INFINITY;
+          if (SAMPLE) fi *= a.smp.inv_temp;
+          f[i] = fi;
         }
-      };
-
-      // sampling, wide: fold stashed tiles base + stride * tq (tq < ntile) one at a time
-      auto fold_wide = [&](int base, int stride, int ntile) {
-#pragma unroll 1
-        for (int tq = 0; tq < ntile; ++tq) {
-          f32x4_t acc;
+        lse_push4_fin(P[0].L, xl);
+        lse_push4_fin(P[0].S, xs);
+        lse_push4_fin(P[0].F, f);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) acc[i] = i < nb ? s_stash[(tq * 16 + 4 * g4 + i) * 16 + n16] : 0.f;
-          fold_tile(acc, base + stride * tq);
-        }
+        for (int i = 0; i < 4; ++i) top2_push(P[0], SAMPLE ? f[i] + gz[i] : f[i], v0 + i);
       };
 
       // AGPR-resident tiles of this wave, two at a time: four independent MFMA chains
@@ -1339,29 +1454,37 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
           if (!long_only) {
 #pragma unroll
             for (int kk = 0; kk < KK; ++kk) {
-              c0 = mfma_va(ahi[kk], wr[q * KK + kk], c0);
-              if (!MARKOV && !PACK) c1 = mfma_va(alo[kk], wr[q * KK + kk], c1);
-              if (two) {
-                c2 = mfma_va(ahi[kk], wr[q2 * KK + kk], c2);
-                if (!MARKOV && !PACK) c3 = mfma_va(alo[kk], wr[q2 * KK + kk], c3);
+              if (narrow) {
+                c0 = mfma_va(ahi[kk], wr[q * KK + kk], c0);
+                if (!MARKOV && !PACK) c1 = mfma_va(alo[kk], wr[q * KK + kk], c1);
+                if (two) {
+                  c2 = mfma_va(ahi[kk], wr[q2 * KK + kk], c2);
+                  if (!MARKOV && !PACK) c3 = mfma_va(alo[kk], wr[q2 * KK + kk], c3);
+                }
+              } else {
+                c0 = mfma_av(wr[q * KK + kk], ahi[kk], c0);
+                if (!MARKOV) c1 = mfma_av(wr[q * KK + kk], alo[kk], c1);
+                if (two) {
+                  c2 = mfma_av(wr[q2 * KK + kk], ahi[kk], c2);
+                  if (!MARKOV) c3 = mfma_av(wr[q2 * KK + kk], alo[kk], c3);
+                }
               }
             }
           }
-          if (narrow || stash_wide) {
+          if (narrow) {
             stash(PACK ? c0 : c0 + c1, q % 4);
             if (two) stash(PACK ? c2 : c2 + c3, q % 4 + 1);
           } else {
-            fold_tile(c0 + c1, lt);
-            if (two && lt + 1 < na) fold_tile(c2 + c3, lt + 1);
+            fold4(c0 + c1, lt);
+            if (two && lt + 1 < na) fold4(c2 + c3, lt + 1);
           }
         }
-        if ((narrow || stash_wide) && (q % 4 == 2 || q + 2 >= TPW)) {   // a group of four tiles (or the last) is stashed
+        if (narrow && (q % 4 == 2 || q + 2 >= TPW)) {   // a group of four tiles (or the last) is stashed
           const int g0 = q - q % 4;
           const int cnt = (TPW - g0 < 4 ? TPW - g0 : 4);
           const int avail = na - (wave * TPW + g0);
           const int nf = avail < cnt ? (avail > 0 ? avail : 0) : cnt;
-          if (narrow) fold_narrow(wave * TPW + g0, 1, nf);
-          else fold_wide(wave * TPW + g0, 1, nf);
+          fold_narrow(wave * TPW + g0, 1, nf);
         }
       }
       // LDS-resident tiles, round robin over the waves (narrow: four at a time)
@@ -1371,13 +1494,18 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
 #pragma unroll
           for (int kk = 0; kk < KK; ++kk) {
             const uint4 bw = s_wtiles[((size_t)lq * KK + kk) * 64 + lane];
-            c0 = mfma_vv(ahi[kk], bw, c0);
-            if (!MARKOV && !PACK) c1 = mfma_vv(alo[kk], bw, c1);
+            if (narrow) {
+              c0 = mfma_vv(ahi[kk], bw, c0);
+              if (!MARKOV && !PACK) c1 = mfma_vv(alo[kk], bw, c1);
+            } else {
+              c0 = mfma_vv(bw, ahi[kk], c0);
+              if (!MARKOV) c1 = mfma_vv(bw, alo[kk], c1);
+            }
           }
         }
         return PACK ? c0 : c0 + c1;
       };
-      if (narrow || stash_wide) {
+      if (narrow) {
         for (int m0 = 0; wave + 4 * m0 < nl; m0 += 4) {
           int cnt = 0;
           for (int tq = 0; tq < 4; ++tq) {
@@ -1387,24 +1515,24 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
               ++cnt;
             }
           }
-          if (narrow) fold_narrow(na + wave + 4 * m0, 4, cnt);
-          else fold_wide(na + wave + 4 * m0, 4, cnt);
+          fold_narrow(na + wave + 4 * m0, 4, cnt);
         }
       } else {
-        for (int lq = wave; lq < nl; lq += 4) fold_tile(lds_tile(lq), na + lq);
+        for (int lq = wave; lq < nl; lq += 4) fold4(lds_tile(lq), na + lq);
       }
-      // argmax key of each slot: max over the 16 lanes of a row (DPP), then over the waves
+      // argmax key of each slot: narrow, over the wave (slot i spread over it); wide, over the
+      // slot's four lanes; then over the waves
+      if (narrow) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (i < nb) {
-          if (narrow) {   // slot i spread over the whole wave
+        for (int i = 0; i < 4; ++i) {
+          if (i < nb) {
             const uint64_t k = wave_key_max(make_key(P[i].t1, P[i].i1, tag8));
             if (lane == 0) s_wkey[wave * 16 + i] = k;
-          } else {
-            const uint64_t k = row_key_max(make_key(P[i].t1, P[i].i1, tag8));
-            if (n16 == 0) s_wkey[wave * 16 + 4 * g4 + i] = k;
           }
         }
+      } else {
+        const uint64_t k = groups_key_max(make_key(P[0].t1, P[0].i1, tag8));
+        if (g4 == 0 && n16 < nb) s_wkey[wave * 16 + n16] = k;
       }
       __syncthreads();
       if (tid < nb) {
@@ -1414,19 +1542,23 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       }
       // the full partials (LSEs, top-2) for the row statistics: off the critical path
       if (a.out_stats) {
+        if (narrow) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (i < nb) {
-            fin_to_empty(P[i].L);
-            fin_to_empty(P[i].S);
-            fin_to_empty(P[i].F);
-            P[i] = allred_partial(P[i], RowRor<NARROW>{});   // over the row (narrow: the wave)
-            if (narrow) {
+          for (int i = 0; i < 4; ++i) {
+            if (i < nb) {
+              fin_to_empty(P[i].L);
+              fin_to_empty(P[i].S);
+              fin_to_empty(P[i].F);
+              P[i] = allred_partial(P[i], RowRor<true>{});   // over the wave
               if (lane == 0) s_part[wave * 16 + i] = P[i];
-            } else if (n16 == 0) {
-              s_part[wave * 16 + 4 * g4 + i] = P[i];
             }
           }
+        } else {
+          fin_to_empty(P[0].L);
+          fin_to_empty(P[0].S);
+          fin_to_empty(P[0].F);
+          P[0] = allred_partial(P[0], GroupXor{});   // over the slot's four lanes
+          if (g4 == 0 && n16 < nb) s_part[wave * 16 + n16] = P[0];
         }
         if (gru && mtiles == 1 && j + 1 < Bk) {
           pending_stats = j;
@@ -1445,6 +1577,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       bail();
       return;
     }
+    tokens_done = true;
   }
   // ---- row statistics: row (b, j) is merged by workgroup (b * B + j) % G from the tagged partials
   if (a.out_stats) {
