@@ -37,6 +37,10 @@ Readings where the paper is silent (each is also listed in the design notes):
   row j of the block; a row decoded from the long logits alone ignores them.
 * The Markov head's state at row j is E_M of the token before it: the last
   accepted token for row 0, the drafted token d_{j-1} afterwards.
+* Adaptive fusion (Sec. 7 proposes it as future work without a rule): row (b, j)
+  fuses with alpha_j * g and beta_j * g, g = clamp((u - h_lo) / (h_hi - h_lo), 0, 1)
+  of that row's uncertainty u, either the entropy of p_L over log V or
+  (1 - max p_L) / (1 - 1/V); u = 0 when V = 1.
 * Sampling at temperature T > 0 (the paper reports T = 0 and T = 1 but not how
   it draws) is the Gumbel-max rule on l / T.  The noise of entry v of row
   (sequence b, position j) comes from Philox4x32-10 keyed by the seed at
@@ -181,6 +185,65 @@ def combine_rows(long_rows, short_rows, prior, w_long, alpha, beta, want_scores=
 
 
 # ----------------------------------------------------------------------------------------
+# adaptive fusion: the local-head and prior weights of a row scaled by a gate that grows with
+# the uncertainty of that row's long logits (Sec. 7 proposes weights adjusted by the
+# token-level entropy or confidence of the long-context logits; the measures and the gate
+# below are this library's reading of that proposal)
+# ----------------------------------------------------------------------------------------
+UNC_ENTROPY, UNC_MAXPROB = 0, 1
+
+
+def long_entropy(long_row) -> float:
+    """H(p_L) = -sum_v p_v log p_v in nats, p = softmax(l_L); a masked entry (p_v = 0) adds
+    nothing (p log p -> 0)."""
+    x = np.asarray(long_row, dtype=F64)
+    logp = x - logsumexp(x)
+    p = np.exp(logp)
+    keep = p > 0
+    return float(-np.sum(p[keep] * logp[keep]))
+
+
+def long_max_prob(long_row) -> float:
+    """max_v p_v, p = softmax(l_L): the confidence of the long logits in their own argmax."""
+    x = np.asarray(long_row, dtype=F64)
+    return float(np.exp(np.max(x) - logsumexp(x)))
+
+
+def uncertainty(long_row, measure: int) -> float:
+    """u in [0, 1]: 0 when p_L is one-hot, 1 when it is uniform over the whole vocabulary.
+    UNC_ENTROPY: H(p_L) / log V.  UNC_MAXPROB: (1 - max p_L) / (1 - 1/V).  V = 1: u = 0."""
+    V = np.asarray(long_row).shape[0]
+    if V == 1:
+        return 0.0
+    if measure == UNC_ENTROPY:
+        return long_entropy(long_row) / np.log(F64(V))
+    if measure == UNC_MAXPROB:
+        return (1.0 - long_max_prob(long_row)) / (1.0 - 1.0 / F64(V))
+    raise ValueError(f"unknown uncertainty measure {measure}")
+
+
+def gate(u: float, h_lo: float, h_hi: float) -> float:
+    """g(u) = min(1, max(0, (u - h_lo) / (h_hi - h_lo))), h_lo < h_hi: no local terms while the
+    long logits are confident (u <= h_lo), full weights once they are uncertain (u >= h_hi),
+    linear between; h_lo < 0 keeps a floor of -h_lo / (h_hi - h_lo) at u = 0."""
+    if not h_lo < h_hi:
+        raise ValueError("the gate needs h_lo < h_hi")
+    return float(min(1.0, max(0.0, (F64(u) - h_lo) / (F64(h_hi) - h_lo))))
+
+
+def adaptive_gates(long_logits, measure: int, h_lo: float, h_hi: float) -> np.ndarray:
+    """The gate of every row (sequence b, position j) of long logits [batch, B, V]."""
+    batch = len(long_logits)
+    B = np.asarray(long_logits[0]).shape[0]
+    g = np.zeros((batch, B), dtype=F64)
+    for b in range(batch):
+        rows = np.asarray(long_logits[b], dtype=F64)
+        for j in range(B):
+            g[b, j] = gate(uncertainty(rows[j], measure), h_lo, h_hi)
+    return g
+
+
+# ----------------------------------------------------------------------------------------
 # sampling noise: Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as
 # easy as 1, 2, 3", SC 2011) keyed by the seed, one counter per 4 vocabulary entries of a row
 # ----------------------------------------------------------------------------------------
@@ -305,11 +368,14 @@ def _at(w, j: int) -> float:
 def draft_block(head, long_logits, last_token: Sequence[int], prior, w_long: float,
                 alpha, beta, first_row_long_only: bool = False,
                 force: Optional[np.ndarray] = None, sequences: Optional[Sequence[int]] = None,
-                temperature: float = 0.0, seed: int = 0) -> DraftResult:
+                temperature: float = 0.0, seed: int = 0,
+                gates: Optional[np.ndarray] = None) -> DraftResult:
     """Greedy DeLS-Spec drafting of one block per sequence (Algorithm 1, decoding steps).
 
     long_logits: [batch, B, V] (anything indexable to rows); last_token: [batch].
     alpha, beta: scalars, or [B] sequences of per-position weights.
+    gates: optional [batch, B] factors of the adaptive fusion (adaptive_gates): row (b, j)
+    fuses with alpha_j * gates[b, j] and beta_j * gates[b, j].
     temperature > 0 samples every row (see combine_row) with the Gumbel noise of
     gumbel_row(seed, b, j, V).
     force: optional [batch, B] tokens that replace the decoded ones (statistics are then
@@ -334,8 +400,9 @@ def draft_block(head, long_logits, last_token: Sequence[int], prior, w_long: flo
                                   temperature=temperature, gumbel=g)
             else:
                 state, s = head.step(state, u)
-                res = combine_row(rows[j], s, prior, w_long, _at(alpha, j), _at(beta, j), force_token=f,
-                                  temperature=temperature, gumbel=g)
+                gf = 1.0 if gates is None else float(gates[b, j])
+                res = combine_row(rows[j], s, prior, w_long, _at(alpha, j) * gf, _at(beta, j) * gf,
+                                  force_token=f, temperature=temperature, gumbel=g)
             out.tokens[b, j] = res.token
             out.score[b, j] = res.score
             out.logprob[b, j] = res.logprob

@@ -13,7 +13,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 PIN_TESTS = [os.path.join(ROOT, "tests", f) for f in
              ("test_oracle_fusion.py", "test_oracle_head.py", "test_oracle_accept.py",
-              "test_oracle_sampling.py")]
+              "test_oracle_sampling.py", "test_oracle_adaptive.py")]
 
 MUTATIONS = {
     "prior_sign": ("f = f - weighted(beta, prior)", "f = f + weighted(beta, prior)"),
@@ -48,6 +48,14 @@ MUTATIONS = {
     "gumbel_single_log": ("return -np.log(-np.log(uniforms_row(seed, b, j, V)))",
                           "return -np.log(uniforms_row(seed, b, j, V))"),
     "temperature_ignored": ("scaled = fused / F64(temperature)", "scaled = fused"),
+    "entropy_sign": ("return float(-np.sum(p[keep] * logp[keep]))", "return float(np.sum(p[keep] * logp[keep]))"),
+    "entropy_over_v": ("return long_entropy(long_row) / np.log(F64(V))", "return long_entropy(long_row) / F64(V)"),
+    "maxprob_unnormalised": ("return (1.0 - long_max_prob(long_row)) / (1.0 - 1.0 / F64(V))",
+                             "return 1.0 - long_max_prob(long_row)"),
+    "gate_unclamped": ("return float(min(1.0, max(0.0, (F64(u) - h_lo) / (F64(h_hi) - h_lo))))",
+                       "return float((F64(u) - h_lo) / (F64(h_hi) - h_lo))"),
+    "gate_alpha_only": ("_at(beta, j) * gf,", "_at(beta, j),"),
+    "gate_of_first_sequence": ("float(gates[b, j])", "float(gates[0, j])"),
     "uniform_no_half": ("return ((x >> np.uint64(9)).astype(F64) + 0.5) * 2.0 ** -23",
                         "return ((x >> np.uint64(9)).astype(F64)) * 2.0 ** -23"),
 }
