@@ -445,6 +445,32 @@ def main():
                               "tokens_per_s": round(wl.batch * wl.B / (pct(sm, 50) * 1e-6), 1),
                               "overhead_vs_greedy": round(pct(sm, 50) / pct(warm, 50) - 1.0, 4)}
         log(f"sampling at T = 1: {pct(sm, 50):.1f} us per block")
+        # adaptive fusion (weights gated by the entropy of the long logits): the pre-pass over the
+        # batch * B long-logit rows, then the gated draft; and the pre-pass alone (HBM-bound)
+        unc = torch.empty((wl.batch, wl.B, 4), dtype=torch.float32, device=dev)
+        rule = (B.UNC_ENTROPY, 0.4, 0.8)
+        for _ in range(3):
+            B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st), workspace=ws,
+                          exclusive_device=EXC, adaptive=rule, out_uncertainty=unc)
+        ad = per_call_us(lambda i: B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, st),
+                                                 workspace=ws, exclusive_device=EXC, adaptive=rule,
+                                                 out_uncertainty=unc), 30, torch)
+        assert B.workspace_error(ws) == 0
+        uws = torch.empty(max(256, B.long_uncertainty_workspace_size(wl.batch * wl.B, wl.V)), dtype=torch.uint8,
+                          device=dev)
+        un = per_call_us(lambda i: B.long_uncertainty(L, *rule, out=unc, workspace=uws), 50, torch)
+        u_bytes = wl.batch * wl.B * (wl.V * L.element_size() + 16)
+        u_gbs = u_bytes / (pct(un, 50) * 1e-6) / 1e9
+        extras["adaptive_fusion"] = {
+            "rule": "gate = clamp((H(p_L) / log V - 0.4) / 0.4, 0, 1) on alpha and beta",
+            "us_per_block": dist(ad), "tokens_per_s": round(wl.batch * wl.B / (pct(ad, 50) * 1e-6), 1),
+            "overhead_vs_greedy": round(pct(ad, 50) / pct(warm, 50) - 1.0, 4),
+            "gate_mean": round(float(unc[..., 3].mean()), 4),
+            "uncertainty_pass": {"rows": wl.batch * wl.B, "us_per_call": dist(un), "algorithmic_bytes": u_bytes,
+                                 "achieved_GBs": round(u_gbs, 1), "frac_of_hbm_peak": round(u_gbs / HBM_PEAK_GBS, 4)}}
+        log(f"adaptive fusion: {pct(ad, 50):.1f} us per block; uncertainty pass {pct(un, 50):.1f} us "
+            f"({u_gbs / HBM_PEAK_GBS:.1%} of HBM peak)")
+        del uws
         # the Markov local head (App. A) on the same workload: rho = E_M[previous token]
         import math
         em, wm = W.make_markov_head(wl.V, wl.r, "bf16", wl.seed, scale=math.sqrt(3.0 / math.sqrt(wl.r)))

@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define DLS_ABI_VERSION 3
+#define DLS_ABI_VERSION 4
 
 typedef enum dls_status {
   DLS_OK = 0,
@@ -269,6 +269,58 @@ dls_status dls_draft_block_sampled(const dls_local_head *head, const void *long_
                                    dls_fusion_schedule schedule, dls_sampling sampling,
                                    int32_t *out_tokens, dls_row_stats *out_stats, void *workspace,
                                    size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------------
+ * Adaptive fusion.  Sec. 7 proposes adjusting the local-head and prior weights by the
+ * token-level entropy or confidence of the long logits, without a rule; the library's
+ * rule, per row (sequence b, position j) of long logits l_L with p = softmax(l_L):
+ *   u = H(p) / log V               DLS_UNC_ENTROPY  (H = -sum_v p_v log p_v, in nats)
+ *   u = (1 - max_v p_v) / (1 - 1/V)  DLS_UNC_MAXPROB
+ *   (u = 0 when V = 1; u = 1 when the row has no finite entry)
+ *   g = min(1, max(0, (u - h_lo) / (h_hi - h_lo)))
+ * and the row fuses with alpha_j * g and beta_j * g: no local terms while the long
+ * logits are confident (u <= h_lo), the full weights once they are uncertain
+ * (u >= h_hi); h_lo < 0 keeps a floor.  -inf entries (masked tokens) have p = 0. */
+typedef enum dls_uncertainty_measure {
+  DLS_UNC_ENTROPY = 0,
+  DLS_UNC_MAXPROB = 1
+} dls_uncertainty_measure;
+typedef struct dls_adaptive {
+  int32_t measure;    /* dls_uncertainty_measure */
+  float h_lo, h_hi;   /* finite, h_lo < h_hi */
+  uint32_t reserved;  /* 0 */
+} dls_adaptive;
+/* What the pre-pass reports for a row.  entropy and max_prob are NaN for a row without a
+ * finite entry. */
+typedef struct dls_row_uncertainty {
+  float entropy;   /* H(p), nats */
+  float max_prob;  /* max_v p_v */
+  float u;         /* the rule's measure, in [0, 1] up to rounding */
+  float gate;      /* g */
+} dls_row_uncertainty;
+
+/* Uncertainty and gate of every row of long logits [rows, V] (device memory, float32 or
+ * bfloat16, 16-byte aligned, finite values or -inf) into out[rows] (device memory).  The
+ * workspace (device, 16-byte aligned; NULL when its size is 0) holds per-range partials when
+ * rows are too few to cover the GPU.  Limits: 0 <= rows <= 2^24, 1 <= V <= 2^24. */
+size_t dls_long_uncertainty_workspace_size(int64_t rows, int32_t V);
+dls_status dls_long_uncertainty(const void *long_logits, dls_dtype dtype, int64_t rows, int32_t V,
+                                dls_adaptive rule, dls_row_uncertainty *out, void *workspace,
+                                size_t ws_bytes, void *stream);
+
+/* dls_draft_block_sampled with adaptive fusion: the rule's pre-pass over the batch * B
+ * rows of long_logits writes out_uncertainty ([batch, B] device memory, required: the
+ * drafting kernels read their gates there), then every row (b, j) fuses with
+ * alpha_j * g[b, j] and beta_j * g[b, j] (w_long unchanged).  The first row of
+ * DLS_FIRST_ROW_LONG_ONLY stays long-only.  The workspace is the drafting workspace of
+ * dls_draft_block_workspace_size, which includes the pre-pass partials. */
+dls_status dls_draft_block_adaptive(const dls_local_head *head, const void *long_logits,
+                                    dls_dtype long_dtype, const int32_t *last_token,
+                                    const float *prior, int32_t batch, int32_t B, dls_fusion fusion,
+                                    dls_fusion_schedule schedule, dls_sampling sampling,
+                                    dls_adaptive rule, dls_row_uncertainty *out_uncertainty,
+                                    int32_t *out_tokens, dls_row_stats *out_stats, void *workspace,
+                                    size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------------------------
  * Allocation-free drafting.  For callers that cannot allocate device memory or own a

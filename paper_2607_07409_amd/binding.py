@@ -43,6 +43,15 @@ class Sampling(ctypes.Structure):
     _fields_ = [("temperature", ctypes.c_float), ("reserved", ctypes.c_uint32), ("seed", ctypes.c_uint64)]
 
 
+class Adaptive(ctypes.Structure):
+    _fields_ = [("measure", ctypes.c_int32), ("h_lo", ctypes.c_float), ("h_hi", ctypes.c_float),
+                ("reserved", ctypes.c_uint32)]
+
+
+UNC_ENTROPY, UNC_MAXPROB = 0, 1
+UNC_FIELDS = ("entropy", "max_prob", "u", "gate")
+
+
 class RowStats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_float) for n in STATS_FIELDS]
 
@@ -82,6 +91,13 @@ def lib() -> ctypes.CDLL:
         L.dls_draft_block_sampled.restype = ctypes.c_int
         L.dls_draft_block_sampled.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
                                               Fusion, Schedule, Sampling, _vp, _vp, _vp, _sz, _vp]
+        L.dls_long_uncertainty_workspace_size.restype = _sz
+        L.dls_long_uncertainty_workspace_size.argtypes = [_i64, _i32]
+        L.dls_long_uncertainty.restype = ctypes.c_int
+        L.dls_long_uncertainty.argtypes = [_vp, ctypes.c_int, _i64, _i32, Adaptive, _vp, _vp, _sz, _vp]
+        L.dls_draft_block_adaptive.restype = ctypes.c_int
+        L.dls_draft_block_adaptive.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
+                                               Fusion, Schedule, Sampling, Adaptive, _vp, _vp, _vp, _vp, _sz, _vp]
         L.dls_prepare_head_size.restype = _sz
         L.dls_prepare_head_size.argtypes = [ctypes.POINTER(LocalHeadC)]
         L.dls_prepare_head.restype = ctypes.c_int
@@ -278,12 +294,15 @@ def workspace_error(workspace: Optional[torch.Tensor], stream=None) -> int:
 
 def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional[torch.Tensor], prior=None,
                 w_long=1.0, alpha=0.3, beta=0.3, first_row_long_only=False, want_stats=True, out=None,
-                workspace=None, stream=None, temperature=0.0, seed=0, exclusive_device=False):
+                workspace=None, stream=None, temperature=0.0, seed=0, exclusive_device=False, adaptive=None,
+                out_uncertainty=None):
     """Draft one block per sequence.  long_logits [batch, B, V]; returns (tokens [batch, B], stats
     [batch, B, 6] or None).  alpha and beta are scalars or [B] per-position weights.
     temperature 0 decodes greedily; T > 0 samples from softmax(l / T) with the Philox noise of
     `seed` (a 64-bit integer).  exclusive_device: the caller runs nothing else on the device
-    during the call (DLS_EXCLUSIVE_DEVICE: an ordinary instead of a cooperative dispatch)."""
+    during the call (DLS_EXCLUSIVE_DEVICE: an ordinary instead of a cooperative dispatch).
+    adaptive = (measure, h_lo, h_hi): adaptive fusion through dls_draft_block_adaptive; the
+    return value then has a third element, the rows' uncertainty [batch, B, 4] (UNC_FIELDS)."""
     L = lib()
     batch, B, V = long_logits.shape
     dev = long_logits.device
@@ -298,7 +317,7 @@ def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional
     sampled = temperature != 0.0
     f = fusion(w_long, 0.0 if np.ndim(alpha) else alpha, 0.0 if np.ndim(beta) else beta, first_row_long_only,
                exclusive_device)
-    if scheduled or sampled:
+    if scheduled or sampled or adaptive is not None:
         # per-position weights: host arrays of B values (kept alive across the call)
         al = np.ascontiguousarray(alpha, np.float32) if np.ndim(alpha) else None
         be = np.ascontiguousarray(beta, np.float32) if np.ndim(beta) else None
@@ -306,6 +325,15 @@ def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional
             if arr is not None and arr.shape != (B,):
                 raise ValueError(f"per-position weights need {B} values")
         sch = Schedule(None if al is None else al.ctypes.data, None if be is None else be.ctypes.data)
+        if adaptive is not None:
+            unc = out_uncertainty if out_uncertainty is not None else \
+                torch.empty((batch, B, 4), dtype=torch.float32, device=dev)
+            smp = Sampling(float(temperature), 0, int(seed) & 0xFFFFFFFFFFFFFFFF)
+            _check(L.dls_draft_block_adaptive(ctypes.byref(head.c), _ptr(long_logits), _dtype_code(long_logits),
+                                              _ptr(last_token), _ptr(prior), batch, B, f, sch, smp,
+                                              adaptive_rule(*adaptive), _ptr(unc), _ptr(tok), _ptr(st),
+                                              _ptr(workspace), workspace.numel(), _stream(stream)))
+            return tok, st, unc
         if sampled:
             smp = Sampling(float(temperature), 0, int(seed) & 0xFFFFFFFFFFFFFFFF)
             _check(L.dls_draft_block_sampled(ctypes.byref(head.c), _ptr(long_logits), _dtype_code(long_logits),
@@ -320,6 +348,33 @@ def draft_block(head: LocalHead, long_logits: torch.Tensor, last_token: Optional
                                  _ptr(last_token), _ptr(prior), batch, B, f, _ptr(tok), _ptr(st), _ptr(workspace),
                                  workspace.numel(), _stream(stream)))
     return tok, st
+
+
+def adaptive_rule(measure: int, h_lo: float, h_hi: float) -> Adaptive:
+    return Adaptive(int(measure), float(h_lo), float(h_hi), 0)
+
+
+def long_uncertainty_workspace_size(rows: int, V: int) -> int:
+    return int(lib().dls_long_uncertainty_workspace_size(rows, V))
+
+
+def long_uncertainty(long_logits: torch.Tensor, measure: int, h_lo: float, h_hi: float, out=None, workspace=None,
+                     stream=None) -> torch.Tensor:
+    """Entropy, maximum probability, measure u and gate of every row of long logits [..., V]:
+    a float32 tensor [..., 4] (UNC_FIELDS)."""
+    L = lib()
+    V = long_logits.shape[-1]
+    rows = long_logits.numel() // V if V else 0
+    dev = long_logits.device
+    if out is None:
+        out = torch.empty((*long_logits.shape[:-1], 4), dtype=torch.float32, device=dev)
+    need = long_uncertainty_workspace_size(rows, V)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    _check(L.dls_long_uncertainty(_ptr(long_logits), _dtype_code(long_logits), rows, V,
+                                  adaptive_rule(measure, h_lo, h_hi), _ptr(out), _ptr(workspace),
+                                  0 if workspace is None else workspace.numel(), _stream(stream)))
+    return out
 
 
 def draft_block_noalloc(head: LocalHead, long_logits: torch.Tensor, last_token: Optional[torch.Tensor], prior=None,

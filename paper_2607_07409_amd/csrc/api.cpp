@@ -89,6 +89,27 @@ dls_status check_fusion(const dls_fusion& f) {
   return DLS_OK;
 }
 
+dls_status check_rule(const dls_adaptive& r) {
+  if (r.measure != DLS_UNC_ENTROPY && r.measure != DLS_UNC_MAXPROB)
+    return fail(DLS_ERR_ARG, "unknown uncertainty measure %d", r.measure);
+  if (r.reserved != 0) return fail(DLS_ERR_ARG, "adaptive.reserved must be 0");
+  if (!std::isfinite(r.h_lo) || !std::isfinite(r.h_hi) || !(r.h_lo < r.h_hi))
+    return fail(DLS_ERR_ARG, "the gate needs finite h_lo < h_hi (got %g, %g)", (double)r.h_lo, (double)r.h_hi);
+  return DLS_OK;
+}
+
+dls::UncRule unc_rule(const dls_adaptive& r, int32_t V) {
+  dls::UncRule u;
+  u.measure = r.measure;
+  u.inv_log_v = V > 1 ? (float)(1.0 / std::log((double)V)) : 0.f;
+  u.maxprob_scale = V > 1 ? (float)((double)V / (double)(V - 1)) : 0.f;
+  u.h_lo = r.h_lo;
+  u.inv_width = (float)(1.0 / ((double)r.h_hi - (double)r.h_lo));
+  return u;
+}
+
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
 dls_status check_head(const dls_local_head* h) {
   if (!h) return fail(DLS_ERR_ARG, "head is NULL");
   if (h->kind != DLS_HEAD_RNN && h->kind != DLS_HEAD_MARKOV) return fail(DLS_ERR_ARG, "unknown head kind %d", h->kind);
@@ -225,8 +246,46 @@ size_t dls_draft_block_workspace_size(const dls_local_head* head, int32_t batch,
   if (!head || batch <= 0 || B <= 0 || check_head(head) != DLS_OK) return 0;
   clear_error();
   const dls_local_head ch = canon(*head);
-  // persistent region first (its header must start zero-filled), per-launch region after it
-  return dls::persist_workspace(ch, batch, B).total + dls::draft_layout(ch, batch, B).total;
+  // persistent region first (its header must start zero-filled), per-launch region after it,
+  // then the partials of the adaptive-fusion pre-pass
+  return dls::persist_workspace(ch, batch, B).total + dls::draft_layout(ch, batch, B).total +
+         align256(dls::uncertainty_workspace_bytes((int64_t)batch * B, ch.V));
+}
+
+size_t dls_long_uncertainty_workspace_size(int64_t rows, int32_t V) {
+  if (rows <= 0 || V <= 0) return 0;
+  return dls::uncertainty_workspace_bytes(rows, V);
+}
+
+dls_status dls_long_uncertainty(const void* long_logits, dls_dtype dtype, int64_t rows, int32_t V,
+                                dls_adaptive rule, dls_row_uncertainty* out, void* workspace, size_t ws_bytes,
+                                void* stream) {
+  clear_error();
+  if (!valid_dtype(dtype)) return fail(DLS_ERR_DTYPE, "unknown dtype %d", (int)dtype);
+  if (rows < 0 || rows > (1 << 24)) return fail(DLS_ERR_SHAPE, "rows=%lld outside [0, 2^24]", (long long)rows);
+  if (V < 1 || V > (1 << 24)) return fail(DLS_ERR_SHAPE, "V=%d outside [1, 2^24]", V);
+  dls_status s = check_rule(rule);
+  if (s != DLS_OK) return s;
+  if (rows == 0) return DLS_OK;
+  if (!long_logits || !out) return fail(DLS_ERR_ARG, "required pointer is NULL");
+  if (!aligned(long_logits, 16)) return fail(DLS_ERR_ARG, "long_logits must be 16-byte aligned");
+  if (!aligned(out, 4)) return fail(DLS_ERR_ARG, "out is misaligned");
+  const size_t need = dls_long_uncertainty_workspace_size(rows, V);
+  if (ws_bytes < need) return fail(DLS_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, need);
+  if (need && (!workspace || !aligned(workspace, 16)))
+    return fail(DLS_ERR_ARG, "workspace is NULL or not 16-byte aligned");
+  if ((s = check_device()) != DLS_OK) return s;
+  dls::UncArgs a;
+  a.long_logits = long_logits;
+  a.dtype = dtype;
+  a.rows = rows;
+  a.V = V;
+  a.rule = unc_rule(rule, V);
+  a.partials = (float4*)workspace;
+  a.out = out;
+  hipError_t e = dls::launch_uncertainty(a, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "long_uncertainty launch");
+  return DLS_OK;
 }
 
 }  // extern "C"
@@ -250,7 +309,8 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_d
                       const int32_t* last_token, const float* prior, int32_t batch, int32_t B, dls_fusion fusion,
                       const float* alphas, const float* betas, dls_sampling sampling, int32_t* out_tokens,
                       dls_row_stats* out_stats, void* workspace, size_t ws_bytes, void* stream,
-                      bool noalloc = false) {
+                      bool noalloc = false, const dls_adaptive* rule = nullptr,
+                      dls_row_uncertainty* out_unc = nullptr) {
   dls_status s = check_head(head);
   if (s != DLS_OK) return s;
   if ((s = check_prepared_size(head)) != DLS_OK) return s;
@@ -279,6 +339,10 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_d
   if ((last_token && !aligned(last_token, 4)) || !aligned(out_tokens, 4) || (prior && !aligned(prior, 4)) ||
       (out_stats && !aligned(out_stats, 4)))
     return fail(DLS_ERR_ARG, "misaligned vector argument");
+  if (rule) {
+    if ((s = check_rule(*rule)) != DLS_OK) return s;
+    if (!out_unc || !aligned(out_unc, 4)) return fail(DLS_ERR_ARG, "out_uncertainty is NULL or misaligned");
+  }
   const size_t need = dls_draft_block_workspace_size(head, batch, B);
   if (noalloc) {
     if (need > dls::kNoallocScratchBytes)
@@ -305,6 +369,19 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_d
 
   const dls_local_head ch = canon(*head);
   const dls::PersistWorkspace pw = dls::persist_workspace(ch, batch, B);
+  // adaptive fusion: the gates of all batch * B rows first, stream-ordered before the draft
+  if (rule) {
+    dls::UncArgs ua;
+    ua.long_logits = long_logits;
+    ua.dtype = long_dtype;
+    ua.rows = (int64_t)batch * B;
+    ua.V = ch.V;
+    ua.rule = unc_rule(*rule, ch.V);
+    ua.partials = (float4*)((char*)workspace + pw.total + dls::draft_layout(ch, batch, B).total);
+    ua.out = out_unc;
+    hipError_t e = dls::launch_uncertainty(ua, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "draft_block_adaptive uncertainty launch");
+  }
   if (head->prepared) {
     const dls::PersistPlan pl = dls::persist_plan(ch, batch, B, long_dtype, prior != nullptr, persist_groups(cus));
     if (pl.ok) {
@@ -349,6 +426,7 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_d
       }
       pa.literal = (fusion.flags & DLS_FIRST_ROW_LONG_ONLY) ? 1 : 0;
       pa.smp = smp;
+      pa.unc = out_unc;
       pa.ordinary_launch = (fusion.flags & DLS_EXCLUSIVE_DEVICE) ? 1 : 0;
       pa.out_tokens = out_tokens;
       pa.out_stats = out_stats;
@@ -384,6 +462,7 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_d
   a.alphas = alphas;
   a.betas = betas;
   a.smp = smp;
+  a.unc = out_unc;
   hipError_t e = dls::launch_draft(a, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "draft_block launch");
   return DLS_OK;
@@ -419,6 +498,17 @@ dls_status dls_draft_block_sampled(const dls_local_head* head, const void* long_
   clear_error();
   return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, schedule.alpha,
                     schedule.beta, sampling, out_tokens, out_stats, workspace, ws_bytes, stream);
+}
+
+dls_status dls_draft_block_adaptive(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,
+                                    const int32_t* last_token, const float* prior, int32_t batch, int32_t B,
+                                    dls_fusion fusion, dls_fusion_schedule schedule, dls_sampling sampling,
+                                    dls_adaptive rule, dls_row_uncertainty* out_uncertainty, int32_t* out_tokens,
+                                    dls_row_stats* out_stats, void* workspace, size_t ws_bytes, void* stream) {
+  clear_error();
+  return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, schedule.alpha,
+                    schedule.beta, sampling, out_tokens, out_stats, workspace, ws_bytes, stream, false, &rule,
+                    out_uncertainty);
 }
 
 dls_status dls_draft_block_noalloc(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,

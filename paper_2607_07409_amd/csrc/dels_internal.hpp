@@ -52,6 +52,26 @@ struct CombineArgs {
 int combine_parts(int64_t rows, int32_t V);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t st);
 
+// adaptive fusion: the measure and gate of dls_adaptive in the form the kernels use
+struct UncRule {
+  int measure;           // DLS_UNC_ENTROPY or DLS_UNC_MAXPROB
+  float inv_log_v;       // 1 / log V (0 when V = 1)
+  float maxprob_scale;   // V / (V - 1) (0 when V = 1)
+  float h_lo, inv_width; // g = clamp((u - h_lo) * inv_width, 0, 1)
+};
+struct UncArgs {
+  const void* long_logits;
+  dls_dtype dtype;
+  int64_t rows;
+  int32_t V;
+  UncRule rule;
+  float4* partials;          // rows * uncertainty_parts(rows, V) when that exceeds 1
+  dls_row_uncertainty* out;  // rows
+};
+int uncertainty_parts(int64_t rows, int32_t V);
+size_t uncertainty_workspace_bytes(int64_t rows, int32_t V);
+hipError_t launch_uncertainty(const UncArgs& a, hipStream_t st);
+
 struct DraftLayout {
   int slice;       // vocabulary rows per workgroup of the LM-head phase
   int groups;      // number of such workgroups
@@ -74,6 +94,7 @@ struct DraftArgs {
   const float* alphas;       // [B] host per-position weights, or NULL (f.alpha everywhere)
   const float* betas;        // [B] host, or NULL (f.beta)
   Sampler smp;               // temperature sampling (smp.inv_temp = 0: greedy)
+  const dls_row_uncertainty* unc;   // [batch, B] adaptive-fusion gates, or NULL (gate 1)
 };
 hipError_t launch_draft(const DraftArgs& a, hipStream_t st);
 
@@ -134,6 +155,7 @@ struct PersistArgs {
   float al_j[64], be_j[64];  // fusion weights of each draft position (B <= 64)
   int literal;
   Sampler smp;               // temperature sampling (smp.inv_temp = 0: greedy)
+  const dls_row_uncertainty* unc;   // [batch, B] adaptive-fusion gates, or NULL (gate 1)
   int ordinary_launch;       // host only: ordinary instead of cooperative dispatch
   int32_t* out_tokens;
   dls_row_stats* out_stats;

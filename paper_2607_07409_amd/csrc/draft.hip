@@ -161,7 +161,7 @@ __global__ __launch_bounds__(kThreads) void k_lmhead(const WT* __restrict__ w_vo
                                                      const float* __restrict__ prior, float wl, float al,
                                                      float be, int slice, int long_only,
                                                      Partial* __restrict__ partials, int batch, Sampler smp,
-                                                     int j) {
+                                                     int j, const dls_row_uncertainty* __restrict__ unc, int B) {
   constexpr int N = Chunk<WT>::N;
   extern __shared__ float smem[];
   float* s_rho = smem;                       // kBC * r
@@ -220,6 +220,9 @@ __global__ __launch_bounds__(kThreads) void k_lmhead(const WT* __restrict__ w_vo
     const bool sample = smp.inv_temp != 0.f;
     for (int b = 0; b < nb; ++b) {
       const LT* lrow = long_j + (size_t)(b0 + b) * long_bstride;
+      // adaptive fusion: this row's gate scales the local terms
+      const float g = unc ? unc[(size_t)(b0 + b) * B + j].gate : 1.f;
+      const float alb = al * g, beb = be * g;
       Partial P = partial_empty();
       for (int i = threadIdx.x; i < nv; i += kThreads) {
         const int v = v0 + i;
@@ -229,8 +232,8 @@ __global__ __launch_bounds__(kThreads) void k_lmhead(const WT* __restrict__ w_vo
           f = weighted(wl, a);
         } else {
           float s = s_S[b * slice + i];
-          f = __builtin_fmaf(al, s, weighted(wl, a));
-          if (PRIOR) f = minus_weighted(f, be, prior[v]);
+          f = __builtin_fmaf(alb, s, weighted(wl, a));
+          if (PRIOR) f = minus_weighted(f, beb, prior[v]);
           lse_fold<1>(P.S, &s, s);
         }
         lse_fold<1>(P.L, &a, a);
@@ -257,7 +260,8 @@ __global__ __launch_bounds__(kThreads) void k_select(const Partial* __restrict__
                                                      float al, int long_only, int j, int B,
                                                      int32_t* __restrict__ out_tokens,
                                                      dls_row_stats* __restrict__ out_stats,
-                                                     int32_t* __restrict__ tok_next, Sampler smp) {
+                                                     int32_t* __restrict__ tok_next, Sampler smp,
+                                                     const dls_row_uncertainty* __restrict__ unc) {
   __shared__ Partial sh[kWaves];
   const int b = blockIdx.x;
   Partial P = partial_empty();
@@ -267,7 +271,8 @@ __global__ __launch_bounds__(kThreads) void k_select(const Partial* __restrict__
     int32_t t;
     const bool sample = smp.inv_temp != 0.f;
     const int ti = P.i1 == 0x7fffffff ? 0 : P.i1;
-    finalize_row(P, wl, al, long_only != 0, &t, out_stats ? out_stats + (size_t)b * B + j : nullptr, nullptr,
+    const float alb = unc ? al * unc[(size_t)b * B + j].gate : al;
+    finalize_row(P, wl, alb, long_only != 0, &t, out_stats ? out_stats + (size_t)b * B + j : nullptr, nullptr,
                  sample ? gumbel_at(smp, b, j, ti) : 0.f, smp.temp);
     out_tokens[(size_t)b * B + j] = t;
     tok_next[b] = t;
@@ -332,10 +337,10 @@ hipError_t launch_draft_t(const DraftArgs& a, hipStream_t st) {
     }
     k_lmhead<WT, LT, PRIOR><<<a.lay.groups, kThreads, lds, st>>>(
         w_vocab, V, r, rho, L + (size_t)j * V, bstride, a.prior, wl, al, be, a.lay.slice, long_only ? 1 : 0,
-        part, batch, a.smp, j);
+        part, batch, a.smp, j, a.unc, B);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     k_select<<<batch, kThreads, 0, st>>>(part, a.lay.groups, wl, al, long_only ? 1 : 0, j, B, a.out_tokens,
-                                         a.out_stats, tok, a.smp);
+                                         a.out_stats, tok, a.smp, a.unc);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     tok_in = tok;
   }

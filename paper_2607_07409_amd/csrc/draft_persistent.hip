@@ -55,7 +55,7 @@ PersistPlan persist_plan(const dls_local_head& h, int32_t batch, int32_t B, dls_
     size_t lds = region_a + (((size_t)ll_slots * rows_max * esz + 15) & ~(size_t)15);
     if (prior) lds += (size_t)rows_max * 4;
     lds += (size_t)2 * kPlane * 2 + (size_t)16 * pl.rpg * 16 + (size_t)((batch + 15) / 16) * 16 * 48 * 4 +
-           (size_t)4 * 16 * sizeof(Partial) + (size_t)kMaxBatch * 8 + (size_t)kMaxBatch * 4 + 16;
+           (size_t)4 * 16 * sizeof(Partial) + (size_t)kMaxBatch * 8 + (size_t)kMaxBatch * 4 + 16 * 4 + 16;
     *rows_out = rows_max;
     *region_out = region_a;
     return lds;

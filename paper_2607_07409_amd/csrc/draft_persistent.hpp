@@ -673,6 +673,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   p += (size_t)kMaxBatch * 8;
   int* s_tok = (int*)p;                             // kMaxBatch
   p += (size_t)kMaxBatch * 4;
+  float* s_gate = (float*)p;                        // 16 slots: the M tile's adaptive-fusion gates
+  p += (size_t)16 * 4;
   lds_flag_t* s_fail = (lds_flag_t*)p;              // sticky failure flag
 
   // A failed call leaves outputs that cannot pass for a draft: token -1 at every position
@@ -1207,6 +1209,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     // ======================= vocabulary head + fused combine (all workgroups) =======================
     for (int mt = 0; mt < mtiles; ++mt) {
       const int nb = batch - mt * 16 < 16 ? batch - mt * 16 : 16;
+      // the slots' gates (1 without adaptive fusion), read by the folds after the staging barrier
+      if (tid < 16) s_gate[tid] = (a.unc && tid < nb) ? a.unc[(size_t)(mt * 16 + tid) * Bk + j].gate : 1.f;
       // long logits of the owned rows (independent of rho: in flight while rho is awaited).
       // Wide batches: 16-byte loads over [slot][row] flattened, eight per thread in flight, so
       // that 16 slots cost a round trip or two rather than one each
@@ -1366,10 +1370,10 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         const int v = v_base + row;
         const bool ok = g4 < ntile && v < V;
         const int rowc = ok ? row : 0;   // an in-range LDS row for lanes without an entry
-        const float alx = long_only ? 0.f : al, bex = long_only ? 0.f : be;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           if (i < nb) {   // uniform
+            const float alx = long_only ? 0.f : al * s_gate[i], bex = long_only ? 0.f : be * s_gate[i];
             const float xr = to_f32(s_ll[i * a.rows_max + rowc]);
             const float x = ok ? xr : -INFINITY;
             const float sv = PACK ? s_stash[(g4 * 4 + i) * 16 + n16] + s_stash[((4 + g4) * 4 + i) * 16 + n16]
@@ -1397,7 +1401,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         const bool sok = sl_own < nb;
         const int sl = sok ? sl_own : 0;
         // the long-only first row of the literal schedule: no head term, no prior, no short sum
-        const float alx = long_only ? 0.f : al, bex = long_only ? 0.f : be;
+        const float gs = s_gate[sl];
+        const float alx = long_only ? 0.f : al * gs, bex = long_only ? 0.f : be * gs;
         float x[4];
         if constexpr (sizeof(LT) == 2) {
           const uint2 raw = *(const uint2*)(s_ll + (size_t)sl * a.rows_max + row0);
@@ -1611,7 +1616,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       if (tid == 0) {
         int t;
         const int ti = P.i1 == 0x7fffffff ? 0 : P.i1;   // the token finalize_row decodes
-        finalize_row(P, wl, a.al_j[jm], a.literal && jm == 0, &t, a.out_stats + (size_t)b * Bk + jm, nullptr,
+        const float alr = a.unc ? a.al_j[jm] * a.unc[(size_t)b * Bk + jm].gate : a.al_j[jm];
+        finalize_row(P, wl, alr, a.literal && jm == 0, &t, a.out_stats + (size_t)b * Bk + jm, nullptr,
                      SAMPLE ? gumbel_at(a.smp, b, jm, ti) : 0.f, a.smp.temp);
       }
       __syncthreads();

@@ -57,17 +57,19 @@ def check_rows(gpu_tok, gpu_stats, long_rows, short_rows, prior, w_long, alpha, 
 
 
 def check_draft(gpu_tok, gpu_stats, head, long_logits, last_token, prior, w_long, alpha, beta,
-                literal=False, sequences=None, temperature=0.0, seed=0):
+                literal=False, sequences=None, temperature=0.0, seed=0, gates=None):
     """Replay the oracle on the GPU's tokens and apply the comparison protocol.  With
     temperature > 0 the oracle draws the same Gumbel noise (seed) and the gaps and margins
     are those of the perturbed values l / T + g, so a near-tie there is tolerated likewise.
+    gates: the oracle's own adaptive-fusion gates [batch, B] (never the GPU's).
 
     Returns a report dict (near-tie count, max errors, fusion-active fraction, the oracle result)."""
     gt = np.asarray(gpu_tok)
     batch, B = gt.shape
     seqs = list(range(batch)) if sequences is None else list(sequences)
     ref = O.draft_block(head, long_logits, last_token, prior, w_long, alpha, beta,
-                        first_row_long_only=literal, force=gt, sequences=seqs, temperature=temperature, seed=seed)
+                        first_row_long_only=literal, force=gt, sequences=seqs, temperature=temperature, seed=seed,
+                        gates=gates)
     near = 0
     active = 0
     for b in seqs:

@@ -44,10 +44,12 @@ def test_struct_layout_matches_c(tmp_path):
 #include <stddef.h>
 #include "{HEADER}"
 int main(void) {{
-  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(dls_local_head), sizeof(dls_row_stats),
-         sizeof(dls_fusion), offsetof(dls_local_head, dtype), offsetof(dls_local_head, emb),
+  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(dls_local_head),
+         sizeof(dls_row_stats), sizeof(dls_fusion), offsetof(dls_local_head, dtype), offsetof(dls_local_head, emb),
          offsetof(dls_local_head, w_vocab), offsetof(dls_fusion, flags), offsetof(dls_local_head, kind),
-         sizeof(dls_sampling), offsetof(dls_sampling, seed), offsetof(dls_local_head, prepared_bytes));
+         sizeof(dls_sampling), offsetof(dls_sampling, seed), offsetof(dls_local_head, prepared_bytes),
+         sizeof(dls_adaptive), offsetof(dls_adaptive, h_hi), sizeof(dls_row_uncertainty),
+         offsetof(dls_row_uncertainty, gate));
   return 0;
 }}''')
     exe = tmp_path / "lay"
@@ -56,13 +58,14 @@ int main(void) {{
     want = [ctypes.sizeof(b.LocalHeadC), ctypes.sizeof(b.RowStats), ctypes.sizeof(b.Fusion),
             b.LocalHeadC.dtype.offset, b.LocalHeadC.emb.offset, b.LocalHeadC.w_vocab.offset,
             b.Fusion.flags.offset, b.LocalHeadC.kind.offset, ctypes.sizeof(b.Sampling), b.Sampling.seed.offset,
-            b.LocalHeadC.prepared_bytes.offset]
+            b.LocalHeadC.prepared_bytes.offset, ctypes.sizeof(b.Adaptive), b.Adaptive.h_hi.offset, 16,
+            4 * b.UNC_FIELDS.index("gate")]
     assert got == want
 
 
 def test_header_compiles_as_cpp(tmp_path):
     src = tmp_path / "h.cpp"
-    src.write_text(f'#include "{HEADER}"\nint main() {{ return dls_abi_version() == 3 ? 0 : 1; }}\n')
+    src.write_text(f'#include "{HEADER}"\nint main() {{ return dls_abi_version() == 4 ? 0 : 1; }}\n')
     subprocess.run(["g++", "-std=c++17", "-Wall", "-Werror", "-c", str(src), "-o", str(tmp_path / "h.o")],
                    check=True)
 
@@ -72,7 +75,7 @@ def test_status_strings():
     for code, name in b.STATUS.items():
         assert L.dls_status_string(code).decode() == name
     assert L.dls_status_string(99).decode() == "DLS_UNKNOWN_STATUS"
-    assert L.dls_abi_version() == 3
+    assert L.dls_abi_version() == 4
 
 
 def _head(**kw):
@@ -319,3 +322,71 @@ def test_error_query_rejects_bad_arguments():
     if not HAS_GPU:
         assert b.STATUS[L.dls_draft_block_error(FAKE[0], 1 << 20, FAKE[1], None)] == "DLS_ERR_DEVICE"
         assert b.STATUS[L.dls_draft_block_error(None, 0, FAKE[1], None)] == "DLS_ERR_DEVICE"
+
+
+def _adaptive(head, rule, unc=FAKE[10], **kw):
+    a = dict(long=FAKE[5], ldt=b.DLS_BF16, last=FAKE[6], prior=None, batch=2, B=4, f=b.fusion(),
+             tok=FAKE[7], st=FAKE[8], ws=FAKE[9], wsb=1 << 30)
+    a.update(kw)
+    L = b.lib()
+    rc = L.dls_draft_block_adaptive(ctypes.byref(head), a["long"], a["ldt"], a["last"], a["prior"], a["batch"],
+                                    a["B"], a["f"], b.Schedule(None, None), b.Sampling(0.0, 0, 0), rule, unc,
+                                    a["tok"], a["st"], a["ws"], a["wsb"], None)
+    return rc, L.dls_last_error().decode()
+
+
+def _unc(rule, long=FAKE[0], dt=b.DLS_BF16, rows=16, V=151936, out=FAKE[1], ws=FAKE[2], wsb=1 << 24):
+    L = b.lib()
+    rc = L.dls_long_uncertainty(long, dt, rows, V, rule, out, ws, wsb, None)
+    return b.STATUS[rc], L.dls_last_error().decode()
+
+
+BAD_RULES = [b.Adaptive(2, 0.0, 1.0, 0), b.Adaptive(-1, 0.0, 1.0, 0), b.Adaptive(0, 0.5, 0.5, 0),
+             b.Adaptive(1, 0.7, 0.2, 0), b.Adaptive(0, float("nan"), 1.0, 0), b.Adaptive(0, 0.0, float("inf"), 0),
+             b.Adaptive(0, 0.0, 1.0, 3)]
+
+
+def test_adaptive_rejects_bad_rules():
+    for rule in BAD_RULES:
+        st, msg = _unc(rule)
+        assert st == "DLS_ERR_ARG", (rule.measure, rule.h_lo, rule.h_hi, msg)
+        rc, msg = _adaptive(_head(), rule)
+        assert b.STATUS[rc] == "DLS_ERR_ARG", msg
+    good = b.adaptive_rule(b.UNC_ENTROPY, 0.1, 0.9)
+    assert b.STATUS[_adaptive(_head(), good, unc=None)[0]] == "DLS_ERR_ARG"
+    assert b.STATUS[_adaptive(_head(), good, unc=ctypes.c_void_p(FAKE[10].value + 2))[0]] == "DLS_ERR_ARG"
+    assert b.STATUS[_adaptive(_head(), good, B=65)[0]] == "DLS_ERR_SHAPE"
+    assert _adaptive(_head(), good, batch=0, long=None, tok=None, unc=None)[0] == 0
+
+
+def test_long_uncertainty_rejects_bad_arguments():
+    good = b.adaptive_rule(b.UNC_MAXPROB, -0.5, 0.5)
+    assert _unc(good, dt=9)[0] == "DLS_ERR_DTYPE"
+    assert _unc(good, V=0)[0] == "DLS_ERR_SHAPE"
+    assert _unc(good, rows=-1)[0] == "DLS_ERR_SHAPE"
+    assert _unc(good, long=None)[0] == "DLS_ERR_ARG"
+    assert _unc(good, out=None)[0] == "DLS_ERR_ARG"
+    assert _unc(good, long=ctypes.c_void_p(FAKE[0].value + 4))[0] == "DLS_ERR_ARG"
+    need = b.long_uncertainty_workspace_size(16, 151936)
+    assert need > 0
+    assert _unc(good, wsb=need - 1)[0] == "DLS_ERR_WORKSPACE"
+    assert _unc(good, ws=None)[0] == "DLS_ERR_ARG"
+    assert _unc(good, rows=0, long=None, out=None)[0] == "DLS_OK"
+    # enough rows to cover the GPU: one range per row, no workspace
+    assert b.long_uncertainty_workspace_size(4096, 151936) == 0
+    assert _unc(good, rows=4096, ws=None, wsb=0)[0] in ("DLS_ERR_DEVICE", "DLS_OK")
+
+
+def test_draft_workspace_includes_the_uncertainty_partials():
+    L = b.lib()
+    h = _head(V=151936, d=64, H=32, r=16)
+    plain = L.dls_draft_block_workspace_size(ctypes.byref(h), 1, 16)
+    assert plain >= b.long_uncertainty_workspace_size(16, 151936) > 0
+
+
+@pytest.mark.skipif(HAS_GPU, reason="would launch on fake pointers when a GPU is present")
+def test_adaptive_valid_arguments_stop_at_device_check():
+    for m in (b.UNC_ENTROPY, b.UNC_MAXPROB):
+        rc, msg = _adaptive(_head(), b.adaptive_rule(m, -1.0, 2.0))
+        assert b.STATUS[rc] == "DLS_ERR_DEVICE", msg
+        assert _unc(b.adaptive_rule(m, 0.2, 0.3))[0] == "DLS_ERR_DEVICE"
