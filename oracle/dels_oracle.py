@@ -40,7 +40,8 @@ Readings where the paper is silent (each is also listed in the design notes):
 * Adaptive fusion (Sec. 7 proposes it as future work without a rule): row (b, j)
   fuses with alpha_j * g and beta_j * g, g = clamp((u - h_lo) / (h_hi - h_lo), 0, 1)
   of that row's uncertainty u, either the entropy of p_L over log V or
-  (1 - max p_L) / (1 - 1/V); u = 0 when V = 1.
+  (1 - max p_L) / (1 - 1/V); u = 0 when V = 1 and u = 1 for a row without a
+  finite entry.
 * Sampling at temperature T > 0 (the paper reports T = 0 and T = 1 but not how
   it draws) is the Gumbel-max rule on l / T.  The noise of entry v of row
   (sequence b, position j) comes from Philox4x32-10 keyed by the seed at
@@ -195,8 +196,10 @@ UNC_ENTROPY, UNC_MAXPROB = 0, 1
 
 def long_entropy(long_row) -> float:
     """H(p_L) = -sum_v p_v log p_v in nats, p = softmax(l_L); a masked entry (p_v = 0) adds
-    nothing (p log p -> 0)."""
+    nothing (p log p -> 0).  NaN for a row without a finite entry (no distribution)."""
     x = np.asarray(long_row, dtype=F64)
+    if not np.isfinite(x).any():
+        return float("nan")
     logp = x - logsumexp(x)
     p = np.exp(logp)
     keep = p > 0
@@ -204,15 +207,21 @@ def long_entropy(long_row) -> float:
 
 
 def long_max_prob(long_row) -> float:
-    """max_v p_v, p = softmax(l_L): the confidence of the long logits in their own argmax."""
+    """max_v p_v, p = softmax(l_L): the confidence of the long logits in their own argmax.
+    NaN for a row without a finite entry."""
     x = np.asarray(long_row, dtype=F64)
+    if not np.isfinite(x).any():
+        return float("nan")
     return float(np.exp(np.max(x) - logsumexp(x)))
 
 
 def uncertainty(long_row, measure: int) -> float:
     """u in [0, 1]: 0 when p_L is one-hot, 1 when it is uniform over the whole vocabulary.
-    UNC_ENTROPY: H(p_L) / log V.  UNC_MAXPROB: (1 - max p_L) / (1 - 1/V).  V = 1: u = 0."""
+    UNC_ENTROPY: H(p_L) / log V.  UNC_MAXPROB: (1 - max p_L) / (1 - 1/V).  V = 1: u = 0.
+    A row without a finite entry carries no information: u = 1."""
     V = np.asarray(long_row).shape[0]
+    if not np.isfinite(np.asarray(long_row, dtype=F64)).any():
+        return 1.0
     if V == 1:
         return 0.0
     if measure == UNC_ENTROPY:

@@ -63,6 +63,13 @@ def test_exact_rational_distributions(counts):
     assert O.uncertainty(row, O.UNC_ENTROPY) == pytest.approx(h_exact / math.log(V), rel=1e-13, abs=1e-15)
 
 
+def test_row_without_a_finite_entry_is_fully_uncertain():
+    row = np.full(12, -np.inf)
+    assert math.isnan(O.long_entropy(row)) and math.isnan(O.long_max_prob(row))
+    assert O.uncertainty(row, O.UNC_ENTROPY) == 1.0 and O.uncertainty(row, O.UNC_MAXPROB) == 1.0
+    assert O.adaptive_gates(row[None, None], O.UNC_MAXPROB, 0.2, 0.6)[0, 0] == 1.0
+
+
 @pytest.mark.parametrize("q", [0.5, 0.1, 0.999, 1e-6])
 def test_binary_entropy_closed_form(q):
     row = np.array([math.log(q), math.log1p(-q)]) + 3.0

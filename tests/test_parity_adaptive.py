@@ -31,11 +31,8 @@ def _oracle_unc(rows, measure, lo, hi):
     out = []
     for x in rows:
         x = np.asarray(x, np.float64)
-        fin = np.isfinite(x).any()
-        h = O.long_entropy(x) if fin else float("nan")
-        p = O.long_max_prob(x) if fin else float("nan")
-        u = O.uncertainty(x, measure) if fin else 1.0
-        out.append((h, p, u, O.gate(u, lo, hi)))
+        u = O.uncertainty(x, measure)
+        out.append((O.long_entropy(x), O.long_max_prob(x), u, O.gate(u, lo, hi)))
     return np.asarray(out)
 
 
