@@ -62,8 +62,7 @@ def test_combine_shapes(rows, V, dtype, seed):
 def test_combine_serving_shapes(rows):
     L = W.make_logit_rows(rows, QV, "bf16", 10 + rows, "onehot", 3.0, purpose=20)
     S = W.make_logit_rows(rows, QV, "bf16", 10 + rows, "normal", 2.0, purpose=21)
-    ids = list(range(0, rows, 4)) + [rows - 1]
-    _check(L, S, None, 1.0, 0.5, 0.0, row_ids=ids)
+    _check(L, S, None, 1.0, 0.5, 0.0)        # every row against the oracle
 
 
 @pytest.mark.parametrize("wl,al,be", [(1.0, 0.0, 0.0), (0.0, 1.0, 0.0), (1.0, 0.3, 0.3), (1.0, 1.0, 1.0),
@@ -157,7 +156,7 @@ def test_combine_tokens_only_matches(rows, V, dtype, seed, prior):
     assert s_only is None
     assert torch.equal(t_stats, t_only)
     tok = t_only.cpu().numpy()
-    for i in range(0, rows, max(1, rows // 8)):
+    for i in range(rows):
         r = O.combine_row(np.asarray(L[i], np.float32), np.asarray(S[i], np.float32), P, 1.0, 0.5, be)
         assert tok[i] == r.token or r.gap < TOL, (i, tok[i], r.token, r.gap)
 
