@@ -157,7 +157,7 @@ typedef struct dls_local_head {
  * small, 1.98 GB for V = 151,936, H = 1024, r = 256; Markov: V*r*2 + small) and stays
  * valid while the head tensors are unchanged.  Requirements: dtype DLS_BF16, r in {32,
  * 64, 128, 256}, and H a multiple of 32 for the RNN head; otherwise DLS_ERR_SHAPE /
- * DLS_ERR_DTYPE.  Asynchronous on `stream`. */
+ * DLS_ERR_DTYPE, and dls_prepare_head_size returns 0.  Asynchronous on `stream`. */
 size_t dls_prepare_head_size(const dls_local_head *head);
 dls_status dls_prepare_head(const dls_local_head *head, void *prepared, size_t bytes, void *stream);
 

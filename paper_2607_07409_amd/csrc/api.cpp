@@ -78,8 +78,17 @@ dls_status hip_fail(hipError_t e, const char* what) {
   return fail(DLS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-bool valid_dtype(dls_dtype t) { return t == DLS_F32 || t == DLS_BF16; }
-size_t dsize(dls_dtype t) { return t == DLS_BF16 ? 2 : 4; }
+// An enum from a C caller may hold any int; loading an out-of-range value as the C++ enum is
+// undefined, so caller-supplied enums are read through their representation until validated.
+template <typename E>
+int enum_bits(const E& e) {
+  static_assert(sizeof(E) == sizeof(int), "the C enums of the ABI are int-sized");
+  int v;
+  std::memcpy(&v, &e, sizeof v);
+  return v;
+}
+
+bool valid_dtype(int t) { return t == DLS_F32 || t == DLS_BF16; }
 
 dls_status check_fusion(const dls_fusion& f) {
   if (!std::isfinite(f.w_long) || !std::isfinite(f.alpha) || !std::isfinite(f.beta))
@@ -114,7 +123,7 @@ dls_status check_head(const dls_local_head* h) {
   if (!h) return fail(DLS_ERR_ARG, "head is NULL");
   if (h->kind != DLS_HEAD_RNN && h->kind != DLS_HEAD_MARKOV) return fail(DLS_ERR_ARG, "unknown head kind %d", h->kind);
   const bool markov = h->kind == DLS_HEAD_MARKOV;
-  if (!valid_dtype(h->dtype)) return fail(DLS_ERR_DTYPE, "unknown head dtype %d", (int)h->dtype);
+  if (!valid_dtype(enum_bits(h->dtype))) return fail(DLS_ERR_DTYPE, "unknown head dtype %d", enum_bits(h->dtype));
   if (h->V < 1 || h->V > (1 << 24)) return fail(DLS_ERR_SHAPE, "V=%d outside [1, 2^24]", h->V);
   if (!markov && (h->d < 8 || h->d > 16384 || h->d % 8))
     return fail(DLS_ERR_SHAPE, "d=%d must be a multiple of 8 in [8, 16384]", h->d);
@@ -128,6 +137,19 @@ dls_status check_head(const dls_local_head* h) {
     if (!ps[i]) return fail(DLS_ERR_ARG, "head.%s is NULL", nm[i]);
     if (!aligned(ps[i], 16)) return fail(DLS_ERR_ARG, "head.%s is not 16-byte aligned", nm[i]);
   }
+  return DLS_OK;
+}
+
+// A head that dls_prepare_head accepts: a valid bf16 head with r in {32, 64, 128, 256} and, for
+// the RNN head, H a multiple of 32.
+dls_status check_preparable(const dls_local_head* head) {
+  dls_status s = check_head(head);
+  if (s != DLS_OK) return s;
+  if (head->dtype != DLS_BF16) return fail(DLS_ERR_DTYPE, "only bf16 heads can be prepared");
+  if (head->kind == DLS_HEAD_RNN && head->H % 32)
+    return fail(DLS_ERR_SHAPE, "H=%d must be a multiple of 32 to prepare", head->H);
+  if (!(head->r == 32 || head->r == 64 || head->r == 128 || head->r == 256))
+    return fail(DLS_ERR_SHAPE, "r=%d must be 32, 64, 128 or 256 to prepare", head->r);
   return DLS_OK;
 }
 
@@ -148,7 +170,7 @@ dls_local_head canon(const dls_local_head& h) {
 extern "C" {
 
 const char* dls_status_string(dls_status s) {
-  switch (s) {
+  switch (enum_bits(s)) {
     case DLS_OK: return "DLS_OK";
     case DLS_ERR_ARG: return "DLS_ERR_ARG";
     case DLS_ERR_SHAPE: return "DLS_ERR_SHAPE";
@@ -173,12 +195,13 @@ size_t dls_combine_logits_workspace_size(int64_t rows, int32_t V) {
   return b;
 }
 
-dls_status dls_combine_logits(const void* long_logits, const void* short_logits, dls_dtype dtype,
+dls_status dls_combine_logits(const void* long_logits, const void* short_logits, dls_dtype dtype_in,
                               const float* prior, int64_t rows, int32_t V, dls_fusion fusion,
                               int32_t* out_token, dls_row_stats* out_stats, float* out_scores,
                               void* workspace, size_t ws_bytes, void* stream) {
   clear_error();
-  if (!valid_dtype(dtype)) return fail(DLS_ERR_DTYPE, "unknown dtype %d", (int)dtype);
+  if (!valid_dtype(enum_bits(dtype_in))) return fail(DLS_ERR_DTYPE, "unknown dtype %d", enum_bits(dtype_in));
+  const dls_dtype dtype = static_cast<dls_dtype>(enum_bits(dtype_in));
   if (rows < 0 || rows > (1 << 20)) return fail(DLS_ERR_SHAPE, "rows=%lld outside [0, 2^20]", (long long)rows);
   if (V < 1 || V > (1 << 24)) return fail(DLS_ERR_SHAPE, "V=%d outside [1, 2^24]", V);
   dls_status s = check_fusion(fusion);
@@ -218,20 +241,15 @@ dls_status dls_combine_logits(const void* long_logits, const void* short_logits,
 }
 
 size_t dls_prepare_head_size(const dls_local_head* head) {
-  if (!head || check_head(head) != DLS_OK) return 0;
+  if (check_preparable(head) != DLS_OK) return 0;
   clear_error();
   return dls::prepared_layout(canon(*head)).total;
 }
 
 dls_status dls_prepare_head(const dls_local_head* head, void* prepared, size_t bytes, void* stream) {
   clear_error();
-  dls_status s = check_head(head);
+  dls_status s = check_preparable(head);
   if (s != DLS_OK) return s;
-  if (head->dtype != DLS_BF16) return fail(DLS_ERR_DTYPE, "only bf16 heads can be prepared");
-  if (head->kind == DLS_HEAD_RNN && head->H % 32)
-    return fail(DLS_ERR_SHAPE, "H=%d must be a multiple of 32 to prepare", head->H);
-  if (!(head->r == 32 || head->r == 64 || head->r == 128 || head->r == 256))
-    return fail(DLS_ERR_SHAPE, "r=%d must be 32, 64, 128 or 256 to prepare", head->r);
   if (!prepared || !aligned(prepared, 256)) return fail(DLS_ERR_ARG, "prepared buffer is NULL or not 256-byte aligned");
   const dls_local_head ch = canon(*head);
   const size_t need = dls::prepared_layout(ch).total;
@@ -257,11 +275,12 @@ size_t dls_long_uncertainty_workspace_size(int64_t rows, int32_t V) {
   return dls::uncertainty_workspace_bytes(rows, V);
 }
 
-dls_status dls_long_uncertainty(const void* long_logits, dls_dtype dtype, int64_t rows, int32_t V,
+dls_status dls_long_uncertainty(const void* long_logits, dls_dtype dtype_in, int64_t rows, int32_t V,
                                 dls_adaptive rule, dls_row_uncertainty* out, void* workspace, size_t ws_bytes,
                                 void* stream) {
   clear_error();
-  if (!valid_dtype(dtype)) return fail(DLS_ERR_DTYPE, "unknown dtype %d", (int)dtype);
+  if (!valid_dtype(enum_bits(dtype_in))) return fail(DLS_ERR_DTYPE, "unknown dtype %d", enum_bits(dtype_in));
+  const dls_dtype dtype = static_cast<dls_dtype>(enum_bits(dtype_in));
   if (rows < 0 || rows > (1 << 24)) return fail(DLS_ERR_SHAPE, "rows=%lld outside [0, 2^24]", (long long)rows);
   if (V < 1 || V > (1 << 24)) return fail(DLS_ERR_SHAPE, "V=%d outside [1, 2^24]", V);
   dls_status s = check_rule(rule);
@@ -305,7 +324,7 @@ dls_status check_prepared_size(const dls_local_head* head) {
 
 // The drafting entry points.  noalloc: run in the current device's scratch array instead of
 // the caller's workspace (workspace and ws_bytes are then ignored).
-dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_dtype long_dtype,
+dls_status draft_impl(const dls_local_head* head, const void* long_logits, int long_dtype_bits,
                       const int32_t* last_token, const float* prior, int32_t batch, int32_t B, dls_fusion fusion,
                       const float* alphas, const float* betas, dls_sampling sampling, int32_t* out_tokens,
                       dls_row_stats* out_stats, void* workspace, size_t ws_bytes, void* stream,
@@ -314,7 +333,8 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, dls_d
   dls_status s = check_head(head);
   if (s != DLS_OK) return s;
   if ((s = check_prepared_size(head)) != DLS_OK) return s;
-  if (!valid_dtype(long_dtype)) return fail(DLS_ERR_DTYPE, "unknown long-logit dtype %d", (int)long_dtype);
+  if (!valid_dtype(long_dtype_bits)) return fail(DLS_ERR_DTYPE, "unknown long-logit dtype %d", long_dtype_bits);
+  const dls_dtype long_dtype = static_cast<dls_dtype>(long_dtype_bits);
   if (batch < 0 || batch > 256) return fail(DLS_ERR_SHAPE, "batch=%d outside [0, 256]", batch);
   if (B < 0 || B > 64) return fail(DLS_ERR_SHAPE, "B=%d outside [0, 64]", B);
   if ((s = check_fusion(fusion)) != DLS_OK) return s;
@@ -477,7 +497,7 @@ dls_status dls_draft_block(const dls_local_head* head, const void* long_logits, 
                            dls_fusion fusion, int32_t* out_tokens, dls_row_stats* out_stats, void* workspace,
                            size_t ws_bytes, void* stream) {
   clear_error();
-  return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, nullptr, nullptr,
+  return draft_impl(head, long_logits, enum_bits(long_dtype), last_token, prior, batch, B, fusion, nullptr, nullptr,
                     dls_sampling{0.f, 0u, 0ull}, out_tokens, out_stats, workspace, ws_bytes, stream);
 }
 
@@ -486,7 +506,7 @@ dls_status dls_draft_block_scheduled(const dls_local_head* head, const void* lon
                                      dls_fusion fusion, dls_fusion_schedule schedule, int32_t* out_tokens,
                                      dls_row_stats* out_stats, void* workspace, size_t ws_bytes, void* stream) {
   clear_error();
-  return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, schedule.alpha,
+  return draft_impl(head, long_logits, enum_bits(long_dtype), last_token, prior, batch, B, fusion, schedule.alpha,
                     schedule.beta, dls_sampling{0.f, 0u, 0ull}, out_tokens, out_stats, workspace, ws_bytes, stream);
 }
 
@@ -496,7 +516,7 @@ dls_status dls_draft_block_sampled(const dls_local_head* head, const void* long_
                                    int32_t* out_tokens, dls_row_stats* out_stats, void* workspace, size_t ws_bytes,
                                    void* stream) {
   clear_error();
-  return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, schedule.alpha,
+  return draft_impl(head, long_logits, enum_bits(long_dtype), last_token, prior, batch, B, fusion, schedule.alpha,
                     schedule.beta, sampling, out_tokens, out_stats, workspace, ws_bytes, stream);
 }
 
@@ -506,7 +526,7 @@ dls_status dls_draft_block_adaptive(const dls_local_head* head, const void* long
                                     dls_adaptive rule, dls_row_uncertainty* out_uncertainty, int32_t* out_tokens,
                                     dls_row_stats* out_stats, void* workspace, size_t ws_bytes, void* stream) {
   clear_error();
-  return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, schedule.alpha,
+  return draft_impl(head, long_logits, enum_bits(long_dtype), last_token, prior, batch, B, fusion, schedule.alpha,
                     schedule.beta, sampling, out_tokens, out_stats, workspace, ws_bytes, stream, false, &rule,
                     out_uncertainty);
 }
@@ -515,7 +535,7 @@ dls_status dls_draft_block_noalloc(const dls_local_head* head, const void* long_
                                    const int32_t* last_token, const float* prior, int32_t batch, int32_t B,
                                    dls_fusion fusion, int32_t* out_tokens, dls_row_stats* out_stats, void* stream) {
   clear_error();
-  return draft_impl(head, long_logits, long_dtype, last_token, prior, batch, B, fusion, nullptr, nullptr,
+  return draft_impl(head, long_logits, enum_bits(long_dtype), last_token, prior, batch, B, fusion, nullptr, nullptr,
                     dls_sampling{0.f, 0u, 0ull}, out_tokens, out_stats, nullptr, 0, stream, true);
 }
 
@@ -541,7 +561,7 @@ dls_status dls_draft_block_error(const void* workspace, size_t ws_bytes, int32_t
 int dls_draft_block_path(const dls_local_head* head, int32_t batch, int32_t B, dls_dtype long_dtype,
                          int has_prior) {
   clear_error();
-  if (check_head(head) != DLS_OK || check_prepared_size(head) != DLS_OK || !valid_dtype(long_dtype) || batch < 1 ||
+  if (check_head(head) != DLS_OK || check_prepared_size(head) != DLS_OK || !valid_dtype(enum_bits(long_dtype)) || batch < 1 ||
       batch > 256 || B < 1 || B > 64)
     return -1;
   if (!head->prepared) return 0;
