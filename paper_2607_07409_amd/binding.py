@@ -5,6 +5,7 @@ and the stream.  Calling anything here without the built library raises at once.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 from typing import Optional
@@ -14,6 +15,7 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libdels.so")
+STRESS_LIB_PATH = os.path.join(_HERE, "libdels_stress.so")   # test build: pauses before every hand-off
 
 DLS_F32, DLS_BF16 = 0, 1
 DLS_HEAD_RNN, DLS_HEAD_MARKOV = 0, 1
@@ -72,54 +74,81 @@ def lib() -> ctypes.CDLL:
     """The loaded HIP library (raises if it has not been built)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
-        L = ctypes.CDLL(LIB_PATH)
-        L.dls_combine_logits_workspace_size.restype = _sz
-        L.dls_combine_logits_workspace_size.argtypes = [_i64, _i32]
-        L.dls_combine_logits.restype = ctypes.c_int
-        L.dls_combine_logits.argtypes = [_vp, _vp, ctypes.c_int, _vp, _i64, _i32, Fusion, _vp, _vp, _vp,
-                                         _vp, _sz, _vp]
-        L.dls_draft_block_workspace_size.restype = _sz
-        L.dls_draft_block_workspace_size.argtypes = [ctypes.POINTER(LocalHeadC), _i32, _i32]
-        L.dls_draft_block.restype = ctypes.c_int
-        L.dls_draft_block.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
-                                      Fusion, _vp, _vp, _vp, _sz, _vp]
-        L.dls_draft_block_scheduled.restype = ctypes.c_int
-        L.dls_draft_block_scheduled.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
-                                                Fusion, Schedule, _vp, _vp, _vp, _sz, _vp]
-        L.dls_draft_block_sampled.restype = ctypes.c_int
-        L.dls_draft_block_sampled.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
-                                              Fusion, Schedule, Sampling, _vp, _vp, _vp, _sz, _vp]
-        L.dls_long_uncertainty_workspace_size.restype = _sz
-        L.dls_long_uncertainty_workspace_size.argtypes = [_i64, _i32]
-        L.dls_long_uncertainty.restype = ctypes.c_int
-        L.dls_long_uncertainty.argtypes = [_vp, ctypes.c_int, _i64, _i32, Adaptive, _vp, _vp, _sz, _vp]
-        L.dls_draft_block_adaptive.restype = ctypes.c_int
-        L.dls_draft_block_adaptive.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
-                                               Fusion, Schedule, Sampling, Adaptive, _vp, _vp, _vp, _vp, _sz, _vp]
-        L.dls_prepare_head_size.restype = _sz
-        L.dls_prepare_head_size.argtypes = [ctypes.POINTER(LocalHeadC)]
-        L.dls_prepare_head.restype = ctypes.c_int
-        L.dls_prepare_head.argtypes = [ctypes.POINTER(LocalHeadC), _vp, _sz, _vp]
-        L.dls_draft_block_noalloc.restype = ctypes.c_int
-        L.dls_draft_block_noalloc.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
-                                              Fusion, _vp, _vp, _vp]
-        L.dls_draft_block_error.restype = ctypes.c_int
-        L.dls_draft_block_error.argtypes = [_vp, _sz, _vp, _vp]
-        L.dls_draft_block_path.restype = ctypes.c_int
-        L.dls_draft_block_path.argtypes = [ctypes.POINTER(LocalHeadC), _i32, _i32, ctypes.c_int, ctypes.c_int]
-        L.dls_unigram_log_prior.restype = ctypes.c_int
-        L.dls_unigram_log_prior.argtypes = [_vp, _i64, _i32, ctypes.c_float, _vp, _vp, _vp]
-        L.dls_accept_len.restype = ctypes.c_int
-        L.dls_accept_len.argtypes = [_vp, _vp, _i32, _i32, _vp, _vp]
-        L.dls_status_string.restype = ctypes.c_char_p
-        L.dls_status_string.argtypes = [ctypes.c_int]
-        L.dls_last_error.restype = ctypes.c_char_p
-        L.dls_last_error.argtypes = []
-        L.dls_abi_version.restype = ctypes.c_int
-        _lib = L
+        _lib = load(LIB_PATH)
     return _lib
+
+
+_loaded = {}
+
+
+def load(path: str) -> ctypes.CDLL:
+    """A build of the library at `path` (the product library, or the delay-injecting test build
+    libdels_stress.so), with the argument types of every entry point; loaded once per path."""
+    if path not in _loaded:
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it with __graft_entry__.build()")
+        _loaded[path] = _configure(ctypes.CDLL(path))
+    return _loaded[path]
+
+
+@contextlib.contextmanager
+def using(path: str):
+    """Route every call of this module to the library at `path` inside the block."""
+    global _lib
+    prev = lib()
+    _lib = load(path)
+    try:
+        yield _lib
+    finally:
+        _lib = prev
+
+
+def _configure(L: ctypes.CDLL) -> ctypes.CDLL:
+    """Argument and result types of every entry point of dels.h."""
+    L.dls_combine_logits_workspace_size.restype = _sz
+    L.dls_combine_logits_workspace_size.argtypes = [_i64, _i32]
+    L.dls_combine_logits.restype = ctypes.c_int
+    L.dls_combine_logits.argtypes = [_vp, _vp, ctypes.c_int, _vp, _i64, _i32, Fusion, _vp, _vp, _vp,
+                                     _vp, _sz, _vp]
+    L.dls_draft_block_workspace_size.restype = _sz
+    L.dls_draft_block_workspace_size.argtypes = [ctypes.POINTER(LocalHeadC), _i32, _i32]
+    L.dls_draft_block.restype = ctypes.c_int
+    L.dls_draft_block.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
+                                  Fusion, _vp, _vp, _vp, _sz, _vp]
+    L.dls_draft_block_scheduled.restype = ctypes.c_int
+    L.dls_draft_block_scheduled.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
+                                            Fusion, Schedule, _vp, _vp, _vp, _sz, _vp]
+    L.dls_draft_block_sampled.restype = ctypes.c_int
+    L.dls_draft_block_sampled.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
+                                          Fusion, Schedule, Sampling, _vp, _vp, _vp, _sz, _vp]
+    L.dls_long_uncertainty_workspace_size.restype = _sz
+    L.dls_long_uncertainty_workspace_size.argtypes = [_i64, _i32]
+    L.dls_long_uncertainty.restype = ctypes.c_int
+    L.dls_long_uncertainty.argtypes = [_vp, ctypes.c_int, _i64, _i32, Adaptive, _vp, _vp, _sz, _vp]
+    L.dls_draft_block_adaptive.restype = ctypes.c_int
+    L.dls_draft_block_adaptive.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
+                                           Fusion, Schedule, Sampling, Adaptive, _vp, _vp, _vp, _vp, _sz, _vp]
+    L.dls_prepare_head_size.restype = _sz
+    L.dls_prepare_head_size.argtypes = [ctypes.POINTER(LocalHeadC)]
+    L.dls_prepare_head.restype = ctypes.c_int
+    L.dls_prepare_head.argtypes = [ctypes.POINTER(LocalHeadC), _vp, _sz, _vp]
+    L.dls_draft_block_noalloc.restype = ctypes.c_int
+    L.dls_draft_block_noalloc.argtypes = [ctypes.POINTER(LocalHeadC), _vp, ctypes.c_int, _vp, _vp, _i32, _i32,
+                                          Fusion, _vp, _vp, _vp]
+    L.dls_draft_block_error.restype = ctypes.c_int
+    L.dls_draft_block_error.argtypes = [_vp, _sz, _vp, _vp]
+    L.dls_draft_block_path.restype = ctypes.c_int
+    L.dls_draft_block_path.argtypes = [ctypes.POINTER(LocalHeadC), _i32, _i32, ctypes.c_int, ctypes.c_int]
+    L.dls_unigram_log_prior.restype = ctypes.c_int
+    L.dls_unigram_log_prior.argtypes = [_vp, _i64, _i32, ctypes.c_float, _vp, _vp, _vp]
+    L.dls_accept_len.restype = ctypes.c_int
+    L.dls_accept_len.argtypes = [_vp, _vp, _i32, _i32, _vp, _vp]
+    L.dls_status_string.restype = ctypes.c_char_p
+    L.dls_status_string.argtypes = [ctypes.c_int]
+    L.dls_last_error.restype = ctypes.c_char_p
+    L.dls_last_error.argtypes = []
+    L.dls_abi_version.restype = ctypes.c_int
+    return L
 
 
 def _check(status: int):

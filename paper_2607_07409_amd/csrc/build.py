@@ -17,6 +17,11 @@ SOURCES = ["api.cpp", "combine.hip", "draft.hip", "accept.hip", "prepare.hip", "
            # the persistent kernel's instantiations, one unit per rank size and decoding mode
            "persist_greedy_r128.hip", "persist_greedy_r256.hip", "persist_sampled_r128.hip",
            "persist_sampled_r256.hip"]
+# the test build libdels_stress.so recompiles the units that include the persistent kernel with
+# DLS_STRESS_DELAYS (pauses before every hand-off publish) and reuses every other object
+STRESS_LIB = os.path.join(PKG, "libdels_stress.so")
+STRESS_UNITS = ["draft_persistent.hip", "persist_greedy_r128.hip", "persist_greedy_r256.hip",
+                "persist_sampled_r128.hip", "persist_sampled_r256.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-Wall", "-Wno-unused-function",
          # no packed fp32 arithmetic in any generated code
@@ -35,22 +40,36 @@ def _run(cmd):
     return out
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(OBJ_DIR, exist_ok=True)
+def build(verbose: bool = False, stress: bool = True) -> str:
+    """Compile every source and link libdels.so; with `stress`, also the test build
+    libdels_stress.so."""
+    os.makedirs(os.path.join(OBJ_DIR, "stress"), exist_ok=True)
 
-    def compile_one(src):
-        obj = os.path.join(OBJ_DIR, src + ".o")
-        out = _run([HIPCC, *FLAGS, "-c", os.path.join(HERE, src), "-o", obj])
+    def compile_one(job):
+        src, extra, sub = job
+        obj = os.path.join(OBJ_DIR, sub, src + ".o")
+        out = _run([HIPCC, *FLAGS, *extra, "-c", os.path.join(HERE, src), "-o", obj])
         if verbose and out.strip():
             print(out)
         return obj
 
-    with ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(compile_one, SOURCES))
-    tmp = LIB + ".tmp"
-    _run([HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", *objs, "-o", tmp])
-    os.replace(tmp, LIB)
+    jobs = [(src, [], "") for src in SOURCES]
+    if stress:
+        jobs += [(src, ["-DDLS_STRESS_DELAYS"], "stress") for src in STRESS_UNITS]
+    with ThreadPoolExecutor(max_workers=min(8, len(jobs))) as ex:
+        objs = list(ex.map(compile_one, jobs))
+    plain = objs[:len(SOURCES)]
+    _link(plain, LIB)
+    if stress:
+        stressed = dict(zip(STRESS_UNITS, objs[len(SOURCES):]))
+        _link([stressed.get(src, o) for src, o in zip(SOURCES, plain)], STRESS_LIB)
     return LIB
+
+
+def _link(objs, lib):
+    tmp = lib + ".tmp"
+    _run([HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", *objs, "-o", tmp])
+    os.replace(tmp, lib)
 
 
 if __name__ == "__main__":

@@ -61,6 +61,29 @@ __device__ __forceinline__ uint32_t ld32(const uint32_t* p) {
 __device__ __forceinline__ void st32(uint32_t* p, uint32_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// Test builds (DLS_STRESS_DELAYS defined; libdels_stress.so): a pseudo-random pause of 0 to
+// about 10 us before each hand-off publish, different for every call, workgroup, wave, position
+// and publish site, so that the hand-offs run under other interleavings; the drafted tokens and
+// statistics must not change.  The pause count is wave-uniform, and every pause is far inside the
+// bounded waits.  In the product library the hook is empty.
+#ifdef DLS_STRESS_DELAYS
+__device__ __forceinline__ void stress_pause(uint32_t epoch, int w, int j, int site) {
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  uint32_t h = epoch * 0x9E3779B1u ^ (uint32_t)w * 0x85EBCA77u ^ (uint32_t)(j + 1) * 0xC2B2AE3Du ^
+               (uint32_t)site * 0x27D4EB2Fu ^ wave * 0x165667B1u;
+  h ^= h >> 15;
+  h *= 0x2C1B3C6Du;
+  h ^= h >> 12;
+  h *= 0x297A2D39u;
+  h ^= h >> 15;
+  const int rounds = (h & 3u) == 0u ? (int)((h >> 8) & 3u) : 0;   // about one publish in five pauses
+  for (int i = 0; i < rounds; ++i) __builtin_amdgcn_s_sleep(127);   // 127 x 64 cycles each
+}
+#define DLS_STRESS(ep, w, j, site) stress_pause((ep), (w), (j), (site))
+#else
+#define DLS_STRESS(ep, w, j, site) ((void)0)
+#endif
+
 __device__ __forceinline__ void stf(float* p, float v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -853,6 +876,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   // written by the lanes of wave `by` (a wave's loads wait for its earlier stores, so the
   // stores go to a wave that loads nothing critical soon after).
   auto publish_stats = [&](int jp, int mtp, int nbp, int by) {
+    DLS_STRESS(epoch, w, jp, 5);
     const int sl = tid - 64 * by;
     if (sl >= 0 && sl < nbp) {
       Partial T = s_part[sl];
@@ -973,6 +997,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         }
         // the stores after all the values: a store ahead of the arithmetic of the next slot
         // would make the wave wait for its completion
+        DLS_STRESS(epoch, w, j, 1);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
           const int pp = wave * npw + k, mt = pp >> 2, slot = 4 * g4 + (pp & 3), bb = mt * 16 + slot;
@@ -1080,6 +1105,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
               g1 += s_red[(k * 4 + 2) * 64 + lane];
               g2 += s_red[(k * 4 + 3) * 64 + lane];
             }
+            DLS_STRESS(epoch, w, j, 2);
             if (n16 < rpg) {
 #pragma unroll
               for (int i = 0; i < 4; ++i) {
@@ -1153,6 +1179,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
           bail();
           return;
         }
+        DLS_STRESS(epoch, w, j, 3);
         if (wave == 0 && n16 < rpg) {
           f32x4_t sm = s_rred[g4 * rpg + n16];
           for (int q = 1; q < 4; ++q) sm += s_rred[(q * 4 + g4) * rpg + n16];
@@ -1540,6 +1567,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
         if (g4 == 0 && n16 < nb) s_wkey[wave * 16 + n16] = k;
       }
       __syncthreads();
+      DLS_STRESS(epoch, w, j, 4);
       if (tid < nb) {
         uint64_t k = s_wkey[tid];
         for (int q = 1; q < 4; ++q) k = key_max(k, s_wkey[q * 16 + tid]);
@@ -1624,6 +1652,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     }
   }
   if (w == 0 && tid == 0) {
+    DLS_STRESS(epoch, w, Bk, 6);
     vm_wait();
     st32(a.hdr, epoch_full + 1u);
   }
