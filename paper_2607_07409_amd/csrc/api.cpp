@@ -454,9 +454,9 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, int l
       pa.keys = (uint64_t*)(ws + pw.off_keys);
       pa.hbuf = (uint64_t*)(ws + pw.off_h);
       pa.h32 = (uint32_t*)(ws + pw.off_h32);
-      // replicas of the wide h hand-off: as many as fit the fixed-size set, at most 8
+      // one copy of the wide h hand-off words: replicas (each GRU workgroup reading its own) cost
+      // more in publish stores on the critical path than they saved in reads
       pa.hrep = 1;
-      while (pa.hrep < 8 && (size_t)4 * pa.hrep * batch * (ch.H > 0 ? ch.H : 1) <= dls::kH32Set) pa.hrep *= 2;
       pa.rbuf = (uint64_t*)(ws + pw.off_rho);
       pa.stats = (uint64_t*)(ws + pw.off_stats);
       hipError_t e = dls::launch_persistent(pa, pl, long_dtype, (hipStream_t)stream);

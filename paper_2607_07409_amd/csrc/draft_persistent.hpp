@@ -47,7 +47,7 @@ constexpr int kInflight = 8;     // hand-off loads a thread issues before checki
                                  // 64-bit word each for narrow batches, 16 bytes for wide ones)
 constexpr int kStageK = 256;     // K chunk of staged hand-off values (16 slots x 256 floats in LDS)
 constexpr int kStatWords = 9;    // tagged words of one published partial
-constexpr int kRhoCopies = 8;    // replicas of the published rank vector (spreads the readers)
+constexpr int kRhoCopies = 1;    // copies of the published rank vector (more copies measured slower: their stores sit on the critical path)
 
 __device__ __forceinline__ uint64_t ld64(const uint64_t* p) {
   return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
