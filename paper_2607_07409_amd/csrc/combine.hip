@@ -16,13 +16,16 @@ namespace dls {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kWideThreads = 1024;
 constexpr int kUnroll = 2;
 
-// l_v for one element (the GPU's float32 reading of the fusion equation)
-template <bool PRIOR>
+// l_v for one element (the GPU's float32 reading of the fusion equation).  The launch resolves
+// the zero-weight cases (a term whose weight is 0 is absent, masked entries included): WLONG
+// means w_long != 0, and PRIOR a prior with beta != 0, so no entry needs a test of its weight.
+template <bool PRIOR, bool WLONG>
 __device__ __forceinline__ float fuse1(float a, float b, float p, float wl, float al, float be) {
-  float f = __builtin_fmaf(al, b, weighted(wl, a));
-  if (PRIOR) f = minus_weighted(f, be, p);
+  float f = __builtin_fmaf(al, b, WLONG ? wl * a : 0.f);
+  if (PRIOR) f = __builtin_fmaf(-be, p, f);
   return f;
 }
 
@@ -33,15 +36,15 @@ __device__ __forceinline__ void top1_push(Partial& p, float x, int idx) {
   p.i1 = up ? idx : p.i1;
 }
 
-template <typename T, bool PRIOR, bool STATS>
+template <typename T, bool PRIOR, bool STATS, bool WLONG>
 __device__ __forceinline__ void fold_scalar(Partial& P, const T* Lr, const T* Sr, const float* prior,
                                             int v, float wl, float al, float be) {
   float a = to_f32(Lr[v]), b = to_f32(Sr[v]);
-  float f = fuse1<PRIOR>(a, b, PRIOR ? prior[v] : 0.f, wl, al, be);
-  if (STATS) {
-    lse_fold<1>(P.L, &a, a);
-    lse_fold<1>(P.S, &b, b);
-    lse_fold<1>(P.F, &f, f);
+  float f = fuse1<PRIOR, WLONG>(a, b, PRIOR ? prior[v] : 0.f, wl, al, be);
+  if (STATS) {   // finite-start states (see k_combine_part)
+    lse_fold_fin<1>(P.L, &a, a);
+    lse_fold_fin<1>(P.S, &b, b);
+    lse_fold_fin<1>(P.F, &f, f);
     top2_push(P, f, v);
   } else {
     top1_push(P, f, v);
@@ -54,13 +57,14 @@ __device__ __forceinline__ int head_elems(const T* p, int V) {
   return h < V ? h : V;
 }
 
-template <typename T, bool PRIOR, bool STATS>
-__global__ __launch_bounds__(kThreads) void k_combine_part(
+template <typename T, bool PRIOR, bool STATS, int NT, bool WLONG>
+__global__ __launch_bounds__(NT) void k_combine_part(
     const T* __restrict__ L, const T* __restrict__ S, const float* __restrict__ prior, int V,
     float wl, float al, float be, Partial* __restrict__ part_out, int32_t* __restrict__ out_token,
     dls_row_stats* __restrict__ out_stats, float* __restrict__ norm_out) {
   constexpr int N = Chunk<T>::N;
-  __shared__ Partial sh[kThreads / 64];
+  constexpr int NU = N * kUnroll;   // entries per thread and iteration
+  __shared__ Partial sh[NT / 64];
   const int row = blockIdx.x, part = blockIdx.y, parts = gridDim.y;
   const T* Lr = L + (size_t)row * V;
   const T* Sr = S + (size_t)row * V;
@@ -71,29 +75,59 @@ __global__ __launch_bounds__(kThreads) void k_combine_part(
   const int t = threadIdx.x;
 
   Partial P = partial_empty();
-  if (part == 0 && t < h0) fold_scalar<T, PRIOR, STATS>(P, Lr, Sr, prior, t, wl, al, be);
+  if (STATS) P.L.m = P.S.m = P.F.m = kFinMin;   // the finite start of the folds below
+  if (part == 0 && t < h0) fold_scalar<T, PRIOR, STATS, WLONG>(P, Lr, Sr, prior, t, wl, al, be);
 
-  for (int c = c0 + t; c < c1; c += kThreads * kUnroll) {
+  for (int c = c0 + t; c < c1; c += NT * kUnroll) {
     uint4 ra[kUnroll], rb[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int cc = c + u * kThreads;
+      const int cc = c + u * NT;
       if (cc < c1) {
         ra[u] = Chunk<T>::raw(Lr + h0 + (size_t)cc * N);
         rb[u] = Chunk<T>::raw(Sr + h0 + (size_t)cc * N);
       }
     }
+    if (STATS && c + (kUnroll - 1) * NT < c1) {
+      // every chunk of the iteration in range: one fold per log-sum-exp, one rescale per NU entries
+      float a[NU], b[NU], f[NU];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int cc = c + u * kThreads;
-      if (cc < c1) {
-        float a[N], b[N], f[N];
-        Chunk<T>::widen(ra[u], a);
-        Chunk<T>::widen(rb[u], b);
-        const int v0 = h0 + cc * N;
+      for (int u = 0; u < kUnroll; ++u) {
+        Chunk<T>::widen(ra[u], a + u * N);
+        Chunk<T>::widen(rb[u], b + u * N);
+        const int v0 = h0 + (c + u * NT) * N;
 #pragma unroll
-        for (int i = 0; i < N; ++i) f[i] = fuse1<PRIOR>(a[i], b[i], PRIOR ? prior[v0 + i] : 0.f, wl, al, be);
-        if (STATS) {
+        for (int i = 0; i < N; ++i)
+          f[u * N + i] = fuse1<PRIOR, WLONG>(a[u * N + i], b[u * N + i], PRIOR ? prior[v0 + i] : 0.f, wl, al, be);
+      }
+      float ma = a[0], mb = b[0], mf = f[0];
+#pragma unroll
+      for (int i = 1; i < NU; ++i) {
+        ma = fmaxf(ma, a[i]);
+        mb = fmaxf(mb, b[i]);
+        mf = fmaxf(mf, f[i]);
+      }
+      lse_fold_fin<NU>(P.L, a, ma);
+      lse_fold_fin<NU>(P.S, b, mb);
+      lse_fold_fin<NU>(P.F, f, mf);
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int v0 = h0 + (c + u * NT) * N;
+#pragma unroll
+        for (int i = 0; i < N; ++i) top2_push(P, f[u * N + i], v0 + i);
+      }
+    } else if (STATS) {
+      // the last, partial iteration: chunk by chunk
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int cc = c + u * NT;
+        if (cc < c1) {
+          float a[N], b[N], f[N];
+          Chunk<T>::widen(ra[u], a);
+          Chunk<T>::widen(rb[u], b);
+          const int v0 = h0 + cc * N;
+#pragma unroll
+          for (int i = 0; i < N; ++i) f[i] = fuse1<PRIOR, WLONG>(a[i], b[i], PRIOR ? prior[v0 + i] : 0.f, wl, al, be);
           float ma = a[0], mb = b[0], mf = f[0];
 #pragma unroll
           for (int i = 1; i < N; ++i) {
@@ -101,21 +135,36 @@ __global__ __launch_bounds__(kThreads) void k_combine_part(
             mb = fmaxf(mb, b[i]);
             mf = fmaxf(mf, f[i]);
           }
-          lse_fold<N>(P.L, a, ma);
-          lse_fold<N>(P.S, b, mb);
-          lse_fold<N>(P.F, f, mf);
+          lse_fold_fin<N>(P.L, a, ma);
+          lse_fold_fin<N>(P.S, b, mb);
+          lse_fold_fin<N>(P.F, f, mf);
 #pragma unroll
           for (int i = 0; i < N; ++i) top2_push(P, f[i], v0 + i);
-        } else {
+        }
+      }
+    } else {
 #pragma unroll
-          for (int i = 0; i < N; ++i) top1_push(P, f[i], v0 + i);
+      for (int u = 0; u < kUnroll; ++u) {
+        const int cc = c + u * NT;
+        if (cc < c1) {
+          float a[N], b[N];
+          Chunk<T>::widen(ra[u], a);
+          Chunk<T>::widen(rb[u], b);
+          const int v0 = h0 + cc * N;
+#pragma unroll
+          for (int i = 0; i < N; ++i) top1_push(P, fuse1<PRIOR, WLONG>(a[i], b[i], PRIOR ? prior[v0 + i] : 0.f, wl, al, be), v0 + i);
         }
       }
     }
   }
-  if (part == parts - 1 && t < V - tail0) fold_scalar<T, PRIOR, STATS>(P, Lr, Sr, prior, tail0 + t, wl, al, be);
+  if (part == parts - 1 && t < V - tail0) fold_scalar<T, PRIOR, STATS, WLONG>(P, Lr, Sr, prior, tail0 + t, wl, al, be);
+  if (STATS) {
+    fin_to_empty(P.L);
+    fin_to_empty(P.S);
+    fin_to_empty(P.F);
+  }
 
-  P = block_merge(P, sh, kThreads / 64);
+  P = block_merge(P, sh, NT / 64);
   if (t == 0) {
     if (parts == 1)
       finalize_row(P, wl, al, false, out_token + row, out_stats ? out_stats + row : nullptr,
@@ -139,7 +188,7 @@ __global__ __launch_bounds__(64) void k_combine_finalize(const Partial* __restri
 }
 
 // c_v = l_v - (w_long * lse_long + alpha * lse_short), recomputing l_v exactly as above
-template <typename T, bool PRIOR>
+template <typename T, bool PRIOR, bool WLONG>
 __global__ __launch_bounds__(kThreads) void k_combine_scores(const T* __restrict__ L, const T* __restrict__ S,
                                                              const float* __restrict__ prior, int V, float wl,
                                                              float al, float be, const float* __restrict__ norm,
@@ -150,19 +199,23 @@ __global__ __launch_bounds__(kThreads) void k_combine_scores(const T* __restrict
   float* Cr = scores + (size_t)row * V;
   const float nr = norm[row];
   for (int v = blockIdx.y * kThreads + threadIdx.x; v < V; v += gridDim.y * kThreads)
-    Cr[v] = fuse1<PRIOR>(to_f32(Lr[v]), to_f32(Sr[v]), PRIOR ? prior[v] : 0.f, wl, al, be) - nr;
+    Cr[v] = fuse1<PRIOR, WLONG>(to_f32(Lr[v]), to_f32(Sr[v]), PRIOR ? prior[v] : 0.f, wl, al, be) - nr;
 }
 
-template <typename T, bool PRIOR>
+template <typename T, bool PRIOR, bool WLONG>
 hipError_t launch_combine_t(const CombineArgs& a, hipStream_t st) {
   const int parts = a.parts;
   dim3 grid((unsigned)a.rows, parts);
   // the normaliser feeds only the statistics and the score rows
   const bool stats = a.out_stats != nullptr || a.out_scores != nullptr;
   float* norm = stats ? a.norm : nullptr;
-  auto kern = stats ? k_combine_part<T, PRIOR, true> : k_combine_part<T, PRIOR, false>;
-  kern<<<grid, kThreads, 0, st>>>((const T*)a.long_logits, (const T*)a.short_logits, a.prior, a.V, a.wl, a.al,
-                                  a.be, a.partials, a.out_token, a.out_stats, norm);
+  const bool wide = combine_wide(a.rows, a.V);
+  auto kern = wide ? (stats ? k_combine_part<T, PRIOR, true, kWideThreads, WLONG>
+                             : k_combine_part<T, PRIOR, false, kWideThreads, WLONG>)
+                   : (stats ? k_combine_part<T, PRIOR, true, kThreads, WLONG> : k_combine_part<T, PRIOR, false, kThreads, WLONG>);
+  kern<<<grid, wide ? kWideThreads : kThreads, 0, st>>>((const T*)a.long_logits, (const T*)a.short_logits, a.prior,
+                                                        a.V, a.wl, a.al, a.be, a.partials, a.out_token, a.out_stats,
+                                                        norm);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (parts > 1) {
@@ -172,7 +225,7 @@ hipError_t launch_combine_t(const CombineArgs& a, hipStream_t st) {
   }
   if (a.out_scores) {
     dim3 g2((unsigned)a.rows, (unsigned)std::min<int64_t>((a.V + kThreads - 1) / kThreads, 64));
-    k_combine_scores<T, PRIOR><<<g2, kThreads, 0, st>>>((const T*)a.long_logits, (const T*)a.short_logits,
+    k_combine_scores<T, PRIOR, WLONG><<<g2, kThreads, 0, st>>>((const T*)a.long_logits, (const T*)a.short_logits,
                                                         a.prior, a.V, a.wl, a.al, a.be, a.norm, a.out_scores);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
@@ -181,7 +234,12 @@ hipError_t launch_combine_t(const CombineArgs& a, hipStream_t st) {
 
 }  // namespace
 
+// 256 to 1023 rows: one row per workgroup of 1024 threads (about one per CU, as many bytes in
+// flight as four workgroups of 256 threads), so that no merge launch follows
+bool combine_wide(int64_t rows, int32_t V) { return rows >= 256 && rows < 1024 && V >= 4 * kWideThreads; }
+
 int combine_parts(int64_t rows, int32_t V) {
+  if (combine_wide(rows, V)) return 1;
   // enough workgroups to cover the chip when rows are few (four per CU); each range >= 2048
   // elements.  From 1024 rows on every row is one workgroup and no merge launch follows.
   const int64_t target = 1024;
@@ -192,10 +250,14 @@ int combine_parts(int64_t rows, int32_t V) {
 }
 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t st) {
-  const bool pr = a.prior != nullptr;
+  // a zero weight removes its term, masked entries included: a prior with beta = 0 is no prior
+  const bool pr = a.prior != nullptr && a.be != 0.f;
+  const bool wlong = a.wl != 0.f;
   if (a.dtype == DLS_BF16)
-    return pr ? launch_combine_t<bf16_t, true>(a, st) : launch_combine_t<bf16_t, false>(a, st);
-  return pr ? launch_combine_t<float, true>(a, st) : launch_combine_t<float, false>(a, st);
+    return pr ? (wlong ? launch_combine_t<bf16_t, true, true>(a, st) : launch_combine_t<bf16_t, true, false>(a, st))
+              : (wlong ? launch_combine_t<bf16_t, false, true>(a, st) : launch_combine_t<bf16_t, false, false>(a, st));
+  return pr ? (wlong ? launch_combine_t<float, true, true>(a, st) : launch_combine_t<float, true, false>(a, st))
+            : (wlong ? launch_combine_t<float, false, true>(a, st) : launch_combine_t<float, false, false>(a, st));
 }
 
 }  // namespace dls

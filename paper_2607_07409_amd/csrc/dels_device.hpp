@@ -91,6 +91,23 @@ __device__ __forceinline__ void lse_fold(Lse& a, const float* x, float cm) {
   a.s = acc;
 }
 
+// Running log-sum-exps that start from a finite floor (kFinMin instead of -inf) need no test of
+// their values: x = -inf adds exp2(-inf) = 0 and never becomes the maximum.  Such a state is
+// empty while s == 0; fin_to_empty restores the -inf form before states are merged.
+constexpr float kFinMin = -2.0e38f;   // kFinMin * log2(e) is still finite
+__device__ __forceinline__ void fin_to_empty(Lse& a) { a.m = a.s > 0.f ? a.m : -INFINITY; }
+// n values whose maximum is cm into a finite-start state: one rescale, one exponential per value
+template <int n>
+__device__ __forceinline__ void lse_fold_fin(Lse& a, const float* x, float cm) {
+  const float mn = fmaxf(a.m, cm);
+  const float ml = mn * kLog2e;
+  float acc = a.s * fast_exp2((a.m - mn) * kLog2e);   // exactly 1 while the maximum stays
+#pragma unroll
+  for (int i = 0; i < n; ++i) acc += fast_exp2(__builtin_fmaf(x[i], kLog2e, -ml));
+  a.m = mn;
+  a.s = acc;
+}
+
 __device__ __forceinline__ Lse lse_merge(Lse a, Lse b) {
   const float mn = fmaxf(a.m, b.m);
   if (mn == -INFINITY) return lse_empty();

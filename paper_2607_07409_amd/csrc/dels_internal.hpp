@@ -50,6 +50,7 @@ struct CombineArgs {
   float* out_scores;
 };
 int combine_parts(int64_t rows, int32_t V);
+bool combine_wide(int64_t rows, int32_t V);   // one 1024-thread workgroup per row
 hipError_t launch_combine(const CombineArgs& a, hipStream_t st);
 
 // adaptive fusion: the measure and gate of dls_adaptive in the form the kernels use

@@ -232,7 +232,6 @@ __device__ __forceinline__ void lse_push(Lse& a, float x) {
 // lse_push for a running maximum that starts finite (kFinMin instead of -inf): no test of the
 // value is needed, since x = -inf gives d = -inf, a zero term and no new maximum.  Such a
 // state is empty while s == 0 (a push sets s >= 1); fin_to_empty restores the -inf form.
-constexpr float kFinMin = -2.0e38f;   // kFinMin * log2(e) is still finite
 __device__ __forceinline__ void lse_push_fin(Lse& a, float x) {
   const float d = x - a.m;
   const float e = fast_exp2(-fabsf(d) * kLog2e);
@@ -240,7 +239,6 @@ __device__ __forceinline__ void lse_push_fin(Lse& a, float x) {
   a.s = up ? __builtin_fmaf(a.s, e, 1.0f) : a.s + e;
   a.m = up ? x : a.m;
 }
-__device__ __forceinline__ void fin_to_empty(Lse& a) { a.m = a.s > 0.f ? a.m : -INFINITY; }
 // four values at once into a finite-start state: one new maximum, one rescale of the sum and
 // one exponential per value (values of -inf add nothing)
 __device__ __forceinline__ void lse_push4_fin(Lse& a, const float (&x)[4]) {

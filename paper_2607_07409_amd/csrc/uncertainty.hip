@@ -4,7 +4,8 @@
 // Per row of V logits x (finite or -inf) the kernel keeps, over the finite entries,
 //   m = the largest value, s = sum exp(x - m), t = sum exp(x - m) (x - m),
 // so that log-sum-exp = m + log s, max p = 1 / s and H(p) = log s - t / s (t <= 0, s >= 1).
-// A 16-byte chunk is folded with one rescale to its maximum and one exponential per entry.
+// The chunks of an iteration are folded with one rescale to their maximum and one exponential
+// per entry.
 // A row is split into `parts` contiguous ranges, one workgroup each, when rows are too few
 // to cover the chip; a second kernel then merges the per-range triples of each row in a fixed
 // order.  The gate g = clamp((u - h_lo) / (h_hi - h_lo), 0, 1) of the chosen measure u is
@@ -44,7 +45,7 @@ __device__ __forceinline__ void ent_fold(Ent& a, const float* x, float cm) {
     const float d = x[i] - a.m;                    // <= 0; -inf for a masked entry
     const float e = fast_exp2(d * kLog2e);          // exp2(-inf) = 0
     a.s += e;
-    a.t = __builtin_fmaf(e, x[i] == -INFINITY ? 0.f : d, a.t);
+    a.t = __builtin_fmaf(e, fmaxf(d, kDMin), a.t);  // a masked entry: 0 * kDMin = 0
   }
 }
 
@@ -116,16 +117,26 @@ __global__ __launch_bounds__(kThreads) void k_unc_part(const T* __restrict__ L, 
       const int cc = c + u * kThreads;
       if (cc < c1) raw[u] = Chunk<T>::raw(Lr + h0 + (size_t)cc * N);
     }
+    if (c + (kUnroll - 1) * kThreads < c1) {   // every chunk in range: one rescale for all of them
+      float x[N * kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int cc = c + u * kThreads;
-      if (cc < c1) {
-        float x[N];
-        Chunk<T>::widen(raw[u], x);
-        float cm = x[0];
+      for (int u = 0; u < kUnroll; ++u) Chunk<T>::widen(raw[u], x + u * N);
+      float cm = x[0];
 #pragma unroll
-        for (int i = 1; i < N; ++i) cm = fmaxf(cm, x[i]);
-        ent_fold<N>(a, x, cm);
+      for (int i = 1; i < N * kUnroll; ++i) cm = fmaxf(cm, x[i]);
+      ent_fold<N * kUnroll>(a, x, cm);
+    } else {
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int cc = c + u * kThreads;
+        if (cc < c1) {
+          float x[N];
+          Chunk<T>::widen(raw[u], x);
+          float cm = x[0];
+#pragma unroll
+          for (int i = 1; i < N; ++i) cm = fmaxf(cm, x[i]);
+          ent_fold<N>(a, x, cm);
+        }
       }
     }
   }

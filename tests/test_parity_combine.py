@@ -51,6 +51,8 @@ def _check(long_h, short_h, prior, wl, al, be, row_ids=None, want_scores=False):
     (3, 1, "bf16", 4),            # a single-token vocabulary
     (6, 3, "f32", 5),
     (33, 8191, "bf16", 6),
+    (300, 5003, "bf16", 7),       # one 1024-thread workgroup per row (256 to 1023 rows)
+    (257, 4099, "f32", 8),
 ])
 def test_combine_shapes(rows, V, dtype, seed):
     L = W.make_logit_rows(rows, V, dtype, seed, "onehot", 3.0, purpose=20)
