@@ -295,6 +295,8 @@ def main():
     ap.add_argument("--cooperative", action="store_true",
                     help="launch the persistent kernel cooperatively in the timed step (default: an ordinary "
                          "dispatch, DLS_EXCLUSIVE_DEVICE, since this process owns the device)")
+    ap.add_argument("--no-cooperative-comparison", action="store_true",
+                    help="leave out the timing of the other launch mode (a profiled run without cooperative launches)")
     ap.add_argument("--oracle-leg", help=argparse.SUPPRESS)
     ap.add_argument("--oracle-parity", action="store_true", help=argparse.SUPPRESS)
     args = ap.parse_args()
@@ -423,11 +425,12 @@ def main():
     extras = {}
     if not args.no_extras:
         # the other launch mode (cooperative vs ordinary dispatch)
-        for _ in range(3):
-            draft(exclusive=not EXC)
-        other = per_call_us(lambda i: draft(exclusive=not EXC), 30, torch)
-        extras["draft_block_" + ("cooperative" if EXC else "ordinary") + "_launch_us"] = dist(other)
-        log(f"draft block with {'a cooperative' if EXC else 'an ordinary'} launch: {pct(other, 50):.1f} us")
+        if not args.no_cooperative_comparison:
+            for _ in range(3):
+                draft(exclusive=not EXC)
+            other = per_call_us(lambda i: draft(exclusive=not EXC), 30, torch)
+            extras["draft_block_" + ("cooperative" if EXC else "ordinary") + "_launch_us"] = dist(other)
+            log(f"draft block with {'a cooperative' if EXC else 'an ordinary'} launch: {pct(other, 50):.1f} us")
         # the same block through the per-position launches (no prepared head)
         base_head = B.LocalHead(head.emb, head.w_ih, head.w_hh, head.w_rank, head.w_vocab)
         ws2 = B.draft_workspace(base_head, wl.batch, wl.B, dev)
