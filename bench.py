@@ -534,6 +534,8 @@ def main():
         torch.cuda.empty_cache()
         cases = [(n, W.WORKLOADS[n]) for n in W.WORKLOAD_ORDER]
         cases.append(("qwen3-8b-b1-block7", W.WORKLOADS["qwen3-8b-b1"].with_(B=7)))
+        # the ABI's largest batch: four persistent launches of 64 sequences on one workspace
+        cases.append(("b256-d5120", W.WORKLOADS["b64-d5120"].with_(batch=256)))
         for name, w_ in cases:
             wls[name] = time_workload(B, W, w_, dev, torch)
             torch.cuda.empty_cache()

@@ -183,10 +183,13 @@ dls_status dls_combine_logits(const void *long_logits, const void *short_logits,
 /* ---------------------------------------------------------------------------------
  * One draft block per sequence (Algorithm 1, the decoding loop).
  * Two implementations share this entry point.  With head->prepared set and a supported
- * shape (bf16 head, batch <= 64, H/16 <= number of CUs, r divisible by H/16 with at most
- * 16 rank rows per group, and the per-CU share of W_vocab fitting in AGPRs + LDS) one
- * persistent kernel keeps the head weights on chip for the whole block; otherwise each
- * position is a sequence of kernel launches.  dls_draft_block_path tells which is used.
+ * shape (bf16 head, H/16 <= number of CUs, r divisible by H/16 with at most 16 rank rows
+ * per group, and the per-CU share of W_vocab fitting in AGPRs + LDS) one persistent kernel
+ * keeps the head weights on chip for the whole block, for at most 64 sequences per launch
+ * (a larger batch runs as consecutive launches of 64 on the same workspace and stream;
+ * sampling keys its noise by each sequence's index in the whole call, so the split does not
+ * change a draw); otherwise each position is a sequence of kernel launches.
+ * dls_draft_block_path tells which is used.
  * The workspace must be zero-filled before its first use; the library keeps it
  * consistent afterwards.  A persistent call that fails sets the workspace's error word
  * (read it with dls_draft_block_error; the call itself has returned DLS_OK long before,

@@ -266,7 +266,8 @@ size_t dls_draft_block_workspace_size(const dls_local_head* head, int32_t batch,
   const dls_local_head ch = canon(*head);
   // persistent region first (its header must start zero-filled), per-launch region after it,
   // then the partials of the adaptive-fusion pre-pass
-  return dls::persist_workspace(ch, batch, B).total + dls::draft_layout(ch, batch, B).total +
+  return dls::persist_workspace(ch, std::min<int32_t>(batch, dls::kMaxBatch), B).total +
+         dls::draft_layout(ch, batch, B).total +
          align256(dls::uncertainty_workspace_bytes((int64_t)batch * B, ch.V));
 }
 
@@ -352,6 +353,7 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, int l
   smp.temp = T > 0.f ? T : 1.f;
   smp.seed_lo = (uint32_t)sampling.seed;
   smp.seed_hi = (uint32_t)(sampling.seed >> 32);
+  smp.b0 = 0;
   const bool literal = (fusion.flags & DLS_FIRST_ROW_LONG_ONLY) != 0;
   if (!long_logits || !out_tokens || (!last_token && !literal))
     return fail(DLS_ERR_ARG, "required pointer is NULL");
@@ -388,7 +390,8 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, int l
   }
 
   const dls_local_head ch = canon(*head);
-  const dls::PersistWorkspace pw = dls::persist_workspace(ch, batch, B);
+  // the persistent kernel runs at most kMaxBatch sequences per launch (below)
+  const dls::PersistWorkspace pw = dls::persist_workspace(ch, std::min<int32_t>(batch, dls::kMaxBatch), B);
   // adaptive fusion: the gates of all batch * B rows first, stream-ordered before the draft
   if (rule) {
     dls::UncArgs ua;
@@ -403,8 +406,15 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, int l
     if (e != hipSuccess) return hip_fail(e, "draft_block_adaptive uncertainty launch");
   }
   if (head->prepared) {
-    const dls::PersistPlan pl = dls::persist_plan(ch, batch, B, long_dtype, prior != nullptr, persist_groups(cus));
-    if (pl.ok) {
+    // A call of more than kMaxBatch sequences runs as consecutive launches of at most kMaxBatch
+    // sequences each, on the same workspace and stream; every launch's plan is checked first.
+    const int nfull = std::min<int32_t>(batch, dls::kMaxBatch);
+    const int nlast = batch - (batch - 1) / dls::kMaxBatch * dls::kMaxBatch;   // the last launch's sequences
+    const dls::PersistPlan pl = dls::persist_plan(ch, nfull, B, long_dtype, prior != nullptr, persist_groups(cus));
+    const dls::PersistPlan pl_last = nlast == nfull ? pl
+                                                    : dls::persist_plan(ch, nlast, B, long_dtype, prior != nullptr,
+                                                                        persist_groups(cus));
+    if (pl.ok && pl_last.ok) {
       const dls::PreparedLayout PL = dls::prepared_layout(ch);
       const char* pp = (const char*)head->prepared;
       char* ws = (char*)workspace;
@@ -427,17 +437,7 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, int l
       pa.V = head->V;
       pa.H = ch.H;
       pa.r = head->r;
-      pa.NT = pl.NT;
-      pa.NG = pl.NG;
-      pa.rpg = pl.rpg;
-      pa.cap_a = pl.cap_a;
-      pa.gcap = pl.gcap;
-      pa.rows_max = pl.rows_max;
-      pa.lds_region_a = pl.lds_region_a;
-      pa.L = long_logits;
-      pa.last = last_token;
       pa.prior = prior;
-      pa.batch = batch;
       pa.B = B;
       pa.wl = fusion.w_long;
       for (int j = 0; j < 64; ++j) {
@@ -445,22 +445,39 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, int l
         pa.be_j[j] = !prior ? 0.f : (j < B && betas ? betas[j] : fusion.beta);
       }
       pa.literal = (fusion.flags & DLS_FIRST_ROW_LONG_ONLY) ? 1 : 0;
-      pa.smp = smp;
-      pa.unc = out_unc;
       pa.ordinary_launch = (fusion.flags & DLS_EXCLUSIVE_DEVICE) ? 1 : 0;
-      pa.out_tokens = out_tokens;
-      pa.out_stats = out_stats;
       pa.hdr = (uint32_t*)ws;
-      pa.keys = (uint64_t*)(ws + pw.off_keys);
-      pa.hbuf = (uint64_t*)(ws + pw.off_h);
-      pa.h32 = (uint32_t*)(ws + pw.off_h32);
       // one copy of the wide h hand-off words: replicas (each GRU workgroup reading its own) cost
       // more in publish stores on the critical path than they saved in reads
       pa.hrep = 1;
-      pa.rbuf = (uint64_t*)(ws + pw.off_rho);
-      pa.stats = (uint64_t*)(ws + pw.off_stats);
-      hipError_t e = dls::launch_persistent(pa, pl, long_dtype, (hipStream_t)stream);
-      if (e != hipSuccess) return hip_fail(e, "draft_block persistent launch");
+      const size_t lsz = long_dtype == DLS_BF16 ? 2 : 4;
+      for (int b0 = 0; b0 < batch; b0 += dls::kMaxBatch) {
+        const int nb = std::min<int32_t>(dls::kMaxBatch, batch - b0);
+        const dls::PersistPlan& plc = nb == nfull ? pl : pl_last;
+        const dls::PersistWorkspace pwc = dls::persist_workspace(ch, nb, B);
+        pa.NT = plc.NT;
+        pa.NG = plc.NG;
+        pa.rpg = plc.rpg;
+        pa.cap_a = plc.cap_a;
+        pa.gcap = plc.gcap;
+        pa.rows_max = plc.rows_max;
+        pa.lds_region_a = plc.lds_region_a;
+        pa.batch = nb;
+        pa.L = (const char*)long_logits + (size_t)b0 * B * ch.V * lsz;
+        pa.last = last_token ? last_token + b0 : nullptr;
+        pa.smp = smp;
+        pa.smp.b0 = (uint32_t)b0;   // the noise of a sequence is keyed by its index in the call
+        pa.unc = out_unc ? out_unc + (size_t)b0 * B : nullptr;
+        pa.out_tokens = out_tokens + (size_t)b0 * B;
+        pa.out_stats = out_stats ? out_stats + (size_t)b0 * B : nullptr;
+        pa.keys = (uint64_t*)(ws + pwc.off_keys);
+        pa.hbuf = (uint64_t*)(ws + pwc.off_h);
+        pa.h32 = (uint32_t*)(ws + pwc.off_h32);
+        pa.rbuf = (uint64_t*)(ws + pwc.off_rho);
+        pa.stats = (uint64_t*)(ws + pwc.off_stats);
+        hipError_t e = dls::launch_persistent(pa, plc, long_dtype, (hipStream_t)stream);
+        if (e != hipSuccess) return hip_fail(e, "draft_block persistent launch");
+      }
       return DLS_OK;
     }
   }
@@ -561,15 +578,19 @@ dls_status dls_draft_block_error(const void* workspace, size_t ws_bytes, int32_t
 int dls_draft_block_path(const dls_local_head* head, int32_t batch, int32_t B, dls_dtype long_dtype,
                          int has_prior) {
   clear_error();
-  if (check_head(head) != DLS_OK || check_prepared_size(head) != DLS_OK || !valid_dtype(enum_bits(long_dtype)) || batch < 1 ||
-      batch > 256 || B < 1 || B > 64)
+  if (check_head(head) != DLS_OK || check_prepared_size(head) != DLS_OK || !valid_dtype(enum_bits(long_dtype)) ||
+      batch < 1 || batch > 256 || B < 1 || B > 64)
     return -1;
   if (!head->prepared) return 0;
   int cus = 0;
   if (check_device(&cus) != DLS_OK) return -1;
-  const dls::PersistPlan pl = dls::persist_plan(canon(*head), batch, B, long_dtype, has_prior != 0, persist_groups(cus));
-  if (!pl.ok) fail(DLS_OK, "%s", pl.why);
-  return pl.ok ? 1 : 0;
+  const int nfull = std::min<int32_t>(batch, dls::kMaxBatch);
+  const int nlast = batch - (batch - 1) / dls::kMaxBatch * dls::kMaxBatch;
+  const dls::PersistPlan pl = dls::persist_plan(canon(*head), nfull, B, long_dtype, has_prior != 0, persist_groups(cus));
+  const dls::PersistPlan pl_last = dls::persist_plan(canon(*head), nlast, B, long_dtype, has_prior != 0,
+                                                     persist_groups(cus));
+  if (!pl.ok || !pl_last.ok) fail(DLS_OK, "%s", pl.ok ? pl_last.why : pl.why);
+  return pl.ok && pl_last.ok ? 1 : 0;
 }
 
 dls_status dls_unigram_log_prior(const int32_t* tokens, int64_t n, int32_t V, float smoothing, uint64_t* out_counts,

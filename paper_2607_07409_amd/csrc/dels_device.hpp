@@ -242,6 +242,7 @@ struct Sampler {
   float inv_temp;   // 1 / T; 0 decodes greedily
   float temp;       // T (1 when greedy)
   uint32_t seed_lo, seed_hi;
+  uint32_t b0;      // index of the launch's first sequence in the call (a call split into launches)
 };
 
 __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
@@ -275,7 +276,7 @@ __device__ __forceinline__ float gumbel_from_word(uint32_t x) {
 }
 
 __device__ __forceinline__ uint4 philox_row(const Sampler& sm, int b, int j, int v) {
-  return philox4x32_10(make_uint4((uint32_t)v >> 2, (uint32_t)j, (uint32_t)b, 0u), sm.seed_lo, sm.seed_hi);
+  return philox4x32_10(make_uint4((uint32_t)v >> 2, (uint32_t)j, sm.b0 + (uint32_t)b, 0u), sm.seed_lo, sm.seed_hi);
 }
 
 __device__ __forceinline__ float gumbel_at(const Sampler& sm, int b, int j, int v) {

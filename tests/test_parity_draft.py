@@ -209,6 +209,39 @@ def test_persistent_extreme_block_sizes(shape):
     _check(p, 0.6, 0.4, with_prior=True, literal=True, prepared=True, sequences=seqs[:1])
 
 
+@pytest.mark.parametrize("batch", [65, 256])
+def test_batches_split_into_launches(batch):
+    """Above 64 sequences (up to the ABI's maximum of 256) a prepared head runs consecutive
+    persistent launches of at most 64 sequences on one workspace; the first and last sequence of
+    every launch are compared, greedy and with the prior and the literal first row."""
+    p = _problem("qwen3-8b-b16", "stress", dtype="bf16", V=2053, d=64, H=128, r=128, Bk=3, batch=batch)
+    seqs = sorted({s for b0 in range(0, batch, 64) for s in (b0, min(b0 + 63, batch - 1))})
+    tok, st = _draft(p, 0.6, prepared=True, expect_path=1)
+    check_draft(tok, st, p["oracle"], p["long_h"], p["last"], None, 1.0, 0.6, 0.0, sequences=seqs)
+    tok, st = _draft(p, 0.6, 0.4, with_prior=True, literal=True, prepared=True, expect_path=1)
+    check_draft(tok, st, p["oracle"], p["long_h"], p["last"], p["prior"], 1.0, 0.6, 0.4, True, seqs)
+
+
+def test_split_launches_sample_by_sequence_index():
+    """Sampling keys the noise by the sequence's index in the whole call: at batch 80 (launches of
+    64 and 16 sequences) the draws of sequences 63, 64 and 79 are the oracle's for that index, and
+    a sequence drafts the same tokens whether the call is split or not."""
+    p = _problem("qwen3-8b-b16", "stress", dtype="bf16", V=2053, d=64, H=128, r=128, Bk=4, batch=80)
+    head = _head(p, True)
+    lt = B.as_tensor(p["long_h"])
+    last = torch.from_numpy(p["last"]).cuda()
+    tok, st = B.draft_block(head, lt, last, None, 1.0, 0.6, 0.0, temperature=1.0, seed=99)
+    torch.cuda.synchronize()
+    tok, st = tok.cpu().numpy(), st.cpu().numpy()
+    check_draft(tok, st, p["oracle"], p["long_h"], p["last"], None, 1.0, 0.6, 0.0,
+                sequences=[0, 63, 64, 79], temperature=1.0, seed=99)
+    # the unsplit per-position launches on the same call draw the same noise
+    tok2, _ = B.draft_block(p["head"], lt, last, None, 1.0, 0.6, 0.0, temperature=1.0, seed=99)
+    torch.cuda.synchronize()
+    same = (tok2.cpu().numpy() == tok).all(axis=1)
+    assert same.mean() > 0.9, same.mean()   # sequences may part at a near-tie of the two paths
+
+
 @pytest.mark.parametrize("shape", [0, 3])
 def test_persistent_small_prior(shape):
     p = _problem("qwen3-8b-b16", "stress", dtype="bf16", **SMALL[shape])
