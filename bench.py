@@ -2,14 +2,17 @@
 """Benchmark of the DeLS-Spec block-drafting hot path on one MI355X.
 
 A step is one pass of the whole path over one batch: dls_draft_block (local head, fusion and
-greedy argmax at every draft position) followed by dls_accept_len.  The default workload is the
-largest single-GPU drafting configuration: batch 64, block B = 16, V = 151,936, embedding width
-5120, GRU hidden 1024, rank 256, bf16 (Zipf-biased long logits).  Inputs are seeded synthetic
-tensors already resident in HBM.  Prints one JSON line: the drafted-token throughput of the step,
-the roofline of the dominant kernel (the persistent drafting kernel), warm and cold per-call
-timing distributions, the standalone fused combine at the two serving shapes, every drafting
-workload, and the CPU oracle timed on the host in fresh subprocesses (1 thread and all threads),
-which also checks the GPU draft of the timed workload element by element (the `parity` object).
+greedy argmax at every draft position, with row statistics) followed by dls_accept_len.  The
+default workload is the largest single-GPU drafting configuration: batch 64, block B = 16,
+V = 151,936, embedding width 5120, GRU hidden 1024, rank 256, bf16 (Zipf-biased long logits).
+Inputs are seeded synthetic tensors already resident in HBM.  Prints one JSON line: the
+drafted-token throughput of the step, the roofline of the dominant kernel (the persistent drafting
+kernel) with warm and cold per-call timing distributions, and beside them the other launch mode,
+the block without statistics, the per-position launches, sampling at T = 1, adaptive fusion and
+its pre-pass, the Markov head, prior estimation, the standalone fused combine at the two serving
+shapes and every drafting workload; then the CPU oracle timed on the host in fresh subprocesses
+(all threads, then 1 thread), which also checks the GPU draft of the timed workload element by
+element (the `parity` object).
 """
 import argparse
 import hashlib
@@ -431,6 +434,12 @@ def main():
             other = per_call_us(lambda i: draft(exclusive=not EXC), 30, torch)
             extras["draft_block_" + ("cooperative" if EXC else "ordinary") + "_launch_us"] = dist(other)
             log(f"draft block with {'a cooperative' if EXC else 'an ordinary'} launch: {pct(other, 50):.1f} us")
+        # the same block without row statistics (Algorithm 1 needs only the tokens): the kernel
+        # then skips the statistics reduction and publish of every M tile
+        tonly = per_call_us(lambda i: B.draft_block(head, L, last_t, None, 1.0, args.alpha, 0.0, out=(tok, None),
+                                                    workspace=ws, exclusive_device=EXC), 30, torch)
+        extras["draft_block_tokens_only_us"] = dist(tonly)
+        log(f"draft block without row statistics: {pct(tonly, 50):.1f} us")
         # the same block through the per-position launches (no prepared head)
         base_head = B.LocalHead(head.emb, head.w_ih, head.w_hh, head.w_rank, head.w_vocab)
         ws2 = B.draft_workspace(base_head, wl.batch, wl.B, dev)
