@@ -232,3 +232,18 @@ def test_zero_gate_decodes_the_long_logits(kind, prepared):
                               prior=W.make_zipf_log_prior(wl.V, wl.seed))
     assert np.all(unc[..., 3] == 0.0)
     assert np.array_equal(tok, np.argmax(np.asarray(long_h, np.float32), axis=2))
+
+
+def test_adaptive_split_launches():
+    """80 sequences run as persistent launches of 64 and 16: each launch reads the gates of its own
+    rows; the first and last sequence of both launches are compared with the oracle's gated draft."""
+    wl = W.WORKLOADS["qwen3-8b-b16"].with_(batch=80, V=2053, d=64, H=128, r=128, B=4, seed=80)
+    hw = W.make_head(wl, "stress")
+    head, oh = B.LocalHead.from_weights(hw).prepare(), O.RnnHead.from_weights(hw)
+    long_h = W.make_long_logits(wl)
+    u = [O.uncertainty(np.asarray(r, np.float64), O.UNC_ENTROPY) for r in np.asarray(long_h).reshape(-1, wl.V)[:60]]
+    lo, hi = float(np.percentile(u, 25)), float(np.percentile(u, 75))
+    tok, st, unc, long_h, last = _run(head, wl, O.UNC_ENTROPY, lo, hi, long_h=long_h)
+    g = _gates(long_h, O.UNC_ENTROPY, lo, hi)
+    assert np.max(np.abs(unc[..., 3] - g)) <= 1e-5 / (hi - lo) + 1e-6
+    check_draft(tok, st, oh, long_h, last, None, 1.0, 0.6, 0.3, sequences=[0, 63, 64, 79], gates=g)

@@ -90,6 +90,7 @@ CASES = [
     dict(V=W.QWEN3_VOCAB, r=256, batch=16, Bk=16, seed=72),
     dict(V=5003, r=128, batch=37, Bk=5, seed=73),
     dict(V=7001, r=256, batch=2, Bk=9, seed=74),
+    dict(V=5003, r=128, batch=100, Bk=4, seed=75),        # prepared: launches of 64 and 36 sequences
 ]
 
 
