@@ -475,6 +475,7 @@ dls_status draft_impl(const dls_local_head* head, const void* long_logits, int l
         pa.h32 = (uint32_t*)(ws + pwc.off_h32);
         pa.rbuf = (uint64_t*)(ws + pwc.off_rho);
         pa.stats = (uint64_t*)(ws + pwc.off_stats);
+        pa.tokw = (uint64_t*)(ws + pwc.off_tokw);
         hipError_t e = dls::launch_persistent(pa, plc, long_dtype, (hipStream_t)stream);
         if (e != hipSuccess) return hip_fail(e, "draft_block persistent launch");
       }

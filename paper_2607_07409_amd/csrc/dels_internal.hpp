@@ -168,6 +168,7 @@ struct PersistArgs {
   int hrep;                  // replicas of the wide h words (a power of two, 2 hrep batch H <= kH32Set)
   uint64_t* rbuf;            // [replicas][2 parities][batch][r]
   uint64_t* stats;           // [B][batch][G][8] tagged LSE partials
+  uint64_t* tokw;            // merged tokens of wide batches: [2 parities][kMaxBatch] tagged words
 };
 struct PersistPlan {
   bool ok;
@@ -176,7 +177,7 @@ struct PersistPlan {
   size_t lds_region_a, lds;
 };
 struct PersistWorkspace {
-  size_t off_keys, off_h, off_h32, off_rho, off_stats, total;
+  size_t off_keys, off_h, off_h32, off_rho, off_tokw, off_stats, total;
 };
 __host__ __device__ inline void persist_tile_range(int w, int G, int NG, int NT, int cap_a, int gcap, int* t0,
                                                    int* n);

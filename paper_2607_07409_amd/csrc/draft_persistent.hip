@@ -97,6 +97,8 @@ PersistWorkspace persist_workspace(const dls_local_head& h, int32_t batch, int32
   o += (size_t)2 * batch * h.H * 8;
   L.off_rho = o;
   o += (size_t)kRhoCopies * 2 * batch * h.r * 8;
+  L.off_tokw = o;
+  o += (size_t)2 * kMaxBatch * 8;
   L.off_stats = o;
   o += (size_t)B * batch * kMaxG * kStatWords * 8;
   L.total = (o + 255) & ~(size_t)255;

@@ -869,6 +869,54 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     return true;
   };
 
+  // Batches of several M tiles delegate the merge: workgroup NG + b (the first non-GRU
+  // workgroups, which wait for rho anyway) merges the keys of sequence b alone and publishes its
+  // token as one tagged word; the workgroups that need the tokens (the GRU workgroups, or every
+  // workgroup of the Markov head) read batch words instead of batch x G keys (128 KB at batch
+  // 64), at the price of one more hand-off.  With one M tile the keys are few and the merging
+  // workgroups would be the last to finish the position, so every reader merges for itself.
+  // Needs G - NG >= batch.
+  const bool delegate = !NARROW && mtiles > 1 && G - a.NG >= batch;
+  const int merge_seq = delegate && w >= a.NG && w - a.NG < batch ? w - a.NG : -1;   // this workgroup's sequence
+  auto merge_one = [&](int jm, int b) -> bool {
+    const uint32_t tag8 = (uint32_t)(jm + 1);
+    const uint64_t* kp = a.keys + (size_t)set * 2 * kstride + (size_t)(jm & 1) * kstride + (size_t)b * Gp;
+    uint64_t k = 0ull;
+    bool ok = true;
+    if (tid < G) {
+      k = ld64(kp + tid);
+      if ((uint32_t)(k & 0xffu) != tag8) ok = wait_key(kp + tid, tag8, err, k);
+    }
+    k = wave_key_max(k);
+    if ((tid & 63) == 0) s_wkey[tid >> 6] = k;
+    if (fail_barrier(!ok, s_fail)) return false;
+    if (tid == 0) {
+      uint64_t m = s_wkey[0];
+      for (int q = 1; q < 4; ++q) m = key_max(m, s_wkey[q]);
+      DLS_STRESS(epoch, w, jm, 7);
+      st64(a.tokw + (size_t)(jm & 1) * kMaxBatch + b,
+           ((uint64_t)((epoch << 8) | tag8) << 32) | (uint32_t)key_index(m, V));
+    }
+    __syncthreads();   // s_wkey read
+    return true;
+  };
+  // the tokens of position jm from the merging workgroups into s_tok (workgroup 0 also writes
+  // the drafted tokens)
+  auto fetch_tokens = [&](int jm) -> bool {
+    const uint32_t tg = (epoch << 8) | (uint32_t)(jm + 1);
+    bool ok = true;
+    if (tid < batch) {
+      const uint64_t* tp = a.tokw + (size_t)(jm & 1) * kMaxBatch + tid;
+      uint64_t v = ld64(tp);
+      if ((uint32_t)(v >> 32) != tg) ok = wait_tag(tp, tg, err, v);
+      const int tok = (int)(uint32_t)v;
+      s_tok[tid] = tok;
+      if (w == 0) a.out_tokens[(size_t)tid * Bk + jm] = tok;
+    }
+    return !fail_barrier(!ok, s_fail);
+  };
+  auto tokens_of = [&](int jm) -> bool { return delegate ? fetch_tokens(jm) : merge_position(jm); };
+
   // Publish the row-statistics partial of this workgroup for position jp (slots of M tile mtp,
   // per-wave partials in s_part): merged over the waves, then nine tagged words per slot,
   // written by the lanes of wave `by` (a wave's loads wait for its earlier stores, so the
@@ -905,6 +953,14 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     const bool long_only = a.literal && j == 0;
     const int hs = a.literal ? j - 1 : j;          // head step index (the first one starts from h = 0)
 
+    // the merging workgroups of the RNN head: the keys of their sequence at the previous position
+    if (!MARKOV && merge_seq >= 0 && j > 0) {
+      if (!merge_one(j - 1, merge_seq)) {
+        bail();
+        return;
+      }
+    }
+
     // ======================= GRU and rank (GRU workgroups) =======================
     if (!MARKOV && gru && !long_only) {
       const uint32_t tag_prev = (epoch << 8) | (uint32_t)j;   // h published at position j-1
@@ -915,7 +971,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
       const size_t hrep_stride = (size_t)batch * H;
       uint32_t* h32new = NARROW ? nullptr : a.h32 + (size_t)set * kH32Set + (size_t)par * a.hrep * hrep_stride;
       if (j > 0) {
-        if (!merge_position(j - 1)) {
+        if (!tokens_of(j - 1)) {
           bail();
           return;
         }
@@ -1218,7 +1274,7 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     // ======================= Markov head: the previous token (all workgroups) =======================
     if (MARKOV && !long_only) {
       if (j > 0) {
-        if (!merge_position(j - 1)) {
+        if ((merge_seq >= 0 && !merge_one(j - 1, merge_seq)) || !tokens_of(j - 1)) {
           bail();
           return;
         }
@@ -1603,8 +1659,12 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   }
 
   // ---- the last position's tokens (workgroup 0)
+  if (merge_seq >= 0 && !merge_one(Bk - 1, merge_seq)) {
+    bail();
+    return;
+  }
   if (w == 0) {
-    if (!merge_position(Bk - 1)) {
+    if (!tokens_of(Bk - 1)) {
       bail();
       return;
     }

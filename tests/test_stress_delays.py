@@ -1,12 +1,12 @@
 """Hand-off robustness under injected delays (GPU).
 
 libdels_stress.so is the library with the persistent kernel compiled with DLS_STRESS_DELAYS: before
-every cross-workgroup publish (h words, rho words, argmax keys, statistics partials, the final
-header) a wave may pause 3 to 10 us, pseudo-randomly per call, workgroup, wave, position and site.
-The pauses reorder the hand-offs but must not change a single bit: each call is compared with the
-product library's result on the same inputs, for the narrow and both wide forms, the Markov head,
-sampling, the prior and both launch modes, several calls in a row on one workspace (every call
-draws other pauses).  The error word must stay clear; the pauses lie far inside the bounded waits.
+every cross-workgroup publish (h words, rho words, argmax keys, merged tokens, statistics partials,
+the final header) a wave may pause 3 to 10 us, pseudo-randomly per call, workgroup, wave, position
+and site.  The pauses reorder the hand-offs but must not change a single bit: each call is compared
+with the product library's result on the same inputs, for the narrow and both wide forms (one M
+tile, and several with the delegated token merge), the Markov head, sampling, the prior and both
+launch modes, several calls in a row on one workspace (every call draws other pauses).  The error word must stay clear; the pauses lie far inside the bounded waits.
 """
 import math
 import os
@@ -48,6 +48,7 @@ def _draft(head, wl, L, last, ws, **kw):
     ("qwen3-8b-b16", False, 37, {}),                                    # wide, three M tiles, ragged
     ("b64-d5120", False, None, {"exclusive_device": True}),             # wide, four M tiles, ordinary dispatch
     ("qwen3-8b-b16", True, None, {}),                                   # Markov head
+    ("b64-d5120", True, 37, {}),                                        # Markov head, delegated merge
     ("qwen3-8b-b16", False, None, {"temperature": 1.0, "seed": 77}),    # sampled
     ("qwen3-8b-b16", False, None, {"prior": True, "beta": 0.4}),        # prior
 ])
