@@ -24,7 +24,9 @@ from parity_util import check_draft
 pytestmark = pytest.mark.gpu
 
 RULES = {"qwen3-4b-b1": {O.UNC_ENTROPY: (0.55, 0.65), O.UNC_MAXPROB: (0.85, 0.97)},
-         "qwen3-8b-b16": {O.UNC_ENTROPY: (0.40, 0.80), O.UNC_MAXPROB: (0.80, 0.99)}}
+         "qwen3-8b-b16": {O.UNC_ENTROPY: (0.40, 0.80), O.UNC_MAXPROB: (0.80, 0.99)},
+         # the 25th and 75th to 80th percentiles of u over the batch-64 rows
+         "b64-d5120": {O.UNC_ENTROPY: (0.35, 0.50), O.UNC_MAXPROB: (0.67, 0.90)}}
 
 
 def _oracle_unc(rows, measure, lo, hi):
@@ -247,3 +249,20 @@ def test_adaptive_split_launches():
     g = _gates(long_h, O.UNC_ENTROPY, lo, hi)
     assert np.max(np.abs(unc[..., 3] - g)) <= 1e-5 / (hi - lo) + 1e-6
     check_draft(tok, st, oh, long_h, last, None, 1.0, 0.6, 0.3, sequences=[0, 63, 64, 79], gates=g)
+
+
+@pytest.mark.parametrize("measure", [O.UNC_ENTROPY, O.UNC_MAXPROB])
+@pytest.mark.parametrize("kind", ["rnn", "markov"])
+def test_adaptive_b64_full_size(kind, measure):
+    """Adaptive fusion at the batch-64 serving shape the bench times (prepared head, four M tiles
+    and the delegated token merge), every sequence against the oracle with its own gates."""
+    wl, head, oh = _rnn("b64-d5120") if kind == "rnn" else _markov("b64-d5120")
+    head.prepare()
+    assert head.path(wl.batch, wl.B, torch.bfloat16, False) == 1
+    lo, hi = RULES["b64-d5120"][measure]
+    tok, st, unc, long_h, last = _run(head, wl, measure, lo, hi, alpha=0.5, beta=0.0)
+    g = _gates(long_h, measure, lo, hi)
+    assert ((g > 0) & (g < 1)).mean() > 0.2
+    assert np.max(np.abs(unc[..., 3] - g)) <= 1e-5 / (hi - lo) + 1e-6
+    rep = check_draft(tok, st, oh, long_h, last, None, 1.0, 0.5, 0.0, gates=g)
+    print(f"  near_ties={rep['near_ties']} fusion_active={rep['fusion_active']:.2f} errs={rep['errs']}")

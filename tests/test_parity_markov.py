@@ -145,3 +145,19 @@ def test_markov_f32_long_logits_and_repeat():
     ref = O.draft_block(p["oracle"], p["long_h"], p["last"], None, 1.0, 0.5, 0.0)
     near = outs[0][0].cpu().numpy() != ref.tokens
     assert np.all(ref.gap[near] < TOL)
+
+
+@pytest.mark.parametrize("with_prior", [False, True])
+def test_markov_b64_full_size(with_prior):
+    """The Markov head at the batch-64 serving shape (V = 151,936, r = 256; prepared, four M
+    tiles and the delegated token merge), greedy, with and without the Zipf prior, every sequence."""
+    wl = W.WORKLOADS["b64-d5120"]
+    em, wm = W.make_markov_head(wl.V, wl.r, "bf16", 92, scale=math.sqrt(3.0 / math.sqrt(wl.r)))
+    head = B.LocalHead.markov_from_weights(em, wm).prepare()
+    oh = O.MarkovHead(np.asarray(em, np.float64), np.asarray(wm, np.float64))
+    long_h, last = W.make_long_logits(wl), W.make_last_token(wl)
+    prior = W.make_zipf_log_prior(wl.V, wl.seed) if with_prior else None
+    be = 0.5 if with_prior else 0.0
+    tok, st = _run(head, long_h, last, prior=prior, wl=1.0, al=0.5, be=be, expect_path=1)
+    rep = check_draft(tok, st, oh, long_h, last, prior, 1.0, 0.5, be)
+    print(f"markov b64 prior={with_prior}: near_ties={rep['near_ties']} errs={rep['errs']}")

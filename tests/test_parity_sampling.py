@@ -201,3 +201,22 @@ def test_sampling_distribution_chi_square(prepared):
     print(f"prepared={prepared} counts={counts[:-1].astype(int).tolist()} expected={np.round(exp).tolist()} "
           f"chi2={chi2:.2f}")
     assert chi2 < 40.5              # chi-square(7 dof) upper 1e-6 quantile
+
+
+@pytest.mark.parametrize("kind", ["rnn", "markov"])
+def test_sampling_b64_full_size(kind):
+    """T = 1 at the batch-64 serving shape the bench times (prepared head, four M tiles and the
+    delegated token merge), every sequence against the oracle's own Philox draws."""
+    wl = W.WORKLOADS["b64-d5120"]
+    if kind == "rnn":
+        hw = W.make_head(wl, "stress")
+        head, oh = B.LocalHead.from_weights(hw), O.RnnHead.from_weights(hw)
+    else:
+        em, wm = W.make_markov_head(wl.V, wl.r, "bf16", 91, scale=math.sqrt(3.0 / math.sqrt(wl.r)))
+        head = B.LocalHead.markov_from_weights(em, wm)
+        oh = O.MarkovHead(np.asarray(em, np.float64), np.asarray(wm, np.float64))
+    head.prepare()
+    long_h, last = W.make_long_logits(wl), W.make_last_token(wl)
+    tok, st = _run(head, long_h, last, expect_path=1)
+    rep = check_draft(tok, st, oh, long_h, last, None, 1.0, 0.5, 0.0, temperature=1.0, seed=SEED)
+    print(f"{kind} b64 T=1: near_ties={rep['near_ties']} errs={rep['errs']}")
