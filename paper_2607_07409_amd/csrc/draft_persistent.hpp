@@ -7,7 +7,8 @@
 // the rest in LDS.  The first NG = H/16 workgroups ("GRU workgroups") also own 16 hidden
 // units each (their W_hh rows in LDS) and r/NG rows of W_rank.  Per draft position j:
 //
-//   GRU wgs  merge the argmax keys of position j-1 -> tokens u_j (all sequences)
+//   GRU wgs  merge the argmax keys of position j-1 -> tokens u_j (all sequences); with
+//            several M tiles workgroup NG + b merges sequence b and they read its token
 //            gi = T[u_j] (folded table) + gh (from the previous step) -> gates -> h_{j+1}
 //            of the owned units, published
 //            rho_i = SiLU(W_rank h_{j+1}) for the owned rank rows (MFMA), published; then
@@ -602,7 +603,8 @@ __device__ __forceinline__ void plane_operand(const uint16_t* hi, const uint16_t
 
 // NARROW: at most 4 sequences (one M tile whose useful rows all sit in lanes 0..15)
 // MARKOV: the Markov head of App. A, rho_j = E_M[u_j]: no GRU workgroups and no hand-off
-//         but the argmax keys; every workgroup merges the keys and reads the E_M row itself
+//         but the argmax keys (and, with several M tiles, the merged tokens); every workgroup
+//         gets the tokens and reads the E_M row itself
 // the value of lane l ^ k within its quad (k = 1, 2, 3): a DPP quad permutation
 __device__ __forceinline__ uint32_t quad_xor(uint32_t v, int k) {
   switch (k) {
