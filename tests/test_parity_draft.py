@@ -222,6 +222,19 @@ def test_batches_split_into_launches(batch):
     check_draft(tok, st, p["oracle"], p["long_h"], p["last"], p["prior"], 1.0, 0.6, 0.4, True, seqs)
 
 
+@pytest.mark.parametrize("batch", [4, 5, 15, 16, 17, 31, 32, 33, 47, 48, 49, 63])
+def test_batch_sweep_across_m_tiles(batch):
+    """Every batch size on either side of the narrow/wide switch (4 | 5) and of each 16-sequence M
+    tile boundary, where the token merge changes hands (one M tile: every GRU workgroup merges;
+    several: workgroup NG + b merges sequence b), every sequence compared, greedy and with the
+    prior and the literal first row."""
+    p = _problem("qwen3-8b-b16", "stress", dtype="bf16", V=2053, d=64, H=128, r=128, Bk=3, batch=batch)
+    tok, st = _draft(p, 0.6, prepared=True, expect_path=1)
+    check_draft(tok, st, p["oracle"], p["long_h"], p["last"], None, 1.0, 0.6, 0.0)
+    tok, st = _draft(p, 0.6, 0.4, with_prior=True, literal=True, prepared=True, expect_path=1)
+    check_draft(tok, st, p["oracle"], p["long_h"], p["last"], p["prior"], 1.0, 0.6, 0.4, True)
+
+
 def test_split_launches_sample_by_sequence_index():
     """Sampling keys the noise by the sequence's index in the whole call: at batch 80 (launches of
     64 and 16 sequences) the draws of sequences 63, 64 and 79 are the oracle's for that index, and
