@@ -211,8 +211,7 @@ __device__ __forceinline__ f32x4_t mfma_av(u32x4 a_agpr, uint4 b, f32x4_t c) {
   aa.u = a_agpr;
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(aa.b, as_bf(b), c, 0, 0, 0);
 }
-__device__ __forceinline__ u32x4 to_agpr(uint4 v) {
-  u32x4 r = {v.x, v.y, v.z, v.w};
+__device__ __forceinline__ u32x4 in_agpr(u32x4 r) {
   asm volatile("; weights -> agpr" : "=a"(r) : "0"(r));
   return r;
 }
@@ -375,6 +374,9 @@ namespace {
 
 // Copy n 16-byte words from global memory into LDS, 8 loads in flight per thread (indices past
 // the end re-read the last word, so that every load is unconditional).
+// Eight loads per thread in flight, then eight stores.  Threads past the end copy the last
+// element again (the same value to the same place) instead of branching: a store under a branch
+// let the compiler sink each load into it and wait for each one in turn.
 __device__ __forceinline__ void copy_to_lds(uint4* dst, const uint4* src, int n) {
   for (int base = 0; base < n; base += kT * 8) {
     uint4 v[8];
@@ -386,7 +388,7 @@ __device__ __forceinline__ void copy_to_lds(uint4* dst, const uint4* src, int n)
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
       const int i = base + m * kT + (int)threadIdx.x;
-      if (i < n) dst[i] = v[m];
+      dst[i < n ? i : n - 1] = v[m];
     }
   }
 }
@@ -737,7 +739,8 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     for (size_t i = (size_t)w * per + tid; i < (size_t)(w + 1) * per && i < n64; i += kT) st64(hz + i, 0ull);
   }
 
-  // ---- resident weights
+  // ---- resident weights: every load of the wave's tiles is issued before any is moved into
+  // its AGPRs (moved one by one, each move waited for its own load before the next was issued)
   u32x4 wr[TPW * KK];
 #pragma unroll
   for (int q = 0; q < TPW; ++q) {
@@ -746,9 +749,11 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     for (int kk = 0; kk < KK; ++kk) {
       uint4 v = make_uint4(0, 0, 0, 0);
       if (lt < na) v = a.wv[((size_t)(t0 + lt) * KK + kk) * 64 + lane];
-      wr[q * KK + kk] = to_agpr(v);
+      wr[q * KK + kk] = u32x4{v.x, v.y, v.z, v.w};
     }
   }
+#pragma unroll
+  for (int i = 0; i < TPW * KK; ++i) wr[i] = in_agpr(wr[i]);
   if (gru) {
     copy_to_lds(s_whh, a.whh + (size_t)w * 3 * KKH * 64, 3 * KKH * 64);
     for (int i = tid; i < rpg * H / 8; i += kT) {
@@ -1672,43 +1677,51 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
     }
     tokens_done = true;
   }
-  // ---- row statistics: row (b, j) is merged by workgroup (b * B + j) % G from the tagged partials
+  // ---- row statistics: row (b, j) is merged by workgroup (b * B + j) % G from the tagged partials,
+  // up to four rows at a time, one per wave: lane l merges the partials of workgroups l, l + 64,
+  // ... in that order, then the wave merges its lanes (a fixed butterfly)
   if (a.out_stats) {
-    for (int q = w; q < batch * Bk; q += G) {
-      const int b = q / Bk, jm = q % Bk;
-      const uint32_t stag = (epoch << 8) | (uint32_t)(jm + 1);
-      Partial P = partial_empty();
+    const int lane64 = local_tid() & 63;
+    for (int q0 = w; q0 < batch * Bk; q0 += 4 * G) {
+      const int q = q0 + wave * G;
       bool ok = true;
-      if (tid < G) {
-        const uint64_t* sp = a.stats + (((size_t)jm * batch + b) * G + tid) * kStatWords;
-        uint64_t w9[kStatWords];
+      if (q < batch * Bk) {   // wave-uniform
+        const int b = q / Bk, jm = q % Bk;
+        const uint32_t stag = (epoch << 8) | (uint32_t)(jm + 1);
+        Partial P = partial_empty();
+        for (int sl = lane64; sl < G; sl += 64) {
+          const uint64_t* sp = a.stats + (((size_t)jm * batch + b) * G + sl) * kStatWords;
+          uint64_t w9[kStatWords];
 #pragma unroll
-        for (int e = 0; e < kStatWords; ++e) w9[e] = ld64(sp + e);
-        float q9[kStatWords];
+          for (int e = 0; e < kStatWords; ++e) w9[e] = ld64(sp + e);
+          float q9[kStatWords];
 #pragma unroll
-        for (int e = 0; e < kStatWords; ++e) {
-          if ((uint32_t)(w9[e] >> 32) != stag) ok &= wait_tag(sp + e, stag, err, w9[e]);
-          q9[e] = __uint_as_float((uint32_t)w9[e]);
+          for (int e = 0; e < kStatWords; ++e) {
+            if ((uint32_t)(w9[e] >> 32) != stag) ok &= wait_tag(sp + e, stag, err, w9[e]);
+            q9[e] = __uint_as_float((uint32_t)w9[e]);
+          }
+          Partial Q;
+          Q.L.m = q9[0]; Q.L.s = q9[1];
+          Q.S.m = q9[2]; Q.S.s = q9[3];
+          Q.F.m = q9[4]; Q.F.s = q9[5];
+          Q.t1 = q9[6]; Q.t2 = q9[7];
+          Q.i1 = __float_as_int(q9[8]);
+          Q.pad = 0;
+          P = sl == lane64 ? Q : partial_merge(P, Q);
         }
-        P.L.m = q9[0]; P.L.s = q9[1];
-        P.S.m = q9[2]; P.S.s = q9[3];
-        P.F.m = q9[4]; P.F.s = q9[5];
-        P.t1 = q9[6]; P.t2 = q9[7];
-        P.i1 = __float_as_int(q9[8]);
+        P = allred_partial(P, WaveXor{});
+        if (lane64 == 0 && ok) {
+          int t;
+          const int ti = P.i1 == 0x7fffffff ? 0 : P.i1;   // the token finalize_row decodes
+          const float alr = a.unc ? a.al_j[jm] * a.unc[(size_t)b * Bk + jm].gate : a.al_j[jm];
+          finalize_row(P, wl, alr, a.literal && jm == 0, &t, a.out_stats + (size_t)b * Bk + jm, nullptr,
+                       SAMPLE ? gumbel_at(a.smp, b, jm, ti) : 0.f, a.smp.temp);
+        }
       }
       if (fail_barrier(!ok, s_fail)) {
         bail();
         return;
       }
-      P = block_merge(P, s_part, 4);
-      if (tid == 0) {
-        int t;
-        const int ti = P.i1 == 0x7fffffff ? 0 : P.i1;   // the token finalize_row decodes
-        const float alr = a.unc ? a.al_j[jm] * a.unc[(size_t)b * Bk + jm].gate : a.al_j[jm];
-        finalize_row(P, wl, alr, a.literal && jm == 0, &t, a.out_stats + (size_t)b * Bk + jm, nullptr,
-                     SAMPLE ? gumbel_at(a.smp, b, jm, ti) : 0.f, a.smp.temp);
-      }
-      __syncthreads();
     }
   }
   if (w == 0 && tid == 0) {
