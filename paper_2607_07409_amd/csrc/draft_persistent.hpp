@@ -756,15 +756,25 @@ __global__ __launch_bounds__(kT, 1) void k_draft_persistent(PersistArgs a) {
   for (int i = 0; i < TPW * KK; ++i) wr[i] = in_agpr(wr[i]);
   if (gru) {
     copy_to_lds(s_whh, a.whh + (size_t)w * 3 * KKH * 64, 3 * KKH * 64);
-    for (int i = tid; i < rpg * H / 8; i += kT) {
-      const int row = i / (H / 8), c = i % (H / 8);
-      *(uint4*)(s_wrank + (size_t)row * H + 8 * c) = *(const uint4*)(a.w_rank + (size_t)(w * rpg + row) * H + 8 * c);
-    }
+    // the owned rank rows are rows w rpg ... w rpg + rpg - 1 of W_rank, one contiguous block
+    copy_to_lds((uint4*)s_wrank, (const uint4*)(a.w_rank + (size_t)w * rpg * H), rpg * H / 8);
   } else {
     copy_to_lds(s_wtiles, a.wv + ((size_t)(t0 + na) * KK) * 64, nl * KK * 64);
   }
-  if (PRIOR)
-    for (int i = tid; i < nrows; i += kT) s_prior[i] = v_base + i < V ? a.prior[v_base + i] : 0.f;
+  if (PRIOR) {   // four loads per thread in flight; past the end a thread copies the last row again
+    for (int base = 0; base < nrows; base += 4 * kT) {
+      float pv[4];
+      int ix[4];
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const int i = base + m * kT + tid;
+        ix[m] = i < nrows ? i : nrows - 1;
+        pv[m] = v_base + ix[m] < V ? a.prior[v_base + ix[m]] : 0.f;
+      }
+#pragma unroll
+      for (int m = 0; m < 4; ++m) s_prior[ix[m]] = pv[m];
+    }
+  }
   if (tid == 0) {
     const PreparedHeader& ex = a.expect;
     const bool mismatch = ph.magic != ex.magic || ph.V != ex.V || ph.d != ex.d || ph.H != ex.H || ph.r != ex.r ||
