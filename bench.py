@@ -124,6 +124,36 @@ def per_call_us(fn, n, torch, scratch=None):
     return [a.elapsed_time(b) * 1e3 for a, b in evs]
 
 
+def measured_peaks(B, dev, torch, read_gib=4, calls=20):
+    """The device's attainable peaks, beside the vendor figures the rooflines are quoted against:
+    a read of a read_gib GiB buffer (far larger than L2 and MALL) with 16-byte non-temporal loads
+    on every CU, and a bf16 matrix-core loop of 8192 workgroups x 4 waves x 1024 rounds x 4
+    independent 32x32x16 products.  Both are checked (the read's checksum words against the buffer's XOR,
+    every MFMA lane against its exact value) and timed per call with HIP events; medians."""
+    nbytes = read_gib << 30
+    buf = torch.empty(nbytes // 4, dtype=torch.int32, device=dev)
+    buf.fill_(0x5A5A5A5A)
+    buf[-1] = 1  # an odd number of equal words and a 1: the buffer's XOR is 0x5A5A5A5B
+    words = B.measure_read(buf)
+    read_us = per_call_us(lambda _: B.measure_read(buf, out=words), calls, torch)
+    xor = 0
+    for w in words.cpu().tolist():
+        xor ^= w & 0xFFFFFFFF
+    del buf
+    torch.cuda.empty_cache()
+    groups, iters, x = 8192, 1024, 1.0 / 64
+    acc = B.measure_mfma(groups, iters, x, device=dev)
+    mfma_us = per_call_us(lambda _: B.measure_mfma(groups, iters, x, out=acc), calls, torch)
+    exact = bool((acc == iters * 1024 * x * x).all().item())
+    flops = groups * 4 * iters * 4 * 32768
+    r_med, m_med = pct(read_us, 50), pct(mfma_us, 50)
+    return {"hbm_read_GBs": round(nbytes / (r_med * 1e-6) / 1e9, 1), "hbm_vendor_GBs": HBM_PEAK_GBS,
+            "read_bytes": nbytes, "read_us": dist(read_us), "read_checksum_ok": xor == 0x5A5A5A5B,
+            "bf16_mfma_TFLOPs": round(flops / (m_med * 1e-6) / 1e12, 1), "bf16_vendor_TFLOPs": BF16_PEAK_TFLOPS,
+            "mfma_flops": flops, "mfma_us": dist(mfma_us), "mfma_exact": exact,
+            "how": "dls_measure_read over a fresh-filled buffer; dls_measure_mfma (v_mfma_f32_32x32x16_bf16)"}
+
+
 # ------------------------------------------------------------------------------------------------
 # CPU oracle leg: a fresh subprocess per thread count (BLAS threads fixed before numpy loads)
 # ------------------------------------------------------------------------------------------------
@@ -425,6 +455,12 @@ def main():
         f"cold median {pct(cold, 50):.1f} us; {achieved:.0f} GB/s re-read algorithmic "
         f"({achieved / HBM_PEAK_GBS:.1%}), compulsory {roofline['compulsory_frac']:.1%}")
 
+    peaks = measured_peaks(B, dev, torch)
+    roofline["frac_of_measured_read_peak"] = round(achieved / peaks["hbm_read_GBs"], 4)
+    log(f"measured peaks: HBM read {peaks['hbm_read_GBs']:.0f} GB/s (checksum ok={peaks['read_checksum_ok']}), "
+        f"bf16 MFMA {peaks['bf16_mfma_TFLOPs']:.0f} TFLOP/s (exact={peaks['mfma_exact']}); the draft block "
+        f"reaches {roofline['frac_of_measured_read_peak']:.1%} of the measured read rate")
+
     extras = {}
     if not args.no_extras:
         # the other launch mode (cooperative vs ordinary dispatch)
@@ -603,6 +639,7 @@ def main():
                    "step": "draft_block + accept_len",
                    "launch": "ordinary dispatch (DLS_EXCLUSIVE_DEVICE)" if EXC else "cooperative"},
         "roofline": roofline,
+        "measured_peaks": peaks,
         "cpu_baseline": cpu,
         "parity": parity,
     }

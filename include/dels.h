@@ -371,6 +371,32 @@ dls_status dls_accept_len(const int32_t *draft, const int32_t *target, int32_t b
 dls_status dls_unigram_log_prior(const int32_t *tokens, int64_t n, int32_t V, float smoothing,
                                  uint64_t *out_counts, float *out_log_prior, void *stream);
 
+/* ---------------------------------------------------------------------------------
+ * Measurement helpers.  They compute nothing of the method: they measure the device's
+ * attainable peaks, which benchmarks report beside the vendor figures (8 TB/s HBM,
+ * 2.5 PFLOP/s dense bf16) that rooflines are quoted against.  Asynchronous on `stream`;
+ * time them with events on it.
+ *
+ * dls_measure_read streams `bytes` of `buf` once with 16-byte non-temporal loads and
+ *   writes one checksum word per workgroup (the XOR of every 32-bit word it read) into
+ *   `out`, so that no load is dropped; the XOR of the DLS_MEASURE_READ_WORDS words is
+ *   the XOR of the whole buffer.  bytes / duration is the attainable HBM read bandwidth
+ *   when the buffer is much larger than the caches (>= 2 GB).
+ *   buf  device, 16-byte aligned, bytes a multiple of 16 (> 0)
+ *   out  device, DLS_MEASURE_READ_WORDS uint32
+ * dls_measure_mfma runs `iters` rounds of 4 independent v_mfma_f32_32x32x16_bf16
+ *   products (32768 flops each) in every wave of `groups` workgroups of 256 threads
+ *   (4 waves): groups * 4 * iters * 131072 flops.  Every input element is x (a power of
+ *   two, exact in bf16), so out[t] (one float per thread, groups * 256 of them) is
+ *   exactly iters * 1024 * x^2 (the iteration limit keeps every partial sum below 2^24
+ *   units of 16 x^2).
+ *   Limits: 1 <= groups <= 65536, 1 <= iters <= 2^18; x a power of two in [2^-20, 1].
+ * Errors: DLS_ERR_ARG for NULL or misaligned pointers, DLS_ERR_SHAPE for sizes outside
+ * the limits, DLS_ERR_DEVICE without a device. */
+#define DLS_MEASURE_READ_WORDS 8192
+dls_status dls_measure_read(const void *buf, size_t bytes, uint32_t *out, void *stream);
+dls_status dls_measure_mfma(int32_t groups, int32_t iters, float x, float *out, void *stream);
+
 /* Names and messages. */
 const char *dls_status_string(dls_status status);
 const char *dls_last_error(void);

@@ -143,6 +143,10 @@ def _configure(L: ctypes.CDLL) -> ctypes.CDLL:
     L.dls_unigram_log_prior.argtypes = [_vp, _i64, _i32, ctypes.c_float, _vp, _vp, _vp]
     L.dls_accept_len.restype = ctypes.c_int
     L.dls_accept_len.argtypes = [_vp, _vp, _i32, _i32, _vp, _vp]
+    L.dls_measure_read.restype = ctypes.c_int
+    L.dls_measure_read.argtypes = [_vp, _sz, _vp, _vp]
+    L.dls_measure_mfma.restype = ctypes.c_int
+    L.dls_measure_mfma.argtypes = [_i32, _i32, ctypes.c_float, _vp, _vp]
     L.dls_status_string.restype = ctypes.c_char_p
     L.dls_status_string.argtypes = [ctypes.c_int]
     L.dls_last_error.restype = ctypes.c_char_p
@@ -449,3 +453,30 @@ def unigram_log_prior(tokens: torch.Tensor, V: int, smoothing: float = 1.0, out=
     _check(L.dls_unigram_log_prior(_ptr(tokens) if n else None, n, V, smoothing, _ptr(counts), _ptr(logp),
                                    _stream(stream)))
     return logp, counts
+
+
+MEASURE_READ_WORDS = 8192
+
+
+def measure_read(buf: torch.Tensor, out=None, stream=None) -> torch.Tensor:
+    """Stream every byte of `buf` once (the attainable HBM read bandwidth when it is much
+    larger than the caches); returns the DLS_MEASURE_READ_WORDS uint32 checksum words, stored
+    as int32, whose XOR is the XOR of the buffer's 32-bit words."""
+    L = lib()
+    if not buf.is_contiguous():
+        raise ValueError("buf must be contiguous")
+    if out is None:
+        out = torch.empty(MEASURE_READ_WORDS, dtype=torch.int32, device=buf.device)
+    _check(L.dls_measure_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(out), _stream(stream)))
+    return out
+
+
+def measure_mfma(groups: int, iters: int, x: float = 1.0 / 64, out=None, stream=None,
+                 device=None) -> torch.Tensor:
+    """Run groups * 4 * iters * 4 dense bf16 32x32x16 matrix-core products (32768 flops each);
+    returns one float per thread, each exactly iters * 1024 * x^2."""
+    L = lib()
+    if out is None:
+        out = torch.empty(groups * 256, dtype=torch.float32, device=device or "cuda")
+    _check(L.dls_measure_mfma(groups, iters, x, _ptr(out), _stream(stream)))
+    return out

@@ -10,6 +10,7 @@
 #include <type_traits>
 
 #include "dels_internal.hpp"
+#include "peaks.hpp"
 
 namespace {
 
@@ -623,6 +624,35 @@ dls_status dls_accept_len(const int32_t* draft, const int32_t* target, int32_t b
   if (s != DLS_OK) return s;
   hipError_t e = dls::launch_accept(draft, target, batch, B, out_len, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "accept_len launch");
+  return DLS_OK;
+}
+
+dls_status dls_measure_read(const void* buf, size_t bytes, uint32_t* out, void* stream) {
+  clear_error();
+  if (bytes == 0 || bytes % 16 != 0) return fail(DLS_ERR_SHAPE, "bytes=%zu must be a positive multiple of 16", bytes);
+  if (!buf || !out) return fail(DLS_ERR_ARG, "required pointer is NULL");
+  if (!aligned(buf, 16) || !aligned(out, 4)) return fail(DLS_ERR_ARG, "misaligned pointer");
+  dls_status s = check_device();
+  if (s != DLS_OK) return s;
+  static_assert(dls::kMeasureReadGroups == DLS_MEASURE_READ_WORDS, "checksum word count");
+  hipError_t e = dls::launch_measure_read(buf, bytes, out, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "measure_read launch");
+  return DLS_OK;
+}
+
+dls_status dls_measure_mfma(int32_t groups, int32_t iters, float x, float* out, void* stream) {
+  clear_error();
+  if (groups < 1 || groups > 65536) return fail(DLS_ERR_SHAPE, "groups=%d outside [1, 65536]", groups);
+  if (iters < 1 || iters > (1 << 18)) return fail(DLS_ERR_SHAPE, "iters=%d outside [1, 2^18]", iters);
+  int ex = 0;
+  if (!std::isfinite(x) || std::frexp(x, &ex) != 0.5f || ex < -19 || ex > 1)
+    return fail(DLS_ERR_ARG, "x must be a power of two in [2^-20, 1]");
+  if (!out) return fail(DLS_ERR_ARG, "required pointer is NULL");
+  if (!aligned(out, 4)) return fail(DLS_ERR_ARG, "misaligned pointer");
+  dls_status s = check_device();
+  if (s != DLS_OK) return s;
+  hipError_t e = dls::launch_measure_mfma(groups, iters, x, out, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "measure_mfma launch");
   return DLS_OK;
 }
 

@@ -13,7 +13,7 @@ ROOT = os.path.dirname(PKG)
 OBJ_DIR = os.path.join(ROOT, "_build", "dels")
 LIB = os.path.join(PKG, "libdels.so")
 SOURCES = ["api.cpp", "combine.hip", "draft.hip", "accept.hip", "prepare.hip", "draft_persistent.hip", "prior.hip",
-           "noalloc.hip", "uncertainty.hip",
+           "noalloc.hip", "uncertainty.hip", "peaks.hip",
            # the persistent kernel's instantiations, one unit per rank size and decoding mode
            "persist_greedy_r128.hip", "persist_greedy_r256.hip", "persist_sampled_r128.hip",
            "persist_sampled_r256.hip"]

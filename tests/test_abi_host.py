@@ -390,3 +390,27 @@ def test_adaptive_valid_arguments_stop_at_device_check():
         rc, msg = _adaptive(_head(), b.adaptive_rule(m, -1.0, 2.0))
         assert b.STATUS[rc] == "DLS_ERR_DEVICE", msg
         assert _unc(b.adaptive_rule(m, 0.2, 0.3))[0] == "DLS_ERR_DEVICE"
+
+
+def test_measure_helpers_reject_bad_arguments():
+    L = b.lib()
+    rd = lambda buf=FAKE[0], n=1 << 20, out=FAKE[1]: b.STATUS[L.dls_measure_read(buf, n, out, None)]
+    assert rd(n=0) == "DLS_ERR_SHAPE"
+    assert rd(n=(1 << 20) + 8) == "DLS_ERR_SHAPE"
+    assert rd(buf=None) == "DLS_ERR_ARG"
+    assert rd(out=None) == "DLS_ERR_ARG"
+    assert rd(buf=ctypes.c_void_p(FAKE[0].value + 4)) == "DLS_ERR_ARG"
+    assert rd(out=ctypes.c_void_p(FAKE[1].value + 2)) == "DLS_ERR_ARG"
+    mf = lambda g=8, it=16, x=1.0 / 64, out=FAKE[2]: b.STATUS[L.dls_measure_mfma(g, it, x, out, None)]
+    assert mf(g=0) == "DLS_ERR_SHAPE"
+    assert mf(g=65537) == "DLS_ERR_SHAPE"
+    assert mf(it=0) == "DLS_ERR_SHAPE"
+    assert mf(it=(1 << 18) + 1) == "DLS_ERR_SHAPE"
+    for x in (0.0, 0.75, 2.0, 2.0 ** -21, -0.5, float("nan"), float("inf")):
+        assert mf(x=x) == "DLS_ERR_ARG", x
+    assert mf(out=None) == "DLS_ERR_ARG"
+    assert mf(out=ctypes.c_void_p(FAKE[2].value + 2)) == "DLS_ERR_ARG"
+    if not HAS_GPU:
+        assert rd() == "DLS_ERR_DEVICE"
+        for x in (1.0, 2.0 ** -20, 0.5):
+            assert mf(x=x, it=1 << 18, g=65536) == "DLS_ERR_DEVICE", x
