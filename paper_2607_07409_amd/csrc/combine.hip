@@ -3,13 +3,14 @@
 //
 // A row of V elements is split into `parts` contiguous ranges, one workgroup each.
 // Every thread streams 16-byte chunks of the long and short rows (coalesced across
-// the workgroup), forms l = w_long*l_L + alpha*l_S - beta*l_P in float32 and folds
+// the workgroup, non-temporal loads), forms l = w_long*l_L + alpha*l_S - beta*l_P in float32 and folds
 // the chunk into its running (max, sum exp) for l_L, l_S, l and into the top-2 of l.
 // The workgroup merge is a fixed-order butterfly, so results are deterministic.
 // Without row statistics or scores only the running maximum of l and its index are
 // kept: the argmax needs no normaliser, and the kernel is then bound by HBM bandwidth.
 // With parts > 1 a second kernel merges the per-range partials of each row.
 #include "dels_internal.hpp"
+#include "stream_load.hpp"
 
 namespace dls {
 
@@ -84,8 +85,8 @@ __global__ __launch_bounds__(NT) void k_combine_part(
     for (int u = 0; u < kUnroll; ++u) {
       const int cc = c + u * NT;
       if (cc < c1) {
-        ra[u] = Chunk<T>::raw(Lr + h0 + (size_t)cc * N);
-        rb[u] = Chunk<T>::raw(Sr + h0 + (size_t)cc * N);
+        ra[u] = stream_load16(Lr + h0 + (size_t)cc * N);
+        rb[u] = stream_load16(Sr + h0 + (size_t)cc * N);
       }
     }
     if (STATS && c + (kUnroll - 1) * NT < c1) {

@@ -11,6 +11,7 @@
 // order.  The gate g = clamp((u - h_lo) / (h_hi - h_lo), 0, 1) of the chosen measure u is
 // written beside the entropy and the maximum probability.
 #include "dels_internal.hpp"
+#include "stream_load.hpp"
 
 namespace dls {
 
@@ -115,7 +116,7 @@ __global__ __launch_bounds__(kThreads) void k_unc_part(const T* __restrict__ L, 
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int cc = c + u * kThreads;
-      if (cc < c1) raw[u] = Chunk<T>::raw(Lr + h0 + (size_t)cc * N);
+      if (cc < c1) raw[u] = stream_load16(Lr + h0 + (size_t)cc * N);
     }
     if (c + (kUnroll - 1) * kThreads < c1) {   // every chunk in range: one rescale for all of them
       float x[N * kUnroll];
