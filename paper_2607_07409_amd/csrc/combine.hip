@@ -30,6 +30,12 @@ __device__ __forceinline__ float fuse1(float a, float b, float p, float wl, floa
   return f;
 }
 
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m));
+  return x;
+}
+
 // running maximum and its index only (lowest index among equal values)
 __device__ __forceinline__ void top1_push(Partial& p, float x, int idx) {
   const bool up = x > p.t1;
@@ -65,6 +71,12 @@ __global__ __launch_bounds__(NT) void k_combine_part(
     dls_row_stats* __restrict__ out_stats, float* __restrict__ norm_out) {
   constexpr int N = Chunk<T>::N;
   constexpr int NU = N * kUnroll;   // entries per thread and iteration
+  // Workgroups of 256 threads (four per CU from 1024 rows on) run a software pipeline: the
+  // next iteration's chunks are in flight while this one is folded (indices past the range
+  // clamped to its last chunk: loaded, never folded).  With row statistics they also skip the
+  // top-two pushes of iterations whose entries all lie below the wave's threshold.  The one
+  // 1024-thread workgroup per row of 256 to 1023 rows measured faster without either.
+  constexpr bool kPipe = NT < 1024;
   __shared__ Partial sh[NT / 64];
   const int row = blockIdx.x, part = blockIdx.y, parts = gridDim.y;
   const T* Lr = L + (size_t)row * V;
@@ -79,14 +91,30 @@ __global__ __launch_bounds__(NT) void k_combine_part(
   if (STATS) P.L.m = P.S.m = P.F.m = kFinMin;   // the finite start of the folds below
   if (part == 0 && t < h0) fold_scalar<T, PRIOR, STATS, WLONG>(P, Lr, Sr, prior, t, wl, al, be);
 
-  for (int c = c0 + t; c < c1; c += NT * kUnroll) {
-    uint4 ra[kUnroll], rb[kUnroll];
+  const int clast = c1 > c0 ? c1 - 1 : c0;
+  uint4 ra[kUnroll], rb[kUnroll];
+  if (kPipe && c1 > c0) {
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int cc = c + u * NT;
-      if (cc < c1) {
-        ra[u] = stream_load16(Lr + h0 + (size_t)cc * N);
-        rb[u] = stream_load16(Sr + h0 + (size_t)cc * N);
+      const int cc = min(c0 + t + u * NT, clast);
+      ra[u] = stream_load16(Lr + h0 + (size_t)cc * N);
+      rb[u] = stream_load16(Sr + h0 + (size_t)cc * N);
+    }
+  }
+  // Top two: an entry below wthr, the largest second value among the wave's lanes (so two
+  // entries of the row at least that large), can be neither of the row's top two.
+  float wthr = -INFINITY;
+  for (int c = c0 + t; c < c1; c += NT * kUnroll) {
+    uint4 na[kUnroll], nb[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      if (kPipe) {
+        const int cc = min(c + NT * kUnroll + u * NT, clast);
+        na[u] = stream_load16(Lr + h0 + (size_t)cc * N);
+        nb[u] = stream_load16(Sr + h0 + (size_t)cc * N);
+      } else if (c + u * NT < c1) {
+        ra[u] = stream_load16(Lr + h0 + (size_t)(c + u * NT) * N);
+        rb[u] = stream_load16(Sr + h0 + (size_t)(c + u * NT) * N);
       }
     }
     if (STATS && c + (kUnroll - 1) * NT < c1) {
@@ -111,11 +139,17 @@ __global__ __launch_bounds__(NT) void k_combine_part(
       lse_fold_fin<NU>(P.L, a, ma);
       lse_fold_fin<NU>(P.S, b, mb);
       lse_fold_fin<NU>(P.F, f, mf);
+      const bool hit = !kPipe || mf >= wthr;
+      if (!kPipe || __builtin_amdgcn_ballot_w64(hit)) {
+        if (hit) {
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int v0 = h0 + (c + u * NT) * N;
+          for (int u = 0; u < kUnroll; ++u) {
+            const int v0 = h0 + (c + u * NT) * N;
 #pragma unroll
-        for (int i = 0; i < N; ++i) top2_push(P, f[u * N + i], v0 + i);
+            for (int i = 0; i < N; ++i) top2_push(P, f[u * N + i], v0 + i);
+          }
+        }
+        if (kPipe) wthr = wave_max(P.t2);
       }
     } else if (STATS) {
       // the last, partial iteration: chunk by chunk
@@ -155,6 +189,13 @@ __global__ __launch_bounds__(NT) void k_combine_part(
 #pragma unroll
           for (int i = 0; i < N; ++i) top1_push(P, fuse1<PRIOR, WLONG>(a[i], b[i], PRIOR ? prior[v0 + i] : 0.f, wl, al, be), v0 + i);
         }
+      }
+    }
+    if (kPipe) {
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        ra[u] = na[u];
+        rb[u] = nb[u];
       }
     }
   }

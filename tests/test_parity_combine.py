@@ -80,6 +80,32 @@ def test_combine_weights_and_prior(wl, al, be):
         assert np.array_equal(tok, want)
 
 
+@pytest.mark.parametrize("rows,dtype", [(8, "f32"), (1024, "f32"), (1024, "bf16")])
+def test_combine_leaders_anywhere(rows, dtype):
+    """The row's two largest fused values at the start, at the end, in ascending and descending
+    rows: the 256-thread kernel skips the top-two pushes of iterations below its wave threshold,
+    and must still keep both leaders (and the gap between them) wherever they lie."""
+    V = 40000
+    g = np.random.default_rng(50 + rows)
+    L = g.normal(0, 1, (rows, V)).astype(np.float32)
+    S = g.normal(0, 1, (rows, V)).astype(np.float32)
+    for i in range(rows):
+        k = i % 5
+        if k == 0:
+            L[i] = np.sort(L[i])               # ascending: the threshold rises to the very end
+        elif k == 1:
+            L[i] = np.sort(L[i])[::-1]         # descending: leaders first, nearly all skipped after
+        elif k == 2:
+            L[i, -2:] = [7.0, 6.5]             # both leaders in the last chunk
+        elif k == 3:
+            L[i, :2] = [7.0, 6.5]              # both leaders in the first chunk
+        else:
+            L[i, [3, V - 3]] = [7.0, 7.0]      # equal long leaders far apart: the short logits decide
+    if dtype == "bf16":
+        L, S = W.Bf16Array.from_f32(L), W.Bf16Array.from_f32(S)
+    _check(L, S, None, 1.0, 0.5, 0.0)
+
+
 def test_combine_exact_ties_lowest_index():
     """Equal fused values: the lowest index wins, bit-exactly (alpha = 0 keeps l = l_L exact)."""
     rows, V = 12, 30000
