@@ -18,7 +18,7 @@ namespace dls {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kUnroll = 4;
+constexpr int kUnroll = 2;
 constexpr float kEntEmpty = -2.0e38f;   // m before the first finite entry (finite: no inf - inf)
 constexpr float kDMin = -1.0e30f;       // rescale offsets below this have exp(d) = 0 anyway
 
@@ -111,13 +111,19 @@ __global__ __launch_bounds__(kThreads) void k_unc_part(const T* __restrict__ L, 
     const float x = to_f32(Lr[t]);
     ent_fold<1>(a, &x, x);
   }
-  for (int c = c0 + t; c < c1; c += kThreads * kUnroll) {
-    uint4 raw[kUnroll];
+  // software pipeline: the next iteration's chunks are in flight while this one is folded
+  // (indices past the range clamped to its last chunk: loaded, never folded)
+  const int clast = c1 > c0 ? c1 - 1 : c0;
+  uint4 raw[kUnroll];
+  if (c1 > c0) {
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int cc = c + u * kThreads;
-      if (cc < c1) raw[u] = stream_load16(Lr + h0 + (size_t)cc * N);
-    }
+    for (int u = 0; u < kUnroll; ++u) raw[u] = stream_load16(Lr + h0 + (size_t)min(c0 + t + u * kThreads, clast) * N);
+  }
+  for (int c = c0 + t; c < c1; c += kThreads * kUnroll) {
+    uint4 nraw[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+      nraw[u] = stream_load16(Lr + h0 + (size_t)min(c + kThreads * kUnroll + u * kThreads, clast) * N);
     if (c + (kUnroll - 1) * kThreads < c1) {   // every chunk in range: one rescale for all of them
       float x[N * kUnroll];
 #pragma unroll
@@ -140,6 +146,8 @@ __global__ __launch_bounds__(kThreads) void k_unc_part(const T* __restrict__ L, 
         }
       }
     }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) raw[u] = nraw[u];
   }
   if (part == parts - 1 && t < V - tail0) {
     const float x = to_f32(Lr[tail0 + t]);
@@ -179,8 +187,9 @@ __global__ __launch_bounds__(64) void k_unc_merge(const float4* __restrict__ par
 }  // namespace
 
 int uncertainty_parts(int64_t rows, int32_t V) {
-  // about eight workgroups per CU when rows are few; each range >= 4096 entries
-  const int64_t target = 2048;
+  // about four workgroups per CU when rows are few (from 1024 rows on one per row, no merge
+  // launch); each range >= 4096 entries
+  const int64_t target = 1024;
   int64_t p = (target + rows - 1) / std::max<int64_t>(rows, 1);
   p = std::min<int64_t>(p, std::max<int64_t>(1, V / 4096));
   return (int)std::max<int64_t>(1, std::min<int64_t>(p, 128));
