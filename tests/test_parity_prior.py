@@ -17,6 +17,8 @@ pytestmark = pytest.mark.gpu
     (0, 1000, 1.0, 82),                      # no tokens: the uniform prior
     (777, 1, 1.0, 83),                       # a single-token vocabulary
     (4_000_000, 256, 1.0, 84),               # heavy contention on few counters
+    (50_000, 100_000, 0.5, 86),              # three vocabulary slices, fewer chunks than XCDs
+    (1_000_000, 400_000, 1.0, 85),           # too many slices: the cached counter
 ])
 def test_unigram_prior(n, V, smoothing, seed):
     g = np.random.default_rng(seed)
@@ -44,9 +46,9 @@ def test_unigram_prior(n, V, smoothing, seed):
 
 @pytest.mark.parametrize("kind", ["uniform", "constant", "two_hot"])
 def test_unigram_prior_adversarial_streams(kind):
-    """Streams that defeat the per-workgroup LDS caches: uniform ids over the Qwen3 vocabulary
-    (most tokens fall back to device atomics), one id repeated (every increment hits one slot)
-    and two ids sharing a hash neighbourhood, interleaved."""
+    """Streams that stress the counters: uniform ids over the Qwen3 vocabulary (every counter of
+    every slice touched, and every device count flushed by every chunk), one id repeated (every
+    increment hits one LDS counter) and two adjacent ids, interleaved."""
     V = W.QWEN3_VOCAB
     g = np.random.default_rng(91)
     if kind == "uniform":
