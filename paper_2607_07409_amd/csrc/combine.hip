@@ -102,7 +102,10 @@ __global__ __launch_bounds__(NT) void k_combine_part(
     }
   }
   // Top two: an entry below wthr, the largest second value among the wave's lanes (so two
-  // entries of the row at least that large), can be neither of the row's top two.
+  // entries of the row at least that large), can be neither of the row's top two.  The
+  // threshold is reduced over all 64 lanes; a full iteration runs with part of a wave inactive
+  // only as that wave's last full iteration (the lanes of a wave start at most 63 chunks apart
+  // and advance together by NT x kUnroll chunks), so a threshold formed then is never used.
   float wthr = -INFINITY;
   for (int c = c0 + t; c < c1; c += NT * kUnroll) {
     uint4 na[kUnroll], nb[kUnroll];
