@@ -379,16 +379,16 @@ namespace {
 // let the compiler sink each load into it and wait for each one in turn.
 __device__ __forceinline__ void copy_to_lds(uint4* dst, const uint4* src, int n) {
   for (int base = 0; base < n; base += kT * 8) {
-    uint4 v[8];
+    u32x4 v[8];   // (a uint4 array here was kept in scratch memory)
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
       const int i = base + m * kT + (int)threadIdx.x;
-      v[m] = src[i < n ? i : n - 1];
+      v[m] = *(const u32x4*)(src + (i < n ? i : n - 1));
     }
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
       const int i = base + m * kT + (int)threadIdx.x;
-      dst[i < n ? i : n - 1] = v[m];
+      *(u32x4*)(dst + (i < n ? i : n - 1)) = v[m];
     }
   }
 }
