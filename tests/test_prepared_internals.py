@@ -45,12 +45,28 @@ def test_folded_input_table(prob):
     T = head.prepared[off_T:off_T + V * 3 * H * 4].view(torch.float32).view(V, 3 * H).cpu().numpy()
     emb = np.asarray(hw.emb, np.float64)
     wih = np.asarray(hw.w_ih, np.float64)
-    toks = [0, 1, 17, 2500, V - 1]
+    toks = np.arange(V)                        # every row: all row blocks, the ragged last one
     want = emb[toks] @ wih.T
     # float32 accumulation of exact products: |error| <= d * 2^-24 * sum |products| (plus slack)
     bound = D * 2.0 ** -24 * (np.abs(emb[toks]) @ np.abs(wih).T) + 1e-30
     err = np.abs(T[toks] - want)
     assert np.all(err <= 4 * bound), (err / bound).max()
+
+
+@pytest.mark.parametrize("v,d,h", [(77, 8, 32), (300, 200, 96), (1000, 520, 160)])
+def test_folded_input_table_shapes(v, d, h):
+    """The fold's GEMM tiles (128 x 128 blocks, K steps of 64) at shapes that leave every edge
+    ragged: rows past V, columns past 3H and K past d must read as zeros."""
+    wl = W.WORKLOADS["qwen3-8b-b16"].with_(V=v, d=d, H=h, r=32, B=1, batch=1, dtype="bf16")
+    hw = W.make_head(wl, "stress")
+    head = B.LocalHead.from_weights(hw).prepare()
+    torch.cuda.synchronize()
+    T = head.prepared[256:256 + v * 3 * h * 4].view(torch.float32).view(v, 3 * h).cpu().numpy()
+    emb = np.asarray(hw.emb, np.float64)
+    wih = np.asarray(hw.w_ih, np.float64)
+    want = emb @ wih.T
+    bound = d * 2.0 ** -24 * (np.abs(emb) @ np.abs(wih).T) + 1e-30
+    assert np.all(np.abs(T - want) <= 4 * bound), (np.abs(T - want) / bound).max()
 
 
 def test_operand_order_copies(prob):
