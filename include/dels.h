@@ -390,7 +390,8 @@ dls_status dls_unigram_log_prior(const int32_t *tokens, int64_t n, int32_t V, fl
  *   two, exact in bf16), so out[t] (one float per thread, groups * 256 of them) is
  *   exactly iters * 1024 * x^2 (the iteration limit keeps every partial sum below 2^24
  *   units of 16 x^2).
- *   Limits: 1 <= groups <= 65536, 1 <= iters <= 2^18; x a power of two in [2^-20, 1].
+ *   Limits: 1 <= groups <= 65536, 1 <= iters <= 2^18, groups * iters <= 2^24 (at most
+ *   8.8 TFLOP, a few milliseconds); x a power of two in [2^-20, 1].
  * Errors: DLS_ERR_ARG for NULL or misaligned pointers, DLS_ERR_SHAPE for sizes outside
  * the limits, DLS_ERR_DEVICE without a device. */
 #define DLS_MEASURE_READ_WORDS 8192

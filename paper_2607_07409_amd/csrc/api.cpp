@@ -644,6 +644,8 @@ dls_status dls_measure_mfma(int32_t groups, int32_t iters, float x, float* out, 
   clear_error();
   if (groups < 1 || groups > 65536) return fail(DLS_ERR_SHAPE, "groups=%d outside [1, 65536]", groups);
   if (iters < 1 || iters > (1 << 18)) return fail(DLS_ERR_SHAPE, "iters=%d outside [1, 2^18]", iters);
+  if ((int64_t)groups * iters > ((int64_t)1 << 24))
+    return fail(DLS_ERR_SHAPE, "groups x iters = %lld above 2^24", (long long)groups * iters);
   int ex = 0;
   if (!std::isfinite(x) || std::frexp(x, &ex) != 0.5f || ex < -19 || ex > 1)
     return fail(DLS_ERR_ARG, "x must be a power of two in [2^-20, 1]");

@@ -406,6 +406,7 @@ def test_measure_helpers_reject_bad_arguments():
     assert mf(g=65537) == "DLS_ERR_SHAPE"
     assert mf(it=0) == "DLS_ERR_SHAPE"
     assert mf(it=(1 << 18) + 1) == "DLS_ERR_SHAPE"
+    assert mf(g=65536, it=1 << 18) == "DLS_ERR_SHAPE"          # groups x iters above 2^24
     for x in (0.0, 0.75, 2.0, 2.0 ** -21, -0.5, float("nan"), float("inf")):
         assert mf(x=x) == "DLS_ERR_ARG", x
     assert mf(out=None) == "DLS_ERR_ARG"
@@ -413,4 +414,4 @@ def test_measure_helpers_reject_bad_arguments():
     if not HAS_GPU:
         assert rd() == "DLS_ERR_DEVICE"
         for x in (1.0, 2.0 ** -20, 0.5):
-            assert mf(x=x, it=1 << 18, g=65536) == "DLS_ERR_DEVICE", x
+            assert mf(x=x, it=1 << 18, g=64) == "DLS_ERR_DEVICE", x
