@@ -106,6 +106,18 @@ def test_combine_leaders_anywhere(rows, dtype):
     _check(L, S, None, 1.0, 0.5, 0.0)
 
 
+@pytest.mark.parametrize("rows,V", [(8, 40000 + 8 * 37), (1024, 30000 + 8 * 13), (5, 1000)])
+def test_combine_all_negative_rows(rows, V):
+    """Rows whose fused values are all far below zero, at lengths that leave a ragged last
+    iteration: the top-two threshold of a wave must come only from its own lanes' values (a
+    threshold of 0 from anywhere else would skip every entry of such a row)."""
+    g = np.random.default_rng(60 + rows)
+    L = (g.normal(0, 1, (rows, V)) - 200.0).astype(np.float32)
+    S = (g.normal(0, 1, (rows, V)) - 100.0).astype(np.float32)
+    _check(L, S, None, 1.0, 0.5, 0.0)
+    _check(W.Bf16Array.from_f32(L), W.Bf16Array.from_f32(S), None, 1.0, 0.5, 0.0)
+
+
 def test_combine_exact_ties_lowest_index():
     """Equal fused values: the lowest index wins, bit-exactly (alpha = 0 keeps l = l_L exact)."""
     rows, V = 12, 30000
